@@ -1,0 +1,185 @@
+/*
+ * convbwd — convolution backward pass with ReLU-derived sparsity on AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The operations are those of "Exploiting Activation based Gradient Output
+ * Sparsity to Accelerate Backpropagation in CNNs" (arXiv 2109.07710):
+ *
+ *   - the data gradient dX = conv_transpose(dY, W), computed only where the
+ *     forward ReLU footprint of X is live (output sparsity, Sec. III-B: the
+ *     ReLU derivative multiplies the gradient by 1 or 0, so the outputs it
+ *     will zero are known from the forward pass) and written as exact +0.0
+ *     everywhere else;
+ *   - the weight gradient dW = X (star) dY, skipping blocks of dY that are
+ *     entirely zero (input sparsity of the incoming gradient, Sec. III-B and
+ *     the weight-gradient phase of Sec. IV-B);
+ *   - a dense data gradient on the same kernel (the paper's dense-compute
+ *     baseline "DC", Sec. VI).
+ *
+ * Layer notation follows Sec. II-A / Sec. IV-B: an input [C,H,W] is mapped
+ * by filters [M,C,R,S] to an output [M,U,V]; here M is K and [U,V] is [P,Q],
+ * with P = (H + 2*pad_h - R)/stride_h + 1 (floor), likewise Q.  Convolution is
+ * cross-correlation with zero padding:
+ *
+ *   Y[n,k,p,q]  = sum_{c,r,s} X[n,c,p*sh-ph+r, q*sw-pw+s] W[k,c,r,s]
+ *   dX[n,c,h,w] = mask[n,c,h,w] ? sum_{k,r,s : aligned, in range} dY[n,k,p,q] W[k,c,r,s] : +0.0
+ *   dW[k,c,r,s] = sum_{n,p,q} dY[n,k,p,q] X[n,c,p*sh-ph+r, q*sw-pw+s]
+ *
+ * where mask = (X > 0), X being this layer's input, i.e. the output of the
+ * preceding ReLU.
+ *
+ * Conventions for every entry point:
+ *   - Tensor, mask and workspace pointers are DEVICE memory owned by the
+ *     caller and must stay valid until the work queued on `stream` finishes.
+ *     The library never allocates device memory and keeps no per-call state.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     All work is queued on it; no entry point synchronizes the device, except
+ *     cbw_read_stats, which waits for `stream`.
+ *   - Every argument is validated before anything is launched.  On an error
+ *     nothing is launched and no output is touched.  No exception or abort
+ *     crosses this interface.
+ *   - Calls that share a workspace or an output and overlap in time race.
+ */
+#ifndef CONVBWD_H
+#define CONVBWD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CBW_OK = 0,
+    CBW_ERR_INVALID_ARG = -1,  /* null pointer, non-positive size, inconsistent P/Q */
+    CBW_ERR_UNSUPPORTED = -2,  /* valid but not implemented: layout, channel counts
+                                  not a multiple of the 16-byte vector, misaligned
+                                  pointer, tensor of 2^31 elements or more */
+    CBW_ERR_WORKSPACE = -3,    /* workspace missing or smaller than cbw_workspace_size */
+    CBW_ERR_HIP = -4           /* a HIP launch or copy failed (sticky error cleared) */
+} cbw_status;
+
+/* Activation layout of X, dX, Y, dY.  Channel-innermost (NHWC) is the native
+ * one: the paper stores neurons "channel first" and indexes non-zeros through
+ * the channel dimension 32 at a time (Sec. IV-B). */
+typedef enum { CBW_NCHW = 0, CBW_NHWC = 1 } cbw_act_layout;
+/* Filter layout of W and dW. */
+typedef enum { CBW_KCRS = 0, CBW_KRSC = 1 } cbw_w_layout;
+/* Element type of X, W, dY and dX.  dW is always float32. */
+typedef enum { CBW_F32 = 0, CBW_BF16 = 1 } cbw_dtype;
+
+typedef struct {
+    int32_t N, C, H, W;      /* batch, input channels, input height, width     */
+    int32_t K, R, S;         /* output channels (the paper's M), filter size   */
+    int32_t P, Q;            /* output height, width; must equal the formula   */
+    int32_t stride_h, stride_w, pad_h, pad_w;
+    int32_t act_layout;      /* cbw_act_layout; only CBW_NHWC is implemented   */
+    int32_t w_layout;        /* cbw_w_layout; both implemented                 */
+    int32_t dtype;           /* cbw_dtype                                      */
+} cbw_conv_desc;
+
+/* Operation selector for cbw_workspace_size / cbw_read_stats. */
+enum { CBW_OP_BWD_DATA = 0, CBW_OP_BWD_DATA_MASKED = 1, CBW_OP_BWD_WEIGHT = 2 };
+
+/* Flags. CBW_FLAG_NO_SKIP runs the same kernels with every skip disabled:
+ * the masked data gradient computes all rows and applies the mask in its
+ * epilogue; the weight gradient processes every dY block. */
+#define CBW_FLAG_NO_SKIP 1u
+
+/* Execution statistics written by the kernels into the workspace. */
+typedef struct {
+    int64_t rows_total;      /* GEMM rows (pixel x channel-group) the dense path would compute */
+    int64_t rows_live;       /* rows actually computed                                        */
+    int64_t blocks_total;    /* dW (pixel-chunk x k-tile) blocks                               */
+    int64_t blocks_skipped;  /* dW blocks skipped because dY was all zero there                 */
+} cbw_stats;
+
+/* Human-readable name of a cbw_status value (static storage). */
+const char* cbw_status_string(int status);
+
+/* Host-only check of a descriptor (no GPU needed).  Returns CBW_OK,
+ * CBW_ERR_INVALID_ARG or CBW_ERR_UNSUPPORTED. */
+int cbw_validate_desc(const cbw_conv_desc* desc);
+
+/* Number of 32-bit words of the packed X footprint, ceil(N*C*H*W/32), and of
+ * a packed dY footprint, ceil(N*K*P*Q/32).  0 for an invalid descriptor. */
+size_t cbw_mask_words(const cbw_conv_desc* desc);
+size_t cbw_dy_mask_words(const cbw_conv_desc* desc);
+
+/* Workspace bytes needed by `op` for this descriptor (host only; depends on
+ * the descriptor alone).  Returns a cbw_status; *bytes is set on success. */
+int cbw_workspace_size(const cbw_conv_desc* desc, int op, size_t* bytes);
+
+/* ReLU footprint bitmap of X (Sec. III-B boxed derivative, read as the ReLU
+ * output footprint: live iff X > 0; Sec. IV-B: the output bitmap the forward
+ * pass leaves in memory for the backward pass).  Bit i of word i/32 (LSB
+ * first) is element i of X in X's own linear (NHWC) order; trailing bits of
+ * the last word are 0.  x_mask: cbw_mask_words(desc) words. */
+int cbw_relu_mask_pack(const cbw_conv_desc* desc, const void* X, uint32_t* x_mask, void* stream);
+
+/* Non-zero bitmap of any tensor of `count` elements of type `dtype` (bit =
+ * value != 0; +0.0 and -0.0 are zero), same bit order.  Used for the dY
+ * footprint that lets the weight gradient skip all-zero blocks. */
+int cbw_nonzero_mask_pack(int32_t dtype, int64_t count, const void* t, uint32_t* bits, void* stream);
+
+/* Dense data gradient (Sec. IV-B, the backward pass as the forward operation
+ * with M and C interchanged): dX[N,H,W,C] from dY[N,P,Q,K] and W (KRSC or
+ * KCRS).  Workspace: cbw_workspace_size(desc, CBW_OP_BWD_DATA). */
+int conv_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, void* dX,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* Masked data gradient (output sparsity, Sec. III-B; output-bitmap-driven
+ * address generation, Sec. IV-B): only outputs whose x_mask bit is set are
+ * computed; all others are written as +0.0 (bit pattern 0).  x_mask is the
+ * packed footprint of X (cbw_relu_mask_pack).  The footprint is compacted per
+ * channel group into ascending lists of live pixels and the GEMM runs only
+ * over those rows; flags = CBW_FLAG_NO_SKIP computes every row instead.
+ * Workspace: cbw_workspace_size(desc, CBW_OP_BWD_DATA_MASKED). */
+int conv_bwd_data_masked(const cbw_conv_desc* desc, const void* dY, const void* W,
+                         const uint32_t* x_mask, void* dX,
+                         void* workspace, size_t workspace_bytes, uint32_t flags, void* stream);
+
+/* Weight gradient with input sparsity (Sec. III-B; weight-gradient phase of
+ * Sec. IV-B): dW (float32, layout desc->w_layout) from X[N,H,W,C] and
+ * dY[N,P,Q,K].  Blocks of (pixel chunk x output-channel tile) in which dY is
+ * entirely zero are skipped; the skipped products are exactly zero.  dy_mask
+ * (nullable) is a packed dY footprint (cbw_nonzero_mask_pack or the next
+ * layer's ReLU bitmap, any superset of dY's non-zeros); when NULL the
+ * occupancy is read from dY itself.  The result is deterministic: partial
+ * sums are reduced in a fixed order.  dW is fully overwritten.
+ * Workspace: cbw_workspace_size(desc, CBW_OP_BWD_WEIGHT). */
+int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void* dY,
+                           const uint32_t* dy_mask, float* dW,
+                           void* workspace, size_t workspace_bytes, uint32_t flags, void* stream);
+
+/* Copy the statistics of the last `op` call that used `workspace` to the host
+ * (waits for `stream`). */
+int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, size_t workspace_bytes,
+                   cbw_stats* out, void* stream);
+
+/* Inspection of the integer steps (for tests and tools; waits for `stream`).
+ *
+ * cbw_read_live_lists: after a conv_bwd_data_masked call without
+ * CBW_FLAG_NO_SKIP on `workspace`, copies the compacted footprint of channel
+ * group `group` (channels [group*G, min(C, (group+1)*G)), G = the value
+ * returned in *group_width) to the host: *count live pixels, in ascending
+ * order, into `pixels` (capacity N*H*W entries).  A pixel is listed iff at
+ * least one of its channels in the group is live (non-zero indexing of the
+ * output bitmap, Sec. IV-B).  `pixels` may be NULL to query count and width.
+ *
+ * cbw_read_occupancy: after a conv_bwd_weight_sparse call without
+ * CBW_FLAG_NO_SKIP, copies the block occupancy map occ[chunk][ktile] (uint8,
+ * 1 = dY has a non-zero in that block) to `occ` (capacity *nchunks x
+ * *ktiles, both returned; chunk = *chunk_pixels pixels of dY in N,P,Q order,
+ * ktile = *ktile_width output channels).  `occ` may be NULL to query sizes. */
+int cbw_read_live_lists(const cbw_conv_desc* desc, const void* workspace, size_t workspace_bytes, int group,
+                        int32_t* pixels, int32_t* count, int32_t* group_width, void* stream);
+int cbw_read_occupancy(const cbw_conv_desc* desc, const void* workspace, size_t workspace_bytes, uint8_t* occ,
+                       int32_t* nchunks, int32_t* ktiles, int32_t* chunk_pixels, int32_t* ktile_width,
+                       void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CONVBWD_H */

@@ -1,0 +1,342 @@
+// C-ABI entry points: validation, workspace carving and kernel launches on
+// the caller's stream.  See include/convbwd.h for the contract.
+#include <hip/hip_runtime.h>
+
+#include "../../include/convbwd.h"
+#include "kernels.hpp"
+#include "plan.hpp"
+
+using namespace cbw;
+
+namespace {
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int hip_status(hipError_t e)
+{
+    if (e == hipSuccess) return CBW_OK;
+    (void)hipGetLastError();
+    return CBW_ERR_HIP;
+}
+
+template <typename T>
+T* at(void* ws, const Region& r) { return reinterpret_cast<T*>(static_cast<char*>(ws) + r.off); }
+
+bool tiles_consistent()
+{
+    return data_tile_channels() == kDataTileC && data_tile_pixels() == kDataTileP &&
+           weight_tile_channels() == kWeightTileC && weight_tile_k() == kWeightTileK &&
+           compact_block_pixels() == kCompactBlock && weight_chunk(CBW_BF16) == weight_chunk_px(CBW_BF16) &&
+           weight_chunk(CBW_F32) == weight_chunk_px(CBW_F32);
+}
+
+int check_ws(const void* ws, size_t ws_bytes, size_t need)
+{
+    if (need > 0 && ws == nullptr) return CBW_ERR_WORKSPACE;
+    if (ws_bytes < need) return CBW_ERR_WORKSPACE;
+    if (!aligned16(ws)) return CBW_ERR_UNSUPPORTED;
+    return CBW_OK;
+}
+
+DataParams data_params(const cbw_conv_desc* d, const void* dY, const void* wt, void* dX, int64_t npix,
+                       int groups)
+{
+    DataParams p{};
+    p.dy = dY;
+    p.wt = wt;
+    p.dx = dX;
+    p.N = d->N; p.H = d->H; p.W = d->W; p.C = d->C; p.K = d->K; p.R = d->R; p.S = d->S;
+    p.P = d->P; p.Q = d->Q;
+    p.stride_h = d->stride_h; p.stride_w = d->stride_w; p.pad_h = d->pad_h; p.pad_w = d->pad_w;
+    p.npix = (int)npix;
+    p.ctiles = groups;
+    p.div_w = make_fastdiv((uint32_t)d->W);
+    p.div_h = make_fastdiv((uint32_t)d->H);
+    return p;
+}
+
+int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const uint32_t* x_mask, void* dX,
+                 void* ws, size_t ws_bytes, uint32_t flags, void* stream, bool masked)
+{
+    DataPlan plan;
+    int st = plan_data(desc, masked, &plan);
+    if (st != CBW_OK) return st;
+    if (!dY || !W || !dX || (masked && !x_mask)) return CBW_ERR_INVALID_ARG;
+    if (!aligned16(dY) || !aligned16(W) || !aligned16(dX) || (masked && ((uintptr_t)x_mask & 3u)))
+        return CBW_ERR_UNSUPPORTED;
+    if ((st = check_ws(ws, ws_bytes, plan.total)) != CBW_OK) return st;
+    if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    const bool gather = masked && !(flags & CBW_FLAG_NO_SKIP);
+    const int mode = !masked ? MODE_DENSE : (gather ? MODE_GATHER : MODE_SELECT);
+    int* header = at<int>(ws, plan.header);
+    void* wt = at<void>(ws, plan.wt);
+    hipError_t e = launch_transform_filters(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S,
+                                            desc->w_layout == CBW_KRSC, header, mode, s);
+    if (e != hipSuccess) return hip_status(e);
+
+    DataParams p = data_params(desc, dY, wt, dX, plan.npix, plan.groups);
+    p.mask = x_mask;
+    if (gather) {
+        CompactParams cp{};
+        cp.mask = x_mask;
+        cp.blk_counts = at<int32_t>(ws, plan.blk_counts);
+        cp.counts = at<int32_t>(ws, plan.counts);
+        cp.lists = at<int32_t>(ws, plan.lists);
+        cp.dx = dX;
+        cp.npix = (int)plan.npix;
+        cp.C = desc->C;
+        cp.G = kDataTileC;
+        cp.groups = plan.groups;
+        cp.nblk = plan.nblk;
+        cp.elem_bytes = elem_bytes(desc->dtype);
+        if ((e = launch_compact(cp, s)) != hipSuccess) return hip_status(e);
+        p.lists = cp.lists;
+        p.counts = cp.counts;
+    }
+    return hip_status(launch_bwd_data(desc->dtype, mode, p, s));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* cbw_status_string(int status)
+{
+    switch (status) {
+    case CBW_OK: return "ok";
+    case CBW_ERR_INVALID_ARG: return "invalid argument";
+    case CBW_ERR_UNSUPPORTED: return "unsupported configuration";
+    case CBW_ERR_WORKSPACE: return "workspace missing or too small";
+    case CBW_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+    }
+}
+
+int cbw_validate_desc(const cbw_conv_desc* desc) { return validate_desc(desc); }
+
+size_t cbw_mask_words(const cbw_conv_desc* d)
+{
+    if (validate_desc(d) != CBW_OK) return 0;
+    return (size_t)(((int64_t)d->N * d->C * d->H * d->W + 31) / 32);
+}
+
+size_t cbw_dy_mask_words(const cbw_conv_desc* d)
+{
+    if (validate_desc(d) != CBW_OK) return 0;
+    return (size_t)(((int64_t)d->N * d->K * d->P * d->Q + 31) / 32);
+}
+
+int cbw_workspace_size(const cbw_conv_desc* desc, int op, size_t* bytes)
+{
+    if (!bytes) return CBW_ERR_INVALID_ARG;
+    int st;
+    if (op == CBW_OP_BWD_DATA || op == CBW_OP_BWD_DATA_MASKED) {
+        DataPlan p;
+        if ((st = plan_data(desc, op == CBW_OP_BWD_DATA_MASKED, &p)) != CBW_OK) return st;
+        *bytes = p.total;
+        return CBW_OK;
+    }
+    if (op == CBW_OP_BWD_WEIGHT) {
+        WeightPlan p;
+        if ((st = plan_weight(desc, &p)) != CBW_OK) return st;
+        *bytes = p.total;
+        return CBW_OK;
+    }
+    return CBW_ERR_INVALID_ARG;
+}
+
+int cbw_relu_mask_pack(const cbw_conv_desc* desc, const void* X, uint32_t* x_mask, void* stream)
+{
+    int st = validate_desc(desc);
+    if (st != CBW_OK) return st;
+    if (!X || !x_mask) return CBW_ERR_INVALID_ARG;
+    if (!aligned16(X) || ((uintptr_t)x_mask & 3u)) return CBW_ERR_UNSUPPORTED;
+    const int64_t count = (int64_t)desc->N * desc->C * desc->H * desc->W;
+    return hip_status(launch_relu_mask_pack(desc->dtype, count, X, x_mask, 1, static_cast<hipStream_t>(stream)));
+}
+
+int cbw_nonzero_mask_pack(int32_t dtype, int64_t count, const void* t, uint32_t* bits, void* stream)
+{
+    if (dtype != CBW_F32 && dtype != CBW_BF16) return CBW_ERR_INVALID_ARG;
+    if (count < 0 || (count > 0 && (!t || !bits))) return CBW_ERR_INVALID_ARG;
+    if (count == 0) return CBW_OK;
+    if (!aligned16(t) || ((uintptr_t)bits & 3u)) return CBW_ERR_UNSUPPORTED;
+    return hip_status(launch_relu_mask_pack(dtype, count, t, bits, 0, static_cast<hipStream_t>(stream)));
+}
+
+int conv_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, void* dX, void* workspace,
+                  size_t workspace_bytes, void* stream)
+{
+    return run_bwd_data(desc, dY, W, nullptr, dX, workspace, workspace_bytes, 0, stream, false);
+}
+
+int conv_bwd_data_masked(const cbw_conv_desc* desc, const void* dY, const void* W, const uint32_t* x_mask,
+                         void* dX, void* workspace, size_t workspace_bytes, uint32_t flags, void* stream)
+{
+    return run_bwd_data(desc, dY, W, x_mask, dX, workspace, workspace_bytes, flags, stream, true);
+}
+
+int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void* dY, const uint32_t* dy_mask,
+                           float* dW, void* workspace, size_t workspace_bytes, uint32_t flags, void* stream)
+{
+    WeightPlan plan;
+    int st = plan_weight(desc, &plan);
+    if (st != CBW_OK) return st;
+    if (!X || !dY || !dW) return CBW_ERR_INVALID_ARG;
+    if (!aligned16(X) || !aligned16(dY) || !aligned16(dW) || ((uintptr_t)dy_mask & 3u))
+        return CBW_ERR_UNSUPPORTED;
+    if ((st = check_ws(workspace, workspace_bytes, plan.total)) != CBW_OK) return st;
+    if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool skip = !(flags & CBW_FLAG_NO_SKIP);
+    hipError_t e;
+    uint8_t* occ = at<uint8_t>(workspace, plan.occ);
+    if (skip) {
+        OccParams op{};
+        op.dy = dY;
+        op.bits = dy_mask;
+        op.occ = occ;
+        op.npq = (int)plan.npq;
+        op.K = desc->K;
+        op.chunk = weight_chunk_px(desc->dtype);
+        op.BNk = kWeightTileK;
+        op.ktiles = plan.ktiles;
+        op.nchunks = plan.nchunks;
+        op.dtype = desc->dtype;
+        if ((e = launch_occupancy(op, s)) != hipSuccess) return hip_status(e);
+    }
+    WeightParams p{};
+    p.x = X;
+    p.dy = dY;
+    p.out = plan.direct ? dW : at<float>(workspace, plan.partials);
+    p.occ = skip ? occ : nullptr;
+    p.skip_slots = at<int32_t>(workspace, plan.skip_slots);
+    p.header = at<int>(workspace, plan.header);
+    p.N = desc->N; p.H = desc->H; p.W = desc->W; p.C = desc->C; p.K = desc->K; p.R = desc->R; p.S = desc->S;
+    p.P = desc->P; p.Q = desc->Q;
+    p.stride_h = desc->stride_h; p.stride_w = desc->stride_w; p.pad_h = desc->pad_h; p.pad_w = desc->pad_w;
+    p.npq = (int)plan.npq;
+    p.nchunks = plan.nchunks;
+    p.chunks_per_split = plan.chunks_per_split;
+    p.ctiles = plan.ctiles;
+    p.ktiles = plan.ktiles;
+    p.nsplit = plan.nsplit;
+    p.mode_flags = (int)flags;
+    p.div_q = make_fastdiv((uint32_t)desc->Q);
+    p.div_p = make_fastdiv((uint32_t)desc->P);
+    if ((e = launch_bwd_weight(desc->dtype, p, s)) != hipSuccess) return hip_status(e);
+    if (!plan.direct) {
+        e = launch_splitk_reduce(p.out, dW, plan.nsplit, desc->K, desc->R * desc->S, desc->C,
+                                 desc->w_layout == CBW_KRSC, s);
+        if (e != hipSuccess) return hip_status(e);
+    }
+    return CBW_OK;
+}
+
+int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, size_t workspace_bytes,
+                   cbw_stats* out, void* stream)
+{
+    if (!out || !workspace) return CBW_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    cbw_stats r{};
+    int st;
+    if (op == CBW_OP_BWD_DATA || op == CBW_OP_BWD_DATA_MASKED) {
+        DataPlan plan;
+        if ((st = plan_data(desc, op == CBW_OP_BWD_DATA_MASKED, &plan)) != CBW_OK) return st;
+        if (workspace_bytes < plan.total) return CBW_ERR_WORKSPACE;
+        int header = 0;
+        hipError_t e = hipMemcpyAsync(&header, at<void>(const_cast<void*>(workspace), plan.header), sizeof(int),
+                                      hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_status(e);
+        r.rows_total = (int64_t)plan.groups * plan.npix;
+        r.rows_live = r.rows_total;
+        if (op == CBW_OP_BWD_DATA_MASKED && header == MODE_GATHER) {
+            int32_t counts[64];
+            int64_t live = 0;
+            for (int g0 = 0; g0 < plan.groups; g0 += 64) {
+                const int n = plan.groups - g0 < 64 ? plan.groups - g0 : 64;
+                e = hipMemcpyAsync(counts, at<int32_t>(const_cast<void*>(workspace), plan.counts) + g0,
+                                   n * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+                if (e == hipSuccess) e = hipStreamSynchronize(s);
+                if (e != hipSuccess) return hip_status(e);
+                for (int i = 0; i < n; ++i) live += counts[i];
+            }
+            r.rows_live = live;
+        }
+    } else if (op == CBW_OP_BWD_WEIGHT) {
+        WeightPlan plan;
+        if ((st = plan_weight(desc, &plan)) != CBW_OK) return st;
+        if (workspace_bytes < plan.total) return CBW_ERR_WORKSPACE;
+        r.blocks_total = (int64_t)plan.nchunks * plan.ktiles;
+        int64_t skipped = 0;
+        int32_t buf[256];
+        const int32_t* slots = at<int32_t>(const_cast<void*>(workspace), plan.skip_slots);
+        for (int i0 = 0; i0 < plan.grid; i0 += 256) {
+            const int n = plan.grid - i0 < 256 ? plan.grid - i0 : 256;
+            hipError_t e = hipMemcpyAsync(buf, slots + i0, n * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+            if (e == hipSuccess) e = hipStreamSynchronize(s);
+            if (e != hipSuccess) return hip_status(e);
+            for (int i = 0; i < n; ++i) skipped += buf[i];
+        }
+        r.blocks_skipped = skipped / ((int64_t)desc->R * desc->S * plan.ctiles);
+    } else {
+        return CBW_ERR_INVALID_ARG;
+    }
+    *out = r;
+    return CBW_OK;
+}
+
+int cbw_read_live_lists(const cbw_conv_desc* desc, const void* workspace, size_t workspace_bytes, int group,
+                        int32_t* pixels, int32_t* count, int32_t* group_width, void* stream)
+{
+    DataPlan plan;
+    int st = plan_data(desc, true, &plan);
+    if (st != CBW_OK) return st;
+    if (!workspace || !count || !group_width || group < 0 || group >= plan.groups) return CBW_ERR_INVALID_ARG;
+    if (workspace_bytes < plan.total) return CBW_ERR_WORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void* ws = const_cast<void*>(workspace);
+    int32_t n = 0;
+    hipError_t e = hipMemcpyAsync(&n, at<int32_t>(ws, plan.counts) + group, sizeof(int32_t),
+                                  hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_status(e);
+    if (n < 0 || n > plan.npix) return CBW_ERR_INVALID_ARG;  // workspace not written by a gather call
+    *count = n;
+    *group_width = kDataTileC;
+    if (pixels && n > 0) {
+        e = hipMemcpyAsync(pixels, at<int32_t>(ws, plan.lists) + (int64_t)group * plan.npix,
+                           (size_t)n * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_status(e);
+    }
+    return CBW_OK;
+}
+
+int cbw_read_occupancy(const cbw_conv_desc* desc, const void* workspace, size_t workspace_bytes, uint8_t* occ,
+                       int32_t* nchunks, int32_t* ktiles, int32_t* chunk_pixels, int32_t* ktile_width,
+                       void* stream)
+{
+    WeightPlan plan;
+    int st = plan_weight(desc, &plan);
+    if (st != CBW_OK) return st;
+    if (!workspace || !nchunks || !ktiles || !chunk_pixels || !ktile_width) return CBW_ERR_INVALID_ARG;
+    if (workspace_bytes < plan.total) return CBW_ERR_WORKSPACE;
+    *nchunks = plan.nchunks;
+    *ktiles = plan.ktiles;
+    *chunk_pixels = weight_chunk_px(desc->dtype);
+    *ktile_width = kWeightTileK;
+    if (occ) {
+        hipStream_t s = static_cast<hipStream_t>(stream);
+        hipError_t e = hipMemcpyAsync(occ, at<uint8_t>(const_cast<void*>(workspace), plan.occ),
+                                      (size_t)plan.nchunks * plan.ktiles, hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_status(e);
+    }
+    return CBW_OK;
+}
+
+}  // extern "C"

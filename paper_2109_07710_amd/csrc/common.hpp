@@ -1,0 +1,95 @@
+// Shared device helpers for the gfx950 kernels: element traits, bf16
+// rounding, fast integer division, MFMA wrappers and the LDS swizzle.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cbw {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// Element traits.  bf16 is stored as its 16-bit pattern.  A "vector" is 16
+// bytes: E elements.  One MFMA "chunk step" consumes one 16-byte fragment of
+// A and of B per lane and reduces 4*E elements of the reduction dimension
+// (the four 16-lane groups each hold E consecutive reduction indices).
+template <typename T> struct Elem;
+template <> struct Elem<uint16_t> { static constexpr int E = 8; };
+template <> struct Elem<float> { static constexpr int E = 4; };
+
+__device__ __forceinline__ floatx4 mfma_chunk(floatx4 acc, const uint4& a, const uint4& b, uint16_t)
+{
+    // 16x16x32 bf16 -> fp32.  Lane l supplies row (l % 16) of A and column
+    // (l % 16) of B, with the same 8 reduction indices for both; the result
+    // holds rows 4*(l/16)+v, v = 0..3, of column l % 16.
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                    __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ floatx4 mfma_chunk(floatx4 acc, const uint4& a, const uint4& b, float)
+{
+    // Four 16x16x4 fp32 MFMAs.  In MFMA j a lane supplies element j of its
+    // fragment for both A and B, so the four reduction indices a lane group
+    // covers are the same on both sides; the sum over all of them is the
+    // full product whatever index each lane is assigned.
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+    return acc;
+}
+
+// fp32 -> bf16 bit pattern, round to nearest, ties to even; NaN stays NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+// Unsigned division by a runtime constant d (1 <= d < 2^31) for numerators
+// below 2^31: q = (mulhi(n, m) + n) >> s with s = ceil(log2 d) and
+// m = floor(2^32 (2^s - d) / d) + 1 (Granlund & Montgomery, 1994).
+struct FastDiv {
+    uint32_t d, m, s;
+};
+
+inline FastDiv make_fastdiv(uint32_t d)
+{
+    FastDiv f;
+    f.d = d;
+    uint32_t s = 0;
+    while ((1ull << s) < d) ++s;
+    f.s = s;
+    f.m = (uint32_t)(((1ull << 32) * ((1ull << s) - d)) / d + 1);
+    return f;
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f)
+{
+    return (__umulhi(n, f.m) + n) >> f.s;
+}
+
+// XCD-aware block order.  The dispatcher hands consecutive workgroups to the
+// eight XCDs in turn; this maps the j-th workgroup an XCD receives to the
+// j-th tile of a contiguous range owned by that XCD, so tiles that share
+// operands share one L2.  A bijection on [0, nb) for any nb.
+__device__ __forceinline__ int xcd_remap(int b, int nb)
+{
+    const int xcd = b & 7, j = b >> 3;
+    const int per = nb >> 3, rem = nb & 7;
+    return xcd * per + (xcd < rem ? xcd : rem) + j;
+}
+
+// Swizzle of a 16-byte chunk inside a 256-byte LDS row (16 chunks).  Chosen
+// so that sixteen consecutive rows read at one logical chunk, and rows
+// 8c + j for c = 0..15 written at one logical chunk, fall on sixteen
+// different chunk positions.
+__device__ __forceinline__ int swz16(int row)
+{
+    return (row & 15) ^ ((row >> 4) & 7);
+}
+
+}  // namespace cbw

@@ -1,0 +1,78 @@
+// Launch interfaces between the host dispatcher (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace cbw {
+
+enum { MODE_DENSE = 0, MODE_SELECT = 1, MODE_GATHER = 2 };
+
+struct DataParams {
+    const void* dy;          // [N*P*Q][K]
+    const void* wt;          // [R*S][C][K]
+    void* dx;                // [N*H*W][C]
+    const uint32_t* mask;    // packed footprint of X (select / gather)
+    const int32_t* lists;    // [groups][npix] live pixels (gather)
+    const int32_t* counts;   // [groups] live-pixel counts (gather)
+    int N, H, W, C, K, R, S, P, Q;
+    int stride_h, stride_w, pad_h, pad_w;
+    int npix;                // N*H*W
+    int ctiles;              // channel tiles = compaction groups
+    FastDiv div_w, div_h;    // pixel -> (n, h, w)
+};
+
+struct CompactParams {
+    const uint32_t* mask;    // packed footprint, NHWC bit order
+    int32_t* blk_counts;     // [groups][nblk]
+    int32_t* counts;         // [groups]
+    int32_t* lists;          // [groups][npix]
+    void* dx;                // zero-filled at (pixel, group) rows dead for the whole group
+    int npix, C, G, groups, nblk, elem_bytes;
+};
+
+struct WeightParams {
+    const void* x;           // [N*H*W][C]
+    const void* dy;          // [N*P*Q][K]
+    float* out;              // [nsplit][K][R*S][C] partials, or dW (KRSC) when nsplit == 1
+    const uint8_t* occ;      // [nchunks][ktiles] block occupancy, or null (no skipping)
+    int32_t* skip_slots;     // [grid] skipped-block count per workgroup
+    int* header;
+    int N, H, W, C, K, R, S, P, Q;
+    int stride_h, stride_w, pad_h, pad_w;
+    int npq;                 // N*P*Q
+    int nchunks;             // ceil(npq / chunk)
+    int chunks_per_split;
+    int ctiles, ktiles, nsplit;
+    int mode_flags;
+    FastDiv div_q, div_p;    // pixel -> (n, p, q)
+};
+
+struct OccParams {
+    const void* dy;          // values [npq][K] (used when bits == null)
+    const uint32_t* bits;    // packed dY footprint, or null
+    uint8_t* occ;            // [nchunks][ktiles]
+    int npq, K, chunk, BNk, ktiles, nchunks, dtype;
+};
+
+int data_tile_channels();
+int data_tile_pixels();
+int weight_tile_channels();
+int weight_tile_k();
+int weight_chunk(int dtype);
+int compact_block_pixels();
+
+hipError_t launch_transform_filters(int dtype, const void* w, void* wt, int K, int C, int RS, int krsc,
+                                    int* header, int mode, hipStream_t stream);
+hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream);
+hipError_t launch_compact(const CompactParams& p, hipStream_t stream);
+hipError_t launch_relu_mask_pack(int dtype, int64_t count, const void* x, uint32_t* bits, int relu,
+                                 hipStream_t stream);
+hipError_t launch_occupancy(const OccParams& p, hipStream_t stream);
+hipError_t launch_bwd_weight(int dtype, const WeightParams& p, hipStream_t stream);
+hipError_t launch_splitk_reduce(const float* part, float* dw, int nsplit, int K, int RS, int C, int krsc,
+                                hipStream_t stream);
+
+}  // namespace cbw

@@ -1,0 +1,281 @@
+// Integer kernels around the GEMMs: footprint bitmaps, per-group compaction
+// of live pixels, dY block occupancy and the split-K reduction of dW.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace cbw {
+
+namespace {
+
+constexpr int CNT = 256;                 // threads per compaction block
+constexpr int PX_PER_THREAD = 4;
+constexpr int BLK_PX = CNT * PX_PER_THREAD;
+
+// Any bit set in the bit range [lo, hi) of a packed bitmap.
+__device__ __forceinline__ bool any_bits(const uint32_t* __restrict__ bits, int64_t lo, int64_t hi)
+{
+    if (lo >= hi) return false;
+    int64_t w0 = lo >> 5, w1 = (hi - 1) >> 5;
+    uint32_t acc = 0;
+    for (int64_t w = w0; w <= w1; ++w) {
+        uint32_t v = bits[w];
+        if (w == w0) v &= 0xffffffffu << (lo & 31);
+        if (w == w1) {
+            const int top = (int)((hi - 1) & 31);
+            v &= (top == 31) ? 0xffffffffu : ((2u << top) - 1u);
+        }
+        acc |= v;
+    }
+    return acc != 0;
+}
+
+// Bit per element: relu ? (value > 0) : (value != 0), over 16-byte vectors.
+template <typename T>
+__device__ __forceinline__ uint32_t vec_bits(const uint4& v, bool relu)
+{
+    constexpr int E = Elem<T>::E;
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t b = 0;
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+        uint32_t u;
+        if (sizeof(T) == 2) u = (w[i >> 1] >> ((i & 1) * 16)) & 0xffffu;
+        else u = w[i];
+        bool on;
+        if (sizeof(T) == 2) {
+            const uint32_t mag = u & 0x7fffu;
+            on = relu ? ((u & 0x8000u) == 0 && mag != 0 && mag <= 0x7f80u) : (mag != 0);
+        } else {
+            const uint32_t mag = u & 0x7fffffffu;
+            on = relu ? ((u >> 31) == 0 && mag != 0 && mag <= 0x7f800000u) : (mag != 0);
+        }
+        b |= (on ? 1u : 0u) << i;
+    }
+    return b;
+}
+
+template <typename T>
+__device__ __forceinline__ uint32_t elem_bit(const T* p, int64_t i, bool relu)
+{
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (sizeof(T) == 2) v.x = reinterpret_cast<const uint16_t*>(p)[i];
+    else v.x = reinterpret_cast<const uint32_t*>(p)[i];
+    return vec_bits<T>(v, relu) & 1u;
+}
+
+// One thread per 16-byte vector; the E bits of L = 32/E neighbouring lanes
+// are OR-ed into one word written by the first of them.
+template <typename T>
+__global__ void mask_pack_kernel(const T* __restrict__ x, uint32_t* __restrict__ bits, int64_t count,
+                                 int64_t nvec, bool relu)
+{
+    constexpr int E = Elem<T>::E;
+    constexpr int L = 32 / E;
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    uint32_t b = 0;
+    if (v < nvec) {
+        const int64_t e0 = v * E;
+        if (e0 + E <= count) {
+            b = vec_bits<T>(*reinterpret_cast<const uint4*>(x + e0), relu);
+        } else {
+            for (int i = 0; i < E && e0 + i < count; ++i) b |= elem_bit<T>(x, e0 + i, relu) << i;
+        }
+    }
+    const int lane = threadIdx.x & 63;
+    b <<= (lane % L) * E;
+#pragma unroll
+    for (int off = 1; off < L; off <<= 1) b |= __shfl_xor(b, off);
+    if (lane % L == 0 && v < nvec) bits[v / L] = b;
+}
+
+__device__ __forceinline__ bool pixel_live(const CompactParams& p, int px, int g)
+{
+    if (px >= p.npix) return false;
+    const int64_t base = (int64_t)px * p.C;
+    const int lo = g * p.G;
+    const int hi = min(p.C, lo + p.G);
+    return any_bits(p.mask, base + lo, base + hi);
+}
+
+// Block sum of one int per thread (CNT threads, 4 waves).
+__device__ __forceinline__ int block_sum(int v, int* red)
+{
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    __syncthreads();
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    return red[0] + red[1] + red[2] + red[3];
+}
+
+__global__ __launch_bounds__(CNT) void compact_count_kernel(CompactParams p)
+{
+    __shared__ int red[4];
+    const int blk = blockIdx.x, g = blockIdx.y;
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < PX_PER_THREAD; ++i)
+        cnt += pixel_live(p, blk * BLK_PX + threadIdx.x * PX_PER_THREAD + i, g) ? 1 : 0;
+    const int tot = block_sum(cnt, red);
+    if (threadIdx.x == 0) p.blk_counts[(int64_t)g * p.nblk + blk] = tot;
+}
+
+// Writes the ascending list of live pixels of group g and zero-fills the dX
+// rows of pixels dead for the whole group.
+__global__ __launch_bounds__(CNT) void compact_scatter_kernel(CompactParams p)
+{
+    __shared__ int red[4];
+    __shared__ int wsum[4];
+    const int blk = blockIdx.x, g = blockIdx.y;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+    int before = 0;
+    for (int b = tid; b < blk; b += CNT) before += p.blk_counts[(int64_t)g * p.nblk + b];
+    const int offset = block_sum(before, red);
+
+    bool live[PX_PER_THREAD];
+    int cnt = 0;
+    const int px0 = blk * BLK_PX + tid * PX_PER_THREAD;
+#pragma unroll
+    for (int i = 0; i < PX_PER_THREAD; ++i) {
+        live[i] = pixel_live(p, px0 + i, g);
+        cnt += live[i] ? 1 : 0;
+    }
+    // inclusive scan of cnt over the wave, then over waves
+    int inc = cnt;
+    for (int off = 1; off < 64; off <<= 1) {
+        const int o = __shfl_up(inc, off);
+        if (lane >= off) inc += o;
+    }
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    int wbase = 0;
+    for (int w = 0; w < wave; ++w) wbase += wsum[w];
+    int pos = offset + wbase + inc - cnt;
+    int32_t* list = p.lists + (int64_t)g * p.npix;
+#pragma unroll
+    for (int i = 0; i < PX_PER_THREAD; ++i) {
+        const int px = px0 + i;
+        if (px >= p.npix) break;
+        if (live[i]) {
+            list[pos++] = px;
+        } else {
+            const int lo = g * p.G, hi = min(p.C, lo + p.G);
+            uint4* row = reinterpret_cast<uint4*>(static_cast<char*>(p.dx) +
+                                                  ((int64_t)px * p.C + lo) * p.elem_bytes);
+            const int nvec = (hi - lo) * p.elem_bytes / 16;
+            for (int v = 0; v < nvec; ++v) row[v] = make_uint4(0, 0, 0, 0);
+        }
+    }
+    if (blk == p.nblk - 1 && tid == CNT - 1) p.counts[g] = offset + wbase + inc;
+}
+
+// occ[chunk][kt] = 1 iff dY has a non-zero in pixels of the chunk and
+// channels of k-tile kt (from the packed footprint when given).
+__global__ __launch_bounds__(256) void occupancy_kernel(OccParams p)
+{
+    __shared__ int flags[1024];
+    const int chunk = blockIdx.x;
+    for (int i = threadIdx.x; i < p.ktiles; i += blockDim.x) flags[i] = 0;
+    __syncthreads();
+    const int px0 = chunk * p.chunk;
+    const int npx = min(p.chunk, p.npq - px0);
+    if (p.bits) {
+        const int pairs = npx * p.ktiles;
+        for (int i = threadIdx.x; i < pairs; i += blockDim.x) {
+            const int px = px0 + i / p.ktiles, kt = i % p.ktiles;
+            const int64_t base = (int64_t)px * p.K;
+            const int lo = kt * p.BNk, hi = min(p.K, lo + p.BNk);
+            if (any_bits(p.bits, base + lo, base + hi)) atomicOr(&flags[kt], 1);
+        }
+    } else {
+        const int E = p.dtype == 1 ? 8 : 4;
+        const int vpp = p.K / E;  // vectors per pixel
+        const int nv = npx * vpp;
+        const uint4* v4 = reinterpret_cast<const uint4*>(static_cast<const char*>(p.dy) +
+                                                         (int64_t)px0 * p.K * (p.dtype == 1 ? 2 : 4));
+        for (int i = threadIdx.x; i < nv; i += blockDim.x) {
+            const uint4 v = v4[i];
+            const uint32_t b = p.dtype == 1 ? vec_bits<uint16_t>(v, false) : vec_bits<float>(v, false);
+            if (b) atomicOr(&flags[((i % vpp) * E) / p.BNk], 1);
+        }
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < p.ktiles; i += blockDim.x)
+        p.occ[(int64_t)chunk * p.ktiles + i] = (uint8_t)(flags[i] != 0);
+}
+
+// dW = sum over splits of the partials, in split order.  part is
+// [nsplit][K][RS][C]; dW is written in KRSC or KCRS.
+__global__ void splitk_reduce_kernel(const float* __restrict__ part, float* __restrict__ dw, int nsplit,
+                                     int K, int RS, int C, int krsc)
+{
+    const int64_t total = (int64_t)K * RS * C;
+    const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i4 * 4 >= total) return;
+    const float4* p4 = reinterpret_cast<const float4*>(part);
+    float4 s = p4[i4];
+    for (int z = 1; z < nsplit; ++z) {
+        const float4 v = p4[(int64_t)z * (total / 4) + i4];
+        s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    }
+    if (krsc) {
+        reinterpret_cast<float4*>(dw)[i4] = s;
+    } else {
+        const int64_t i = i4 * 4;
+        const int c = (int)(i % C);
+        const int64_t kt = i / C;
+        const int tap = (int)(kt % RS);
+        const int k = (int)(kt / RS);
+        const float vals[4] = {s.x, s.y, s.z, s.w};
+        for (int j = 0; j < 4; ++j) dw[((int64_t)k * C + c + j) * RS + tap] = vals[j];
+    }
+}
+
+}  // namespace
+
+int compact_block_pixels() { return BLK_PX; }
+
+hipError_t launch_relu_mask_pack(int dtype, int64_t count, const void* x, uint32_t* bits, int relu,
+                                 hipStream_t stream)
+{
+    const int E = dtype == 1 ? 8 : 4;
+    const int L = 32 / E;
+    int64_t nvec = (count + E - 1) / E;
+    nvec = (nvec + L - 1) / L * L;  // whole words
+    const int64_t blocks = (nvec + 255) / 256;
+    if (blocks == 0) return hipSuccess;
+    if (dtype == 1)
+        mask_pack_kernel<uint16_t><<<(unsigned)blocks, 256, 0, stream>>>((const uint16_t*)x, bits, count, nvec,
+                                                                         relu != 0);
+    else
+        mask_pack_kernel<float><<<(unsigned)blocks, 256, 0, stream>>>((const float*)x, bits, count, nvec,
+                                                                      relu != 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_compact(const CompactParams& p, hipStream_t stream)
+{
+    dim3 grid(p.nblk, p.groups);
+    compact_count_kernel<<<grid, CNT, 0, stream>>>(p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    compact_scatter_kernel<<<grid, CNT, 0, stream>>>(p);
+    return hipGetLastError();
+}
+
+hipError_t launch_occupancy(const OccParams& p, hipStream_t stream)
+{
+    occupancy_kernel<<<p.nchunks, 256, 0, stream>>>(p);
+    return hipGetLastError();
+}
+
+hipError_t launch_splitk_reduce(const float* part, float* dw, int nsplit, int K, int RS, int C, int krsc,
+                                hipStream_t stream)
+{
+    const int64_t n4 = (int64_t)K * RS * C / 4;
+    splitk_reduce_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, stream>>>(part, dw, nsplit, K, RS, C, krsc);
+    return hipGetLastError();
+}
+
+}  // namespace cbw

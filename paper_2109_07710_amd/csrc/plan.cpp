@@ -1,0 +1,97 @@
+// Host-only validation and workspace planning (see plan.hpp).
+#include "plan.hpp"
+
+namespace cbw {
+
+namespace {
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+Region take(size_t* cursor, size_t bytes)
+{
+    Region r;
+    r.off = *cursor;
+    r.bytes = bytes;
+    *cursor = align256(*cursor + bytes);
+    return r;
+}
+
+constexpr int64_t kMaxElems = (int64_t)1 << 31;
+
+}  // namespace
+
+int validate_desc(const cbw_conv_desc* d)
+{
+    if (!d) return CBW_ERR_INVALID_ARG;
+    if (d->N <= 0 || d->C <= 0 || d->H <= 0 || d->W <= 0 || d->K <= 0 || d->R <= 0 || d->S <= 0)
+        return CBW_ERR_INVALID_ARG;
+    if (d->stride_h <= 0 || d->stride_w <= 0 || d->pad_h < 0 || d->pad_w < 0) return CBW_ERR_INVALID_ARG;
+    const int64_t ph = (int64_t)d->H + 2 * (int64_t)d->pad_h - d->R;
+    const int64_t pw = (int64_t)d->W + 2 * (int64_t)d->pad_w - d->S;
+    if (ph < 0 || pw < 0) return CBW_ERR_INVALID_ARG;
+    if (d->P != ph / d->stride_h + 1 || d->Q != pw / d->stride_w + 1) return CBW_ERR_INVALID_ARG;
+    if (d->dtype != CBW_F32 && d->dtype != CBW_BF16) return CBW_ERR_INVALID_ARG;
+    if (d->act_layout != CBW_NHWC && d->act_layout != CBW_NCHW) return CBW_ERR_INVALID_ARG;
+    if (d->w_layout != CBW_KRSC && d->w_layout != CBW_KCRS) return CBW_ERR_INVALID_ARG;
+    if (d->act_layout != CBW_NHWC) return CBW_ERR_UNSUPPORTED;
+    const int E = d->dtype == CBW_BF16 ? 8 : 4;
+    if (d->C % E != 0 || d->K % E != 0) return CBW_ERR_UNSUPPORTED;
+    const int64_t npix = (int64_t)d->N * d->H * d->W, npq = (int64_t)d->N * d->P * d->Q;
+    if (npix * d->C >= kMaxElems || npq * d->K >= kMaxElems) return CBW_ERR_UNSUPPORTED;
+    if ((int64_t)d->K * d->C * d->R * d->S >= kMaxElems) return CBW_ERR_UNSUPPORTED;
+    if (d->K > 1024 * kWeightTileK) return CBW_ERR_UNSUPPORTED;  // occupancy flags per chunk
+    return CBW_OK;
+}
+
+int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out)
+{
+    int st = validate_desc(d);
+    if (st != CBW_OK) return st;
+    DataPlan p;
+    p.npix = (int64_t)d->N * d->H * d->W;
+    p.groups = (d->C + kDataTileC - 1) / kDataTileC;
+    p.nblk = (int)((p.npix + kCompactBlock - 1) / kCompactBlock);
+    size_t cur = 0;
+    p.header = take(&cur, 256);
+    p.wt = take(&cur, (size_t)d->K * d->C * d->R * d->S * elem_bytes(d->dtype));
+    if (masked) {
+        p.blk_counts = take(&cur, (size_t)p.groups * p.nblk * 4);
+        p.counts = take(&cur, (size_t)p.groups * 4);
+        p.lists = take(&cur, (size_t)p.groups * p.npix * 4);
+    }
+    p.total = cur;
+    *out = p;
+    return CBW_OK;
+}
+
+int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
+{
+    int st = validate_desc(d);
+    if (st != CBW_OK) return st;
+    WeightPlan p;
+    p.npq = (int64_t)d->N * d->P * d->Q;
+    const int chunk = weight_chunk_px(d->dtype);
+    p.nchunks = (int)((p.npq + chunk - 1) / chunk);
+    p.ctiles = (d->C + kWeightTileC - 1) / kWeightTileC;
+    p.ktiles = (d->K + kWeightTileK - 1) / kWeightTileK;
+    const int tiles = d->R * d->S * p.ctiles * p.ktiles;
+    int nsplit = (kTargetWorkgroups + tiles - 1) / tiles;
+    int max_split = p.nchunks / 4;  // at least four chunks per workgroup
+    if (max_split < 1) max_split = 1;
+    if (nsplit > max_split) nsplit = max_split;
+    if (nsplit < 1) nsplit = 1;
+    p.chunks_per_split = (p.nchunks + nsplit - 1) / nsplit;
+    p.nsplit = (p.nchunks + p.chunks_per_split - 1) / p.chunks_per_split;
+    p.grid = tiles * p.nsplit;
+    p.direct = (p.nsplit == 1 && d->w_layout == CBW_KRSC);
+    size_t cur = 0;
+    p.header = take(&cur, 256);
+    p.occ = take(&cur, (size_t)p.nchunks * p.ktiles);
+    p.skip_slots = take(&cur, (size_t)p.grid * 4);
+    if (!p.direct) p.partials = take(&cur, (size_t)p.nsplit * d->K * d->R * d->S * d->C * 4);
+    p.total = cur;
+    *out = p;
+    return CBW_OK;
+}
+
+}  // namespace cbw

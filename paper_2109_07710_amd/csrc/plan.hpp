@@ -1,0 +1,46 @@
+// Host-only planning: descriptor validation, tile counts, split-K choice and
+// workspace layout.  No HIP dependency, so it is testable without a GPU.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/convbwd.h"
+
+namespace cbw {
+
+// Tile constants shared with the kernels (asserted equal at dispatch time).
+constexpr int kDataTileC = 128;     // channels per data-gradient tile = compaction group width
+constexpr int kDataTileP = 128;     // pixels per data-gradient tile
+constexpr int kWeightTileC = 128;   // channels c per weight-gradient tile
+constexpr int kWeightTileK = 128;   // output channels k per weight-gradient tile
+constexpr int kCompactBlock = 1024; // pixels per compaction block
+constexpr int kTargetWorkgroups = 512;  // 256 CUs x 2 resident workgroups
+
+inline int weight_chunk_px(int dtype) { return 16 * (dtype == CBW_BF16 ? 8 : 4); }
+
+struct Region {
+    size_t off = 0, bytes = 0;
+};
+
+struct DataPlan {
+    int64_t npix = 0;
+    int groups = 0, nblk = 0;
+    Region header, wt, blk_counts, counts, lists;
+    size_t total = 0;
+};
+
+struct WeightPlan {
+    int64_t npq = 0;
+    int nchunks = 0, ctiles = 0, ktiles = 0, nsplit = 0, chunks_per_split = 0, grid = 0;
+    bool direct = false;  // partial of the single split is dW itself
+    Region header, occ, skip_slots, partials;
+    size_t total = 0;
+};
+
+int validate_desc(const cbw_conv_desc* d);
+int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out);
+int plan_weight(const cbw_conv_desc* d, WeightPlan* out);
+inline int elem_bytes(int dtype) { return dtype == CBW_BF16 ? 2 : 4; }
+
+}  // namespace cbw

@@ -1,0 +1,125 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/convbwd.h declares, and its host-only validation and workspace
+planning behave as documented.  No compute call is made here."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2109_07710_amd as cb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "convbwd.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)
+    return sorted(set(n for n in names if n not in ("if", "while")))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(cb.LIB_PATH):
+        pytest.skip("library not built")
+    return cb.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = _declared_functions()
+    assert len(names) >= 13
+    assert set(names) == set(cb.EXPORTS)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings(L):
+    for s in (0, -1, -2, -3, -4):
+        assert cb.status_string(s) != "unknown status"
+    assert cb.status_string(5) == "unknown status"
+
+
+def _desc(**kw):
+    base = dict(N=2, C=64, H=10, W=12, K=32, R=3, S=3, stride=(1, 1), pad=(1, 1), dtype="bf16")
+    base.update(kw)
+    return cb.ConvDesc.make(**base)
+
+
+def test_validation_codes(L):
+    assert cb.cbw_validate_desc(_desc()) == cb.CBW_OK
+    assert cb.cbw_validate_desc(_desc(stride=(2, 3), pad=(0, 2), R=5, S=1)) == cb.CBW_OK
+    d = _desc()
+    d.P += 1
+    assert cb.cbw_validate_desc(d) == cb.CBW_ERR_INVALID_ARG
+    d = _desc()
+    d.N = 0
+    assert cb.cbw_validate_desc(d) == cb.CBW_ERR_INVALID_ARG
+    d = _desc()
+    d.stride_h = 0
+    assert cb.cbw_validate_desc(d) == cb.CBW_ERR_INVALID_ARG
+    d = _desc()
+    d.pad_w = -1
+    assert cb.cbw_validate_desc(d) == cb.CBW_ERR_INVALID_ARG
+    d = _desc()
+    d.dtype = 7
+    assert cb.cbw_validate_desc(d) == cb.CBW_ERR_INVALID_ARG
+    assert cb.cbw_validate_desc(_desc(C=12)) == cb.CBW_ERR_UNSUPPORTED           # not a multiple of 8 (bf16)
+    assert cb.cbw_validate_desc(_desc(C=12, K=8, dtype="f32")) == cb.CBW_OK     # multiple of 4 (fp32)
+    assert cb.cbw_validate_desc(_desc(act_layout="nchw")) == cb.CBW_ERR_UNSUPPORTED
+    assert cb.cbw_validate_desc(_desc(w_layout="kcrs")) == cb.CBW_OK
+    assert cb.cbw_validate_desc(_desc(N=4096, H=1024, W=1024, C=8)) == cb.CBW_ERR_UNSUPPORTED  # >= 2^31 elems
+    assert L.cbw_validate_desc(None) == cb.CBW_ERR_INVALID_ARG
+    assert cb.cbw_validate_desc(_desc(H=1, R=3, pad=(0, 1))) == cb.CBW_ERR_INVALID_ARG  # empty output
+
+
+def test_mask_words(L):
+    d = _desc()
+    assert cb.cbw_mask_words(d) == (2 * 64 * 10 * 12 + 31) // 32
+    assert cb.cbw_dy_mask_words(d) == (2 * 32 * 10 * 12 + 31) // 32
+    bad = _desc()
+    bad.P = 99
+    assert cb.cbw_mask_words(bad) == 0
+
+
+def test_workspace_sizes(L):
+    d = cb.ConvDesc.make(32, 256, 56, 56, 256, 3, 3, 1, 1)
+    dense = cb.cbw_workspace_size(d, cb.CBW_OP_BWD_DATA)
+    masked = cb.cbw_workspace_size(d, cb.CBW_OP_BWD_DATA_MASKED)
+    wgt = cb.cbw_workspace_size(d, cb.CBW_OP_BWD_WEIGHT)
+    wt_bytes = 256 * 256 * 9 * 2
+    assert dense >= wt_bytes + 256
+    npix = 32 * 56 * 56
+    assert masked >= dense + 2 * npix * 4          # two channel groups of live-pixel lists
+    assert wgt >= 2 * 256 * 9 * 256 * 4            # at least two split-K partials of dW
+    assert all(x % 256 == 0 for x in (dense, masked))
+    with pytest.raises(cb.CbwError):
+        cb.cbw_workspace_size(d, 7)
+    assert L.cbw_workspace_size(ctypes.byref(d), 0, None) == cb.CBW_ERR_INVALID_ARG
+
+
+def test_null_arguments_rejected_without_gpu(L):
+    d = _desc()
+    n = ctypes.c_size_t(0)
+    assert L.cbw_workspace_size(ctypes.byref(d), 1, ctypes.byref(n)) == 0
+    # Null tensors are rejected by validation before any HIP call is made.
+    assert L.conv_bwd_data_masked(ctypes.byref(d), None, None, None, None, None, 0, 0, None) == \
+        cb.CBW_ERR_INVALID_ARG
+    assert L.conv_bwd_data(ctypes.byref(d), None, None, None, None, 0, None) == cb.CBW_ERR_INVALID_ARG
+    assert L.conv_bwd_weight_sparse(ctypes.byref(d), None, None, None, None, None, 0, 0, None) == \
+        cb.CBW_ERR_INVALID_ARG
+    assert L.cbw_relu_mask_pack(ctypes.byref(d), None, None, None) == cb.CBW_ERR_INVALID_ARG
+    assert L.cbw_nonzero_mask_pack(1, 10, None, None, None) == cb.CBW_ERR_INVALID_ARG
+    assert L.cbw_nonzero_mask_pack(1, 0, None, None, None) == cb.CBW_OK
+    assert L.cbw_nonzero_mask_pack(9, 10, None, None, None) == cb.CBW_ERR_INVALID_ARG
+    bad = _desc()
+    bad.Q = 1
+    assert L.conv_bwd_data(ctypes.byref(bad), None, None, None, None, 0, None) == cb.CBW_ERR_INVALID_ARG
+    # Workspace check comes after the pointer checks: fake aligned pointers, no workspace.
+    fake = ctypes.c_void_p(1 << 20)
+    assert L.conv_bwd_data(ctypes.byref(d), fake, fake, fake, None, 0, None) == cb.CBW_ERR_WORKSPACE
+    assert L.conv_bwd_weight_sparse(ctypes.byref(d), fake, fake, None, fake, None, 0, 0, None) == \
+        cb.CBW_ERR_WORKSPACE
+    misaligned = ctypes.c_void_p((1 << 20) + 2)
+    assert L.conv_bwd_data(ctypes.byref(d), misaligned, fake, fake, None, 0, None) == cb.CBW_ERR_UNSUPPORTED
