@@ -179,6 +179,15 @@ int cbw_read_occupancy(const cbw_conv_desc* desc, const void* workspace, size_t 
                        int32_t* nchunks, int32_t* ktiles, int32_t* chunk_pixels, int32_t* ktile_width,
                        void* stream);
 
+/* Profiling hook (for benchmarks; not needed for computing).  Until changed,
+ * every call on this host thread of the given op family records `start`
+ * (a hipEvent_t as void*) on the call's stream right before the op's main
+ * GEMM kernel is launched and `stop` right after it, so that
+ * hipEventElapsedTime(start, stop) is that kernel's duration.  op is
+ * CBW_OP_BWD_DATA (covers both data-gradient entry points) or
+ * CBW_OP_BWD_WEIGHT; NULL events switch the hook off. */
+int cbw_set_profile_events(int op, void* start, void* stop);
+
 #ifdef __cplusplus
 }
 #endif

@@ -58,8 +58,15 @@ def _load():
     lib.oracle_conv_bwd_data_at.restype = None
     lib.oracle_conv_bwd_weight_at.argtypes = [sp, dp, dp, i32p, ctypes.c_int64, dp, dp, i64p]
     lib.oracle_conv_bwd_weight_at.restype = None
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
     return lib
+
+
+def num_threads():
+    """OpenMP threads the oracle uses."""
+    return _load().oracle_num_threads()
 
 
 def out_size(h, r, stride, pad):

@@ -22,6 +22,7 @@
 #include <stdint.h>
 #include <stddef.h>
 #include <math.h>
+#include <omp.h>
 
 typedef struct {
     int32_t N, C, H, W, K, R, S, P, Q;
@@ -234,4 +235,10 @@ void oracle_conv_bwd_weight_at(const oracle_shape* sh, const double* X, const do
         if (abs_out) abs_out[i] = aacc;
         if (nterms) nterms[i] = cnt;
     }
+}
+
+/* Number of OpenMP threads the oracle's parallel loops use. */
+int oracle_num_threads(void)
+{
+    return omp_get_max_threads();
 }

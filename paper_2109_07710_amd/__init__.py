@@ -28,7 +28,7 @@ CBW_FLAG_NO_SKIP = 1
 EXPORTS = ("cbw_status_string", "cbw_validate_desc", "cbw_mask_words", "cbw_dy_mask_words",
            "cbw_workspace_size", "cbw_relu_mask_pack", "cbw_nonzero_mask_pack", "conv_bwd_data",
            "conv_bwd_data_masked", "conv_bwd_weight_sparse", "cbw_read_stats", "cbw_read_live_lists",
-           "cbw_read_occupancy")
+           "cbw_read_occupancy", "cbw_set_profile_events")
 
 
 class ConvDesc(ctypes.Structure):
@@ -92,6 +92,7 @@ def lib():
     i32p = ctypes.POINTER(ctypes.c_int32)
     L.cbw_read_live_lists.argtypes = [dp, vp, sz, ctypes.c_int, vp, i32p, i32p, vp]
     L.cbw_read_occupancy.argtypes = [dp, vp, sz, vp, i32p, i32p, i32p, i32p, vp]
+    L.cbw_set_profile_events.argtypes = [ctypes.c_int, vp, vp]
     for name in EXPORTS:
         if name != "cbw_status_string" and name not in ("cbw_mask_words", "cbw_dy_mask_words"):
             getattr(L, name).restype = ctypes.c_int
@@ -216,3 +217,12 @@ def cbw_read_occupancy(desc, ws, stream=None):
                                     out.ctypes.data_as(ctypes.c_void_p), *args, _stream(stream)),
            "cbw_read_occupancy")
     return out, cp.value, kw.value
+
+
+def cbw_set_profile_events(op, start=None, stop=None):
+    """Record torch.cuda.Event `start`/`stop` around the op's main GEMM kernel
+    on every following call of this thread (None, None switches it off).  The
+    events must have been recorded once so that they exist."""
+    sp = ctypes.c_void_p(start.cuda_event) if start is not None else None
+    tp = ctypes.c_void_p(stop.cuda_event) if stop is not None else None
+    _check(lib().cbw_set_profile_events(op, sp, tp), "cbw_set_profile_events")

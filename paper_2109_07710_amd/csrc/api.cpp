@@ -12,6 +12,14 @@ namespace {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Profiling events per op family (0 = data gradient, 1 = weight gradient).
+thread_local hipEvent_t g_prof[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
+
+hipError_t prof_mark(int fam, int which, hipStream_t s)
+{
+    return g_prof[fam][which] ? hipEventRecord(g_prof[fam][which], s) : hipSuccess;
+}
+
 int hip_status(hipError_t e)
 {
     if (e == hipSuccess) return CBW_OK;
@@ -95,7 +103,9 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
         p.lists = cp.lists;
         p.counts = cp.counts;
     }
-    return hip_status(launch_bwd_data(desc->dtype, mode, p, s));
+    if ((e = prof_mark(0, 0, s)) != hipSuccess) return hip_status(e);
+    if ((e = launch_bwd_data(desc->dtype, mode, p, s)) != hipSuccess) return hip_status(e);
+    return hip_status(prof_mark(0, 1, s));
 }
 
 }  // namespace
@@ -226,7 +236,9 @@ int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void*
     p.mode_flags = (int)flags;
     p.div_q = make_fastdiv((uint32_t)desc->Q);
     p.div_p = make_fastdiv((uint32_t)desc->P);
+    if ((e = prof_mark(1, 0, s)) != hipSuccess) return hip_status(e);
     if ((e = launch_bwd_weight(desc->dtype, p, s)) != hipSuccess) return hip_status(e);
+    if ((e = prof_mark(1, 1, s)) != hipSuccess) return hip_status(e);
     if (!plan.direct) {
         e = launch_splitk_reduce(p.out, dW, plan.nsplit, desc->K, desc->R * desc->S, desc->C,
                                  desc->w_layout == CBW_KRSC, s);
@@ -286,6 +298,18 @@ int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, siz
         return CBW_ERR_INVALID_ARG;
     }
     *out = r;
+    return CBW_OK;
+}
+
+int cbw_set_profile_events(int op, void* start, void* stop)
+{
+    int fam;
+    if (op == CBW_OP_BWD_DATA || op == CBW_OP_BWD_DATA_MASKED) fam = 0;
+    else if (op == CBW_OP_BWD_WEIGHT) fam = 1;
+    else return CBW_ERR_INVALID_ARG;
+    if ((start == nullptr) != (stop == nullptr)) return CBW_ERR_INVALID_ARG;
+    g_prof[fam][0] = static_cast<hipEvent_t>(start);
+    g_prof[fam][1] = static_cast<hipEvent_t>(stop);
     return CBW_OK;
 }
 
