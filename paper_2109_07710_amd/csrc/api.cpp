@@ -60,6 +60,9 @@ DataParams data_params(const cbw_conv_desc* d, const void* dY, const void* wt, v
     p.ctiles = groups;
     p.div_w = make_fastdiv((uint32_t)d->W);
     p.div_h = make_fastdiv((uint32_t)d->H);
+    const int64_t esz = elem_bytes(d->dtype);
+    p.dy_bytes = (uint32_t)((int64_t)d->N * d->P * d->Q * d->K * esz);
+    p.wt_bytes = (uint32_t)((int64_t)d->R * d->S * d->C * d->K * esz);
     return p;
 }
 
@@ -70,7 +73,7 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
     int st = plan_data(desc, masked, &plan);
     if (st != CBW_OK) return st;
     if (!dY || !W || !dX || (masked && !x_mask)) return CBW_ERR_INVALID_ARG;
-    if (!aligned16(dY) || !aligned16(W) || !aligned16(dX) || (masked && ((uintptr_t)x_mask & 3u)))
+    if (!aligned16(dY) || !aligned16(W) || !aligned16(dX) || (masked && !aligned16(x_mask)))
         return CBW_ERR_UNSUPPORTED;
     if ((st = check_ws(ws, ws_bytes, plan.total)) != CBW_OK) return st;
     if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;
@@ -236,6 +239,8 @@ int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void*
     p.mode_flags = (int)flags;
     p.div_q = make_fastdiv((uint32_t)desc->Q);
     p.div_p = make_fastdiv((uint32_t)desc->P);
+    p.x_bytes = (uint32_t)((int64_t)desc->N * desc->H * desc->W * desc->C * elem_bytes(desc->dtype));
+    p.dy_bytes = (uint32_t)(plan.npq * desc->K * elem_bytes(desc->dtype));
     if ((e = prof_mark(1, 0, s)) != hipSuccess) return hip_status(e);
     if ((e = launch_bwd_weight(desc->dtype, p, s)) != hipSuccess) return hip_status(e);
     if ((e = prof_mark(1, 1, s)) != hipSuccess) return hip_status(e);

@@ -18,32 +18,52 @@
 //             generation, Sec. IV-B); the epilogue applies the per-element
 //             select.  Rows dead for the whole group were zero-filled by the
 //             compaction kernel and are never touched here.
+//
+// Main loop: both operand tiles are copied by the load unit straight from
+// global memory into a double-buffered LDS ring (no staging registers, one
+// barrier per reduction step).  LDS rows are 128 bytes (8 chunks of 16
+// bytes) with an XOR chunk swizzle so that the MFMA fragment reads of 16
+// consecutive rows spread over all banks.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "tiles.hpp"
+
 
 namespace cbw {
 
 namespace {
 
-constexpr int BM = 128;         // channels per tile (= compaction group width)
-constexpr int BN = 128;         // pixels per tile
-constexpr int NT = 256;         // threads: 4 waves in a 2 x 2 arrangement
-constexpr int CH = 8;           // 16-byte chunks of reduction per row per step
-constexpr int LDSROW = CH + 1;  // padded row length in chunks (144 bytes)
+constexpr int BM = CBW_DX_BM;     // channels per tile (= compaction group width)
+constexpr int BN = CBW_DX_BN;     // pixels per tile
+constexpr int WM = CBW_DX_WM;     // waves along channels
+constexpr int WN = CBW_DX_WN;     // waves along pixels
+constexpr int NT = 64 * WM * WN;
+constexpr int TM = BM / WM, TN = BN / WN;   // wave tile
+constexpr int FM = TM / 16, FN = TN / 16;   // 16x16 MFMA tiles per wave
+constexpr int CH = 8;                       // 16-byte chunks of reduction per row per step
+constexpr int NW = WM * WN;                 // waves
+constexpr int IA = (BM / 8 + NW - 1) / NW;  // 1 KB copy instructions per wave per step, A
+constexpr int IB = (BN / 8 + NW - 1) / NW;  // same for B
+static_assert(BM % 8 == 0 && BN % 8 == 0, "tiles are copied in groups of 8 rows");
+static_assert(TM % 16 == 0 && TN % 16 == 0, "wave tile must be a multiple of 16");
 
-template <typename T, int MODE>
-__global__ __launch_bounds__(NT, 2) void bwd_data_kernel(DataParams p)
+__device__ __forceinline__ int swz8(int row) { return (row >> 1) & 7; }
+
+template <typename T, int MODE, bool UNIT>
+__global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
 {
     constexpr int E = Elem<T>::E;
-    constexpr int BK = CH * E;  // reduction elements per step
+    constexpr int BK = CH * E;     // reduction elements per step
+    constexpr uint32_t ESZ = sizeof(T);
 
-    __shared__ uint4 As[BM * LDSROW];
-    __shared__ uint4 Bs[BN * LDSROW];
+    __shared__ uint4 As[2][BM * CH];
+    __shared__ uint4 Bs[2][BN * CH];
     __shared__ int pix_s[BN];
+    __shared__ uint32_t msk_s[MODE == MODE_DENSE ? 1 : BN * (BM / 32)];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
 
     const int t = xcd_remap(blockIdx.x, gridDim.x);
     const int ptile = t / p.ctiles;
@@ -55,120 +75,181 @@ __global__ __launch_bounds__(NT, 2) void bwd_data_kernel(DataParams p)
     if (MODE == MODE_GATHER) nrows = p.counts[ctile];
     if (row0 >= nrows) return;  // uniform across the workgroup
 
-    if (tid < BN) {
-        const int r = row0 + tid;
+    for (int i = tid; i < BN; i += NT) {
+        const int r = row0 + i;
         int pix = -1;
         if (r < nrows) pix = (MODE == MODE_GATHER) ? p.lists[(int64_t)ctile * p.npix + r] : r;
-        pix_s[tid] = pix;
+        pix_s[i] = pix;
     }
     __syncthreads();
 
-    // Each thread loads rows (tid / CH) + 32 j, j = 0..3, chunk tid % CH, of
-    // both operands.  Pixel coordinates of its four B rows:
-    const int lrow = tid / CH, lch = tid % CH;
-    int bn_[4], bh_[4], bw_[4];
+    // Footprint bits of the tile (pixel row x 32-channel word), staged once;
+    // valid when every pixel's group of BM channels starts on a word.
+    const bool mask_lds = MODE != MODE_DENSE && (p.C % 32) == 0;
+    if (mask_lds) {
+        for (int i = tid; i < BN * (BM / 32); i += NT) {
+            const int pr = i / (BM / 32), wi = i - pr * (BM / 32);
+            const int pix = pix_s[pr];
+            uint32_t word = 0;
+            if (pix >= 0 && c0 + 32 * wi < p.C) word = p.mask[((int64_t)pix * p.C + c0) / 32 + wi];
+            msk_s[i] = word;
+        }
+    }
+
+    const u32x4_t rs_wt = make_rsrc_words(p.wt, p.wt_bytes);
+    const u32x4_t rs_dy = make_rsrc_words(p.dy, p.dy_bytes);
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+
+    // Staging: every wave copies whole groups of 8 LDS rows (1 KB) straight
+    // from global memory into LDS.  Row group g = wave + NW*j; lane l serves
+    // row 8g + l/8 at physical chunk l%8, i.e. logical chunk (l%8) ^ swz(row).
+    const int lrow8 = lane >> 3, pch = lane & 7;
+    uint32_t a_off[IA];   // A: byte offset without the step part, kOOB when no such channel
+    int a_lc[IA];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int pix = pix_s[lrow + 32 * j];
+    for (int j = 0; j < IA; ++j) {
+        const int row = 8 * (wave + NW * j) + lrow8;
+        const int lc = pch ^ swz8(row);
+        const int c = c0 + row;
+        a_lc[j] = lc;
+        a_off[j] = (row < BM && c < p.C) ? (uint32_t)(c * p.K + lc * E) * ESZ : kOOB;
+    }
+    int bn_[IB], bh_[IB], bw_[IB], bbase[IB], b_lc[IB];
+#pragma unroll
+    for (int j = 0; j < IB; ++j) {
+        const int row = 8 * (wave + NW * j) + lrow8;
+        const int lc = pch ^ swz8(row);
+        b_lc[j] = lc;
+        const int pix = row < BN ? pix_s[row] : -1;
+        bn_[j] = -1; bh_[j] = 0; bw_[j] = 0;
         if (pix >= 0) {
             const uint32_t nh = fdiv((uint32_t)pix, p.div_w);
             bw_[j] = pix - (int)nh * p.W;
             const uint32_t n = fdiv(nh, p.div_h);
             bh_[j] = (int)nh - (int)n * p.H;
             bn_[j] = (int)n;
-        } else {
-            bn_[j] = -1; bh_[j] = 0; bw_[j] = 0;
         }
+        // unit stride: element offset of dY at (n, h, w) before the tap shift
+        bbase[j] = ((bn_[j] * p.P + bh_[j]) * p.Q + bw_[j]) * p.K + lc * E;
     }
 
-    floatx4 acc[4][4];
+    floatx4 acc[FM][FN];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     const int kchunks = (p.K + BK - 1) / BK;
     const int nsteps = p.R * p.S * kchunks;
-    const T* __restrict__ wt = reinterpret_cast<const T*>(p.wt);
-    const T* __restrict__ dy = reinterpret_cast<const T*>(p.dy);
+    const bool kfull = (p.K % BK) == 0;
 
-    uint4 ra[4], rb[4];
-    int src[4];  // element offset of the B rows' dY pixel for the current tap, -1 = none
-    int cur_tap = -1;
+    uint32_t b_off[IB];   // B byte offset for the current tap, kOOB when the tap misses
+    int ld_tap = 0, ld_kc = 0;  // next step to load
 
     auto set_tap = [&](int tap) {
-        const int r = tap / p.S, s = tap - (tap / p.S) * p.S;
+        const int r = tap / p.S, s = tap - r * p.S;
+        if (UNIT) {
+            const int delta = ((p.pad_h - r) * p.Q + (p.pad_w - s)) * p.K;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            src[j] = -1;
-            if (bn_[j] < 0) continue;
-            int hh = bh_[j] + p.pad_h - r, ww = bw_[j] + p.pad_w - s;
-            if (hh < 0 || ww < 0) continue;
-            int pp, qq;
-            if (p.stride_h == 1) { pp = hh; } else { if (hh % p.stride_h) continue; pp = hh / p.stride_h; }
-            if (p.stride_w == 1) { qq = ww; } else { if (ww % p.stride_w) continue; qq = ww / p.stride_w; }
-            if (pp >= p.P || qq >= p.Q) continue;
-            src[j] = ((bn_[j] * p.P + pp) * p.Q + qq) * p.K;
+            for (int j = 0; j < IB; ++j) {
+                const int hh = bh_[j] + p.pad_h - r, ww = bw_[j] + p.pad_w - s;
+                const bool ok = bn_[j] >= 0 && hh >= 0 && hh < p.P && ww >= 0 && ww < p.Q;
+                b_off[j] = ok ? (uint32_t)(bbase[j] + delta) * ESZ : kOOB;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < IB; ++j) {
+                b_off[j] = kOOB;
+                const int hh = bh_[j] + p.pad_h - r, ww = bw_[j] + p.pad_w - s;
+                if (bn_[j] < 0 || hh < 0 || ww < 0) continue;
+                if (hh % p.stride_h || ww % p.stride_w) continue;
+                const int pp = hh / p.stride_h, qq = ww / p.stride_w;
+                if (pp >= p.P || qq >= p.Q) continue;
+                b_off[j] = (uint32_t)(((bn_[j] * p.P + pp) * p.Q + qq) * p.K + b_lc[j] * E) * ESZ;
+            }
         }
     };
 
-    auto load = [&](int step) {
-        const int tap = step / kchunks;
-        const int k0 = (step - tap * kchunks) * BK + lch * E;
-        if (tap != cur_tap) { set_tap(tap); cur_tap = tap; }
-        const bool kin = k0 < p.K;
+    // Queue the copies of the next step into LDS buffer `buf`.
+    auto load = [&](int buf) {
+        if (ld_kc == 0) set_tap(ld_tap);
+        const int k0 = ld_kc * BK;
+        const uint32_t a_step = (uint32_t)((ld_tap * p.C) * p.K + k0) * ESZ;
+        const uint32_t b_step = (uint32_t)k0 * ESZ;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int c = c0 + lrow + 32 * j;
-            ra[j] = make_uint4(0, 0, 0, 0);
-            if (kin && c < p.C)
-                ra[j] = *reinterpret_cast<const uint4*>(wt + ((int64_t)(tap * p.C + c) * p.K + k0));
-            rb[j] = make_uint4(0, 0, 0, 0);
-            if (kin && src[j] >= 0)
-                rb[j] = *reinterpret_cast<const uint4*>(dy + ((int64_t)src[j] + k0));
+        for (int j = 0; j < IA; ++j) {
+            const int g = wave + NW * j;
+            if (IA * NW * 8 == BM || g * 8 < BM) {
+                const bool kin = kfull || (k0 + a_lc[j] * E < p.K);
+                buf_load16_lds(rs_wt, kin ? a_off[j] + a_step : kOOB,
+                               lds_addr(&As[buf][(wave_u + NW * j) * 8 * CH]));
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < IB; ++j) {
+            const int g = wave + NW * j;
+            if (IB * NW * 8 == BN || g * 8 < BN) {
+                const bool kin = kfull || (k0 + b_lc[j] * E < p.K);
+                buf_load16_lds(rs_dy, kin ? b_off[j] + b_step : kOOB,
+                               lds_addr(&Bs[buf][(wave_u + NW * j) * 8 * CH]));
+            }
+        }
+        if (++ld_kc == kchunks) { ld_kc = 0; ++ld_tap; }
+    };
+
+    auto compute = [&](int buf) {
+#pragma unroll
+        for (int kc = 0; kc < CH / 4; ++kc) {
+            const int chl = kc * 4 + (lane >> 4);
+            uint4 fa[FM], fb[FN];
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int row = wm * TM + i * 16 + (lane & 15);
+                fa[i] = As[buf][row * CH + (chl ^ swz8(row))];
+            }
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int row = wn * TN + j * 16 + (lane & 15);
+                fb[j] = Bs[buf][row * CH + (chl ^ swz8(row))];
+            }
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) acc[i][j] = mfma_chunk(acc[i][j], fa[i], fb[j], T{});
         }
     };
 
     load(0);
+    wait_vmem();
+    __syncthreads();
     for (int step = 0; step < nsteps; ++step) {
+        const int buf = step & 1;
+        if (step + 1 < nsteps) load(buf ^ 1);
+        compute(buf);
+        wait_vmem();
         __syncthreads();
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            As[(lrow + 32 * j) * LDSROW + lch] = ra[j];
-            Bs[(lrow + 32 * j) * LDSROW + lch] = rb[j];
-        }
-        __syncthreads();
-        if (step + 1 < nsteps) load(step + 1);
-#pragma unroll
-        for (int kc = 0; kc < CH / 4; ++kc) {
-            const int ch = kc * 4 + (lane >> 4);
-            uint4 fa[4], fb[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) fa[i] = As[(wm * 64 + i * 16 + (lane & 15)) * LDSROW + ch];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) fb[j] = Bs[(wn * 64 + j * 16 + (lane & 15)) * LDSROW + ch];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = mfma_chunk(acc[i][j], fa[i], fb[j], T{});
-        }
     }
 
-    // Epilogue: lane holds channels c0 + wm*64 + i*16 + 4*(lane/16) + v of
-    // pixel row wn*64 + j*16 + lane%16.
+    // Epilogue: lane holds channels c0 + wm*TM + i*16 + 4*(lane/16) + v of
+    // pixel row wn*TN + j*16 + lane%16.
     T* __restrict__ dx = reinterpret_cast<T*>(p.dx);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int pix = pix_s[wn * 64 + j * 16 + (lane & 15)];
+    for (int j = 0; j < FN; ++j) {
+        const int pr = wn * TN + j * 16 + (lane & 15);
+        const int pix = pix_s[pr];
         if (pix < 0) continue;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int c = c0 + wm * 64 + i * 16 + 4 * (lane >> 4);
+        for (int i = 0; i < FM; ++i) {
+            const int cl = wm * TM + i * 16 + 4 * (lane >> 4);  // channel within the tile
+            const int c = c0 + cl;
             if (c >= p.C) continue;
             const int64_t o = (int64_t)pix * p.C + c;
             floatx4 v = acc[i][j];
             uint32_t keep = 0xfu;
-            if (MODE != MODE_DENSE) keep = (p.mask[o >> 5] >> (o & 31)) & 0xfu;
+            if (MODE != MODE_DENSE) {
+                if (mask_lds) keep = (msk_s[pr * (BM / 32) + cl / 32] >> (cl & 31)) & 0xfu;
+                else keep = (p.mask[o >> 5] >> (o & 31)) & 0xfu;
+            }
             if constexpr (sizeof(T) == 2) {
                 uint32_t h0 = (keep & 1u) ? f32_to_bf16_rne(v.x) : 0u;
                 uint32_t h1 = (keep & 2u) ? f32_to_bf16_rne(v.y) : 0u;
@@ -229,7 +310,12 @@ hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t
     const int ptiles = (p.npix + BN - 1) / BN;
     const int nb = ptiles * p.ctiles;
     if (nb <= 0) return hipSuccess;
-#define CBW_LAUNCH(T, M) bwd_data_kernel<T, M><<<nb, NT, 0, stream>>>(p)
+    const bool unit = p.stride_h == 1 && p.stride_w == 1;
+#define CBW_LAUNCH(T, M)                                                          \
+    do {                                                                          \
+        if (unit) bwd_data_kernel<T, M, true><<<nb, NT, 0, stream>>>(p);          \
+        else bwd_data_kernel<T, M, false><<<nb, NT, 0, stream>>>(p);              \
+    } while (0)
     if (dtype == 1) {
         if (mode == MODE_DENSE) CBW_LAUNCH(uint16_t, MODE_DENSE);
         else if (mode == MODE_SELECT) CBW_LAUNCH(uint16_t, MODE_SELECT);

@@ -5,10 +5,11 @@
 // (weight-gradient phase, Sec. IV-B).  GEMM view: M = channels c of one tap
 // (A = shifted X), N = output channels k (B = dY), reduction = pixels.  Both
 // operands are pixel-major in NHWC, so the reduction index is the strided
-// one.  Each thread loads an E x E block (E pixels x E channels, one
+// one.  Each staging thread loads an E x E block (E pixels x E channels, one
 // 16-byte vector per pixel, coalesced along channels), transposes it in
 // registers and writes E vectors of E consecutive pixels into LDS, where the
-// MFMA fragments then read reduction-contiguous 16-byte chunks.
+// MFMA fragments then read reduction-contiguous 16-byte chunks.  Half of the
+// workgroup stages X blocks, the other half dY blocks.
 //
 // Input sparsity (Sec. III-B): a (pixel chunk, k tile) block in which dY is
 // entirely zero contributes exactly zero, so the workgroup skips its loads
@@ -19,15 +20,26 @@
 // order (deterministic).
 #include "common.hpp"
 #include "kernels.hpp"
+#include "tiles.hpp"
+
 
 namespace cbw {
 
 namespace {
 
-constexpr int BM = 128;   // channels c per tile
-constexpr int BN = 128;   // output channels k per tile
-constexpr int NT = 256;
-constexpr int CHR = 16;   // 16-byte chunks per LDS row (256 bytes)
+constexpr int BM = CBW_DW_BM;   // channels c per tile
+constexpr int BN = CBW_DW_BN;   // output channels k per tile
+constexpr int WM = CBW_DW_WM, WN = CBW_DW_WN;
+constexpr int NT = 64 * WM * WN;
+constexpr int HT = NT / 2;      // staging threads per operand
+constexpr int TM = BM / WM, TN = BN / WN;
+constexpr int FM = TM / 16, FN = TN / 16;
+constexpr int CH = 8;           // 16-byte chunks per LDS row (128 bytes)
+static_assert(BM == BN, "both operands share the staging layout");
+
+// Chunk swizzle: bijective on 16 consecutive rows (fragment reads) and
+// two-to-one on rows 8c + j, c = 0..15 (transposed block writes).
+__device__ __forceinline__ int swz(int row) { return ((row >> 1) ^ (row >> 3)) & 7; }
 
 template <typename T>
 __device__ __forceinline__ void transpose_block(const uint4 (&v)[Elem<T>::E], uint4 (&u)[Elem<T>::E]);
@@ -41,7 +53,7 @@ __device__ __forceinline__ void transpose_block<uint16_t>(const uint4 (&v)[8], u
 #pragma unroll
     for (int e = 0; e < 8; ++e) { d[e][0] = v[e].x; d[e][1] = v[e].y; d[e][2] = v[e].z; d[e][3] = v[e].w; }
 #pragma unroll
-    for (int m = 0; m < 4; ++m)        // channel pair (2m, 2m+1)
+    for (int m = 0; m < 4; ++m)           // channel pair (2m, 2m+1)
 #pragma unroll
         for (int mp = 0; mp < 4; ++mp) {  // pixel pair (2mp, 2mp+1)
             const uint32_t a = d[2 * mp][m], b = d[2 * mp + 1][m];
@@ -63,20 +75,23 @@ __device__ __forceinline__ void transpose_block<float>(const uint4 (&v)[4], uint
 }
 
 template <typename T>
-__global__ __launch_bounds__(NT, 2) void bwd_weight_kernel(WeightParams p)
+__global__ __launch_bounds__(NT) void bwd_weight_kernel(WeightParams p)
 {
     constexpr int E = Elem<T>::E;
-    constexpr int BK = CHR * E;                 // pixels per chunk
-    constexpr int CB = BM / E;                  // channel blocks per tile row set
-    constexpr int NBLK = (BM / E) * (BK / E);   // E x E blocks per operand tile
-    constexpr int BPT = NBLK / NT;              // blocks per thread per operand
+    constexpr int BK = CH * E;                  // pixels per chunk
+    constexpr int CB = BM / E;                  // channel blocks
+    constexpr int NBLK = CB * (BK / E);         // E x E blocks per operand tile
+    constexpr int BPT = NBLK / HT;              // blocks per staging thread
+    static_assert(NBLK % HT == 0, "blocks must divide evenly");
 
-    __shared__ uint4 As[BM * CHR];
-    __shared__ uint4 Bs[BN * CHR];
+    __shared__ uint4 As[2][BM * CH];
+    __shared__ uint4 Bs[2][BN * CH];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
+    const bool stage_b = tid >= HT;             // wave-uniform role
+    const int st = stage_b ? tid - HT : tid;
 
     const int RS = p.R * p.S;
     const int tiles = RS * p.ctiles * p.ktiles;
@@ -95,113 +110,323 @@ __global__ __launch_bounds__(NT, 2) void bwd_weight_kernel(WeightParams p)
     const int ch_begin = z * p.chunks_per_split;
     const int ch_end = min(p.nchunks, ch_begin + p.chunks_per_split);
 
-    floatx4 acc[4][4];
+    floatx4 acc[FM][FN];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     const T* __restrict__ x = reinterpret_cast<const T*>(p.x);
     const T* __restrict__ dy = reinterpret_cast<const T*>(p.dy);
 
-    uint4 ra[BPT][E], rb[BPT][E];
+    uint4 rg[BPT][E];
     int skipped = 0;
 
+    const __amdgpu_buffer_rsrc_t rs_x = make_rsrc(p.x, p.x_bytes);
+    const __amdgpu_buffer_rsrc_t rs_dy = make_rsrc(p.dy, p.dy_bytes);
+    constexpr uint32_t ESZ = sizeof(T);
+
+    // Staging thread st owns blocks st + bi*HT: channel block cb, pixel block pb.
     auto load = [&](int chunk) {
         const int px_base = chunk * BK;
 #pragma unroll
         for (int bi = 0; bi < BPT; ++bi) {
-            const int blk = tid + bi * NT;
+            const int blk = st + bi * HT;
             const int cb = blk % CB, pb = blk / CB;
-            const int cA = c0 + cb * E;   // A: channel block of X
-            const int kB = k0 + cb * E;   // B: channel block of dY
+            const int pix0 = px_base + pb * E;
+            if (stage_b) {
+                const int kB = k0 + cb * E;
 #pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const int pix = px_base + pb * E + e;
-                ra[bi][e] = make_uint4(0, 0, 0, 0);
-                rb[bi][e] = make_uint4(0, 0, 0, 0);
-                if (pix < p.npq) {
-                    if (kB < p.K) rb[bi][e] = *reinterpret_cast<const uint4*>(dy + ((int64_t)pix * p.K + kB));
-                    if (cA < p.C) {
-                        const uint32_t nq = fdiv((uint32_t)pix, p.div_q);
-                        const int q = pix - (int)nq * p.Q;
-                        const uint32_t n = fdiv(nq, p.div_p);
-                        const int pp = (int)nq - (int)n * p.P;
-                        const int h = pp * p.stride_h - p.pad_h + r;
-                        const int w = q * p.stride_w - p.pad_w + s;
-                        if (h >= 0 && h < p.H && w >= 0 && w < p.W)
-                            ra[bi][e] = *reinterpret_cast<const uint4*>(
-                                x + ((((int64_t)n * p.H + h) * p.W + w) * p.C + cA));
+                for (int e = 0; e < E; ++e) {
+                    const int pix = pix0 + e;
+                    const bool ok = pix < p.npq && kB < p.K;
+                    rg[bi][e] = buf_load16(rs_dy, ok ? (uint32_t)(pix * p.K + kB) * ESZ : kOOB);
+                }
+            } else {
+                const int cA = c0 + cb * E;
+                // decode the block's first pixel once, then step along q
+                const uint32_t nq = fdiv((uint32_t)pix0, p.div_q);
+                int q = pix0 - (int)nq * p.Q;
+                const uint32_t nn = fdiv(nq, p.div_p);
+                int pp = (int)nq - (int)nn * p.P;
+                int n = (int)nn;
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const int h = pp * p.stride_h - p.pad_h + r;
+                    const int w = q * p.stride_w - p.pad_w + s;
+                    const bool ok = n < p.N && cA < p.C && h >= 0 && h < p.H && w >= 0 && w < p.W;
+                    rg[bi][e] = buf_load16(rs_x, ok ? (uint32_t)(((n * p.H + h) * p.W + w) * p.C + cA) * ESZ : kOOB);
+                    if (++q == p.Q) {
+                        q = 0;
+                        if (++pp == p.P) { pp = 0; ++n; }
                     }
                 }
             }
         }
     };
 
-    auto store = [&]() {
+    auto store = [&](int buf) {
+        uint4* dst = stage_b ? Bs[buf] : As[buf];
 #pragma unroll
         for (int bi = 0; bi < BPT; ++bi) {
-            const int blk = tid + bi * NT;
+            const int blk = st + bi * HT;
             const int cb = blk % CB, pb = blk / CB;
-            uint4 ua[E], ub[E];
-            transpose_block<T>(ra[bi], ua);
-            transpose_block<T>(rb[bi], ub);
+            uint4 u[E];
+            transpose_block<T>(rg[bi], u);
 #pragma unroll
             for (int j = 0; j < E; ++j) {
                 const int row = cb * E + j;
-                As[row * CHR + (pb ^ swz16(row))] = ua[j];
-                Bs[row * CHR + (pb ^ swz16(row))] = ub[j];
+                dst[row * CH + (pb ^ swz(row))] = u[j];
             }
         }
     };
 
-    auto live = [&](int chunk) { return p.occ == nullptr || p.occ[(int64_t)chunk * p.ktiles + kt] != 0; };
-
-    // advance to the first chunk that is not skipped
-    int chunk = ch_begin;
-    while (chunk < ch_end && !live(chunk)) { ++chunk; ++skipped; }
-    if (chunk < ch_end) load(chunk);
-    while (chunk < ch_end) {
-        __syncthreads();
-        store();
-        __syncthreads();
-        int next = chunk + 1;
-        while (next < ch_end && !live(next)) { ++next; ++skipped; }
-        if (next < ch_end) load(next);
+    auto compute = [&](int buf) {
 #pragma unroll
-        for (int kc = 0; kc < CHR / 4; ++kc) {
+        for (int kc = 0; kc < CH / 4; ++kc) {
             const int chl = kc * 4 + (lane >> 4);
-            uint4 fa[4], fb[4];
+            uint4 fa[FM], fb[FN];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int row = wm * 64 + i * 16 + (lane & 15);
-                fa[i] = As[row * CHR + (chl ^ swz16(row))];
+            for (int i = 0; i < FM; ++i) {
+                const int row = wm * TM + i * 16 + (lane & 15);
+                fa[i] = As[buf][row * CH + (chl ^ swz(row))];
             }
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int row = wn * 64 + j * 16 + (lane & 15);
-                fb[j] = Bs[row * CHR + (chl ^ swz16(row))];
+            for (int j = 0; j < FN; ++j) {
+                const int row = wn * TN + j * 16 + (lane & 15);
+                fb[j] = Bs[buf][row * CH + (chl ^ swz(row))];
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = mfma_chunk(acc[i][j], fa[i], fb[j], T{});
+                for (int j = 0; j < FN; ++j) acc[i][j] = mfma_chunk(acc[i][j], fa[i], fb[j], T{});
         }
+    };
+
+    auto live = [&](int chunk) { return p.occ == nullptr || p.occ[(int64_t)chunk * p.ktiles + kt] != 0; };
+    auto next_live = [&](int chunk) {
+        while (chunk < ch_end && !live(chunk)) { ++chunk; ++skipped; }
+        return chunk;
+    };
+
+    int chunk = next_live(ch_begin);
+    int buf = 0;
+    if (chunk < ch_end) {
+        load(chunk);
+        store(0);
+    }
+    __syncthreads();
+    while (chunk < ch_end) {
+        const int next = next_live(chunk + 1);
+        if (next < ch_end) load(next);
+        compute(buf);
+        if (next < ch_end) store(buf ^ 1);
+        __syncthreads();
+        buf ^= 1;
         chunk = next;
     }
 
     if (tid == 0) p.skip_slots[blockIdx.x] = skipped;
 
-    // Epilogue: lane holds channels c0 + wm*64 + i*16 + 4*(lane/16) + v of
-    // output channel k0 + wn*64 + j*16 + lane%16; written to [z][k][tap][c].
+    // Epilogue: lane holds channels c0 + wm*TM + i*16 + 4*(lane/16) + v of
+    // output channel k0 + wn*TN + j*16 + lane%16; written to [z][k][tap][c].
     float* __restrict__ out = p.out + (int64_t)z * p.K * RS * p.C;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int k = k0 + wn * 64 + j * 16 + (lane & 15);
+    for (int j = 0; j < FN; ++j) {
+        const int k = k0 + wn * TN + j * 16 + (lane & 15);
         if (k >= p.K) continue;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int c = c0 + wm * 64 + i * 16 + 4 * (lane >> 4);
+        for (int i = 0; i < FM; ++i) {
+            const int c = c0 + wm * TM + i * 16 + 4 * (lane >> 4);
+            if (c >= p.C) continue;
+            *reinterpret_cast<floatx4*>(out + (((int64_t)k * RS + tap) * p.C + c)) = acc[i][j];
+        }
+    }
+}
+
+// bf16 kernel with natural-layout staging.  Both operand tiles are copied
+// by the load unit straight into LDS in their NHWC order, one 512-byte row
+// (256 channels) per pixel: A_s[pixel][c], B_s[pixel][k].  The MFMA fragments
+// need 8 consecutive pixels of one channel per lane; ds_read_b64_tr_b16
+// delivers exactly that from the natural layout: within each group of 16
+// lanes, the lane at position q + 4m addresses the four channels
+// cbase+4q..cbase+4q+3 of pixel k0+m, and the lane at position j receives
+// channel cbase+j of pixels k0..k0+3.  Two such reads (pixels k0..k0+3 and
+// k0+4..k0+7) form one 16x16x32 operand fragment.  No register transposes,
+// no staging registers, no LDS store instructions.
+//
+// LDS rows are 32 chunks of 16 bytes; chunk c of pixel row r is stored at
+// c ^ trswz(r), which makes each 32-lane half of a transpose read hit 16
+// different chunk positions.
+__device__ __forceinline__ int trswz(int row) { return 2 * ((row & 3) | (((row >> 3) & 1) << 2)); }
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint2 ds_read_tr16(const void* lds)
+{
+    const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)lds);
+    return __builtin_bit_cast(uint2, v);
+}
+
+constexpr int TR_BK = 64;              // pixels per step
+constexpr int TR_ROW = BM / 8;         // 16-byte chunks per LDS row (one pixel)
+constexpr int TR_IA = TR_BK * BM * 2 / 1024 / (NT / 64);  // 1 KB copies per wave per step, per operand
+static_assert(BM == 256 && BN == 256, "the natural-layout kernel assumes 256-wide tiles");
+
+__global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
+{
+    constexpr uint32_t ESZ = 2;
+    constexpr int NW = NT / 64;
+    __shared__ uint4 As[2][TR_BK * TR_ROW];
+    __shared__ uint4 Bs[2][TR_BK * TR_ROW];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+
+    const int RS = p.R * p.S;
+    const int tiles = RS * p.ctiles * p.ktiles;
+    const int t = xcd_remap(blockIdx.x, gridDim.x);
+    const int z = t / tiles;
+    int rem = t - z * tiles;
+    const int kt = rem % p.ktiles;
+    rem /= p.ktiles;
+    const int ct = rem % p.ctiles;
+    const int tap = rem / p.ctiles;
+    const int r = tap / p.S, s = tap - r * p.S;
+    const int c0 = ct * BM, k0 = kt * BN;
+
+    if (blockIdx.x == 0 && tid == 0) p.header[0] = p.mode_flags;
+
+    const int ch_begin = z * p.chunks_per_split;
+    const int ch_end = min(p.nchunks, ch_begin + p.chunks_per_split);
+
+    const u32x4_t rs_x = make_rsrc_words(p.x, p.x_bytes);
+    const u32x4_t rs_dy = make_rsrc_words(p.dy, p.dy_bytes);
+
+    // Copy assignment: instruction j of a wave fills LDS rows 2g, 2g+1 with
+    // g = wave + NW*j; lane l serves row 2g + l/32 at physical chunk l%32,
+    // i.e. logical chunk (l%32) ^ trswz(row): channels 8*lc .. 8*lc+7.
+    int rowj[TR_IA];
+    uint32_t xch[TR_IA], dych[TR_IA];   // channel byte offset, kOOB for channels past the end
+    int xn[TR_IA], xp[TR_IA], xq[TR_IA];   // pixel coordinates of the row at the next chunk to load
+    int dpix[TR_IA];
+#pragma unroll
+    for (int j = 0; j < TR_IA; ++j) {
+        const int row = 2 * (wave + NW * j) + (lane >> 5);
+        const int lc = (lane & 31) ^ trswz(row);
+        rowj[j] = row;
+        xch[j] = (c0 + 8 * lc < p.C) ? (uint32_t)(c0 + 8 * lc) * ESZ : kOOB;
+        dych[j] = (k0 + 8 * lc < p.K) ? (uint32_t)(k0 + 8 * lc) * ESZ : kOOB;
+    }
+    auto set_chunk = [&](int chunk) {
+#pragma unroll
+        for (int j = 0; j < TR_IA; ++j) {
+            const int pix = chunk * TR_BK + rowj[j];
+            dpix[j] = pix;
+            const uint32_t nq = fdiv((uint32_t)pix, p.div_q);
+            xq[j] = pix - (int)nq * p.Q;
+            const uint32_t nn = fdiv(nq, p.div_p);
+            xp[j] = (int)nq - (int)nn * p.P;
+            xn[j] = (int)nn;
+        }
+    };
+
+    auto load = [&](int buf) {
+#pragma unroll
+        for (int j = 0; j < TR_IA; ++j) {
+            const int h = xp[j] * p.stride_h - p.pad_h + r;
+            const int w = xq[j] * p.stride_w - p.pad_w + s;
+            const bool ok = xn[j] < p.N && h >= 0 && h < p.H && w >= 0 && w < p.W;
+            const uint32_t xo = ok ? (uint32_t)(((xn[j] * p.H + h) * p.W + w) * p.C) * ESZ + xch[j] : kOOB;
+            buf_load16_lds(rs_x, xo, lds_addr(&As[buf][(wave_u + NW * j) * 2 * TR_ROW]));
+            const uint32_t yo = dpix[j] < p.npq ? (uint32_t)(dpix[j] * p.K) * ESZ + dych[j] : kOOB;
+            buf_load16_lds(rs_dy, yo, lds_addr(&Bs[buf][(wave_u + NW * j) * 2 * TR_ROW]));
+        }
+    };
+
+    // Per-lane transpose-read addresses (bytes within a buffer): for fragment
+    // base channel cb and k-step kc, lane (kg = lane/16, q = lane%4,
+    // m = (lane%16)/4) reads row kc*32 + 8*kg + m (+4), channels cb+4q..+3.
+    const int kg = lane >> 4, q4 = lane & 3, m4 = (lane >> 2) & 3;
+    auto tr_addr = [&](int row, int cb) {
+        const int col = cb + 4 * q4;
+        return row * (TR_ROW * 16) + (((col >> 3) ^ trswz(row)) << 4) + ((col & 7) << 1);
+    };
+
+    floatx4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    auto compute = [&](int buf) {
+        const char* Ab = reinterpret_cast<const char*>(As[buf]);
+        const char* Bb = reinterpret_cast<const char*>(Bs[buf]);
+#pragma unroll
+        for (int kc = 0; kc < TR_BK / 32; ++kc) {
+            const int r0 = kc * 32 + 8 * kg + m4;
+            uint4 fa[FM], fb[FN];
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int cb = wm * TM + i * 16;
+                const uint2 lo = ds_read_tr16(Ab + tr_addr(r0, cb));
+                const uint2 hi = ds_read_tr16(Ab + tr_addr(r0 + 4, cb));
+                fa[i] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+            }
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int cb = wn * TN + j * 16;
+                const uint2 lo = ds_read_tr16(Bb + tr_addr(r0, cb));
+                const uint2 hi = ds_read_tr16(Bb + tr_addr(r0 + 4, cb));
+                fb[j] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+            }
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) acc[i][j] = mfma_chunk(acc[i][j], fa[i], fb[j], uint16_t{});
+        }
+    };
+
+    auto live = [&](int chunk) { return p.occ == nullptr || p.occ[(int64_t)chunk * p.ktiles + kt] != 0; };
+    int skipped = 0;
+    auto next_live = [&](int chunk) {
+        while (chunk < ch_end && !live(chunk)) { ++chunk; ++skipped; }
+        return chunk;
+    };
+
+    int chunk = next_live(ch_begin);
+    int buf = 0;
+    if (chunk < ch_end) {
+        set_chunk(chunk);
+        load(0);
+    }
+    wait_vmem();
+    __syncthreads();
+    while (chunk < ch_end) {
+        const int next = next_live(chunk + 1);
+        if (next < ch_end) {
+            set_chunk(next);
+            load(buf ^ 1);
+        }
+        compute(buf);
+        wait_vmem();
+        __syncthreads();
+        buf ^= 1;
+        chunk = next;
+    }
+
+    if (tid == 0) p.skip_slots[blockIdx.x] = skipped;
+
+    float* __restrict__ out = p.out + (int64_t)z * p.K * RS * p.C;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+        const int k = k0 + wn * TN + j * 16 + (lane & 15);
+        if (k >= p.K) continue;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int c = c0 + wm * TM + i * 16 + 4 * (lane >> 4);
             if (c >= p.C) continue;
             *reinterpret_cast<floatx4*>(out + (((int64_t)k * RS + tap) * p.C + c)) = acc[i][j];
         }
@@ -212,12 +437,12 @@ __global__ __launch_bounds__(NT, 2) void bwd_weight_kernel(WeightParams p)
 
 int weight_tile_channels() { return BM; }
 int weight_tile_k() { return BN; }
-int weight_chunk(int dtype) { return CHR * (dtype == 1 ? 8 : 4); }
+int weight_chunk(int dtype) { return CH * (dtype == 1 ? 8 : 4); }
 
 hipError_t launch_bwd_weight(int dtype, const WeightParams& p, hipStream_t stream)
 {
     const int nb = p.R * p.S * p.ctiles * p.ktiles * p.nsplit;
-    if (dtype == 1) bwd_weight_kernel<uint16_t><<<nb, NT, 0, stream>>>(p);
+    if (dtype == 1) bwd_weight_tr_kernel<<<nb, NT, 0, stream>>>(p);
     else bwd_weight_kernel<float><<<nb, NT, 0, stream>>>(p);
     return hipGetLastError();
 }

@@ -72,6 +72,66 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f)
     return (__umulhi(n, f.m) + n) >> f.s;
 }
 
+// Raw buffer access.  Loads through a buffer descriptor return zeros for
+// byte offsets at or past the buffer's size, which the kernels use for
+// padding, halo and ragged edges: an invalid element gets offset kOOB.
+// Buffers must be smaller than 2^31 bytes so that kOOB plus any in-range
+// offset never wraps.
+constexpr uint32_t kOOB = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off)
+{
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Direct global-to-LDS copy of 16 bytes per lane: lane l's 16 bytes land at
+// LDS byte address lds_base + 16*l (lds_base is wave-uniform); lanes with an
+// out-of-range offset write zeros.  The copy is issued from inline assembly
+// so that the compiler does not track it: its completion (vmcnt) is awaited
+// explicitly with wait_vmem() before the barrier that publishes the data,
+// which keeps the copy of the next step in flight during the MFMAs of the
+// current one.  M0 is saved and restored around the copy.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4_t make_rsrc_words(const void* p, uint32_t bytes)
+{
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    u32x4_t r;
+    r.x = (uint32_t)a;
+    r.y = (uint32_t)(a >> 32) & 0xffffu;  // stride 0
+    r.z = bytes;
+    r.w = 0x00020000u;
+    return r;
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p)
+{
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+__device__ __forceinline__ void buf_load16_lds(const u32x4_t& rsrc, uint32_t off, uint32_t lds_base)
+{
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(off), "s"(rsrc), "s"(lds_base));
+}
+
+// Wait until all of this wave's vector memory operations have completed.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+
 // XCD-aware block order.  The dispatcher hands consecutive workgroups to the
 // eight XCDs in turn; this maps the j-th workgroup an XCD receives to the
 // j-th tile of a contiguous range owned by that XCD, so tiles that share

@@ -21,6 +21,7 @@ struct DataParams {
     int stride_h, stride_w, pad_h, pad_w;
     int npix;                // N*H*W
     int ctiles;              // channel tiles = compaction groups
+    uint32_t dy_bytes, wt_bytes;
     FastDiv div_w, div_h;    // pixel -> (n, h, w)
 };
 
@@ -47,6 +48,7 @@ struct WeightParams {
     int chunks_per_split;
     int ctiles, ktiles, nsplit;
     int mode_flags;
+    uint32_t x_bytes, dy_bytes;
     FastDiv div_q, div_p;    // pixel -> (n, p, q)
 };
 

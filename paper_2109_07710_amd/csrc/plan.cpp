@@ -38,6 +38,9 @@ int validate_desc(const cbw_conv_desc* d)
     if (d->C % E != 0 || d->K % E != 0) return CBW_ERR_UNSUPPORTED;
     const int64_t npix = (int64_t)d->N * d->H * d->W, npq = (int64_t)d->N * d->P * d->Q;
     if (npix * d->C >= kMaxElems || npq * d->K >= kMaxElems) return CBW_ERR_UNSUPPORTED;
+    // every tensor the kernels read through a buffer descriptor stays below 2^31 bytes
+    const int64_t esz = d->dtype == CBW_BF16 ? 2 : 4;
+    if (npix * d->C * esz >= kMaxElems || npq * d->K * esz >= kMaxElems) return CBW_ERR_UNSUPPORTED;
     if ((int64_t)d->K * d->C * d->R * d->S >= kMaxElems) return CBW_ERR_UNSUPPORTED;
     if (d->K > 1024 * kWeightTileK) return CBW_ERR_UNSUPPORTED;  // occupancy flags per chunk
     return CBW_OK;
@@ -75,7 +78,8 @@ int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
     p.ctiles = (d->C + kWeightTileC - 1) / kWeightTileC;
     p.ktiles = (d->K + kWeightTileK - 1) / kWeightTileK;
     const int tiles = d->R * d->S * p.ctiles * p.ktiles;
-    int nsplit = (kTargetWorkgroups + tiles - 1) / tiles;
+    // as many splits as fit in one round of resident workgroups
+    int nsplit = kWeightSlots / tiles;
     int max_split = p.nchunks / 4;  // at least four chunks per workgroup
     if (max_split < 1) max_split = 1;
     if (nsplit > max_split) nsplit = max_split;

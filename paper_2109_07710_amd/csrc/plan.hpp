@@ -6,18 +6,20 @@
 #include <stdint.h>
 
 #include "../../include/convbwd.h"
+#include "tiles.hpp"
 
 namespace cbw {
 
 // Tile constants shared with the kernels (asserted equal at dispatch time).
-constexpr int kDataTileC = 128;     // channels per data-gradient tile = compaction group width
-constexpr int kDataTileP = 128;     // pixels per data-gradient tile
-constexpr int kWeightTileC = 128;   // channels c per weight-gradient tile
-constexpr int kWeightTileK = 128;   // output channels k per weight-gradient tile
-constexpr int kCompactBlock = 1024; // pixels per compaction block
-constexpr int kTargetWorkgroups = 512;  // 256 CUs x 2 resident workgroups
+constexpr int kDataTileC = CBW_DX_BM;   // channels per data-gradient tile = compaction group width
+constexpr int kDataTileP = CBW_DX_BN;   // pixels per data-gradient tile
+constexpr int kWeightTileC = CBW_DW_BM; // channels c per weight-gradient tile
+constexpr int kWeightTileK = CBW_DW_BN; // output channels k per weight-gradient tile
+constexpr int kCompactBlock = 1024;     // pixels per compaction block
+// Resident weight-gradient workgroups the split-K factor aims to fill exactly.
+constexpr int kWeightSlots = CBW_NUM_CUS * CBW_DW_OCC;
 
-inline int weight_chunk_px(int dtype) { return 16 * (dtype == CBW_BF16 ? 8 : 4); }
+inline int weight_chunk_px(int dtype) { return 8 * (dtype == CBW_BF16 ? 8 : 4); }
 
 struct Region {
     size_t off = 0, bytes = 0;
