@@ -91,7 +91,7 @@ def test_workspace_sizes(L):
     wt_bytes = 256 * 256 * 9 * 2
     assert dense >= wt_bytes + 256
     npix = 32 * 56 * 56
-    assert masked >= dense + 2 * npix * 4          # two channel groups of live-pixel lists
+    assert masked >= dense + npix * 4              # at least one channel group of live-pixel lists
     assert wgt >= 2 * 256 * 9 * 256 * 4            # at least two split-K partials of dW
     assert all(x % 256 == 0 for x in (dense, masked))
     with pytest.raises(cb.CbwError):
