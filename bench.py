@@ -1,6 +1,6 @@
 """Benchmark of the masked convolution backward pass (dX + dW) on one MI355X.
 
-    python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--no-cpu]
+    python bench.py [--gpus 1] [--steps 50] [--warmup 200] [--no-cpu]
 
 Workload: the VGG-style 3x3 layer N=32, C=K=256, 56x56, stride 1, pad 1,
 bf16 inputs with fp32 accumulation; X = relu(N(0,1) - 0.25) (footprint
@@ -8,9 +8,10 @@ density 0.401), dY = N(0,1) * Bernoulli(0.4), He-initialised W; seeded
 synthetic data.  Inputs (X, W, dY and the two packed footprints) are resident
 in device memory before timing starts.
 
-One step is the whole sparse backward of the layer:
-  compaction of the X footprint + masked data-gradient GEMM (conv_bwd_data_masked)
-  + dY block occupancy + weight-gradient GEMM + split-K reduce (conv_bwd_weight_sparse).
+One step is the whole sparse backward of the layer, on one stream:
+  compaction of the X footprint + masked data-gradient GEMM (conv_bwd_data_masked),
+  then dY block occupancy + weight-gradient GEMM + split-K reduce
+  (conv_bwd_weight_sparse).
 The dense comparison step runs the same kernels with skipping off:
   conv_bwd_data + conv_bwd_weight_sparse(CBW_FLAG_NO_SKIP).
 Footprint packing (cbw_relu_mask_pack, cbw_nonzero_mask_pack) belongs to the
@@ -38,7 +39,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU baseline time budget")
     return ap.parse_args()
@@ -82,13 +83,28 @@ def main():
         cb.cbw_relu_mask_pack(desc, x, xm)
         cb.cbw_nonzero_mask_pack(desc.dtype, dy.numel(), dy, dym)
 
-    def sparse_step():
+    def sparse_dx():
         cb.conv_bwd_data_masked(desc, dy, w, xm, dx, ws_m, 0)
+
+    def sparse_dw():
         cb.conv_bwd_weight_sparse(desc, x, dy, dym, dw, ws_w, 0)
 
-    def dense_step():
+    def dense_dx():
         cb.conv_bwd_data(desc, dy, w, dx, ws_d)
+
+    def dense_dw():
         cb.conv_bwd_weight_sparse(desc, x, dy, None, dw, ws_w, cb.CBW_FLAG_NO_SKIP)
+
+    # One stream, data gradient then weight gradient.  (Forking the two
+    # independent gradients onto two streams was measured slower: both GEMMs
+    # want every CU.)
+    def sparse_step():
+        sparse_dx()
+        sparse_dw()
+
+    def dense_step():
+        dense_dx()
+        dense_dw()
 
     def timed(fn, steps, per_kernel=False):
         """Mean ms per call of fn over `steps` back-to-back calls, HIP events

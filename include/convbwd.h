@@ -132,7 +132,7 @@ int conv_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, void
 /* Masked data gradient (output sparsity, Sec. III-B; output-bitmap-driven
  * address generation, Sec. IV-B): only outputs whose x_mask bit is set are
  * computed; all others are written as +0.0 (bit pattern 0).  x_mask is the
- * packed footprint of X (cbw_relu_mask_pack).  The footprint is compacted per
+ * packed footprint of X (cbw_relu_mask_pack), 16-byte aligned.  The footprint is compacted per
  * channel group into ascending lists of live pixels and the GEMM runs only
  * over those rows; flags = CBW_FLAG_NO_SKIP computes every row instead.
  * Workspace: cbw_workspace_size(desc, CBW_OP_BWD_DATA_MASKED). */
@@ -145,8 +145,8 @@ int conv_bwd_data_masked(const cbw_conv_desc* desc, const void* dY, const void* 
  * dY[N,P,Q,K].  Blocks of (pixel chunk x output-channel tile) in which dY is
  * entirely zero are skipped; the skipped products are exactly zero.  dy_mask
  * (nullable) is a packed dY footprint (cbw_nonzero_mask_pack or the next
- * layer's ReLU bitmap, any superset of dY's non-zeros); when NULL the
- * occupancy is read from dY itself.  The result is deterministic: partial
+ * layer's ReLU bitmap, any superset of dY's non-zeros; 16-byte aligned);
+ * when NULL the occupancy is read from dY itself.  The result is deterministic: partial
  * sums are reduced in a fixed order.  dW is fully overwritten.
  * Workspace: cbw_workspace_size(desc, CBW_OP_BWD_WEIGHT). */
 int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void* dY,

@@ -83,14 +83,10 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
     const int mode = !masked ? MODE_DENSE : (gather ? MODE_GATHER : MODE_SELECT);
     int* header = at<int>(ws, plan.header);
     void* wt = at<void>(ws, plan.wt);
-    hipError_t e = launch_transform_filters(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S,
-                                            desc->w_layout == CBW_KRSC, header, mode, s);
-    if (e != hipSuccess) return hip_status(e);
-
     DataParams p = data_params(desc, dY, wt, dX, plan.npix, plan.groups);
     p.mask = x_mask;
+    CompactParams cp{};
     if (gather) {
-        CompactParams cp{};
         cp.mask = x_mask;
         cp.blk_counts = at<int32_t>(ws, plan.blk_counts);
         cp.counts = at<int32_t>(ws, plan.counts);
@@ -102,10 +98,13 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
         cp.groups = plan.groups;
         cp.nblk = plan.nblk;
         cp.elem_bytes = elem_bytes(desc->dtype);
-        if ((e = launch_compact(cp, s)) != hipSuccess) return hip_status(e);
         p.lists = cp.lists;
         p.counts = cp.counts;
     }
+    hipError_t e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S,
+                                    desc->w_layout == CBW_KRSC, header, mode, gather ? &cp : nullptr, s);
+    if (e != hipSuccess) return hip_status(e);
+    if (gather && (e = launch_compact_scatter(cp, s)) != hipSuccess) return hip_status(e);
     if ((e = prof_mark(0, 0, s)) != hipSuccess) return hip_status(e);
     if ((e = launch_bwd_data(desc->dtype, mode, p, s)) != hipSuccess) return hip_status(e);
     return hip_status(prof_mark(0, 1, s));
@@ -198,7 +197,7 @@ int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void*
     int st = plan_weight(desc, &plan);
     if (st != CBW_OK) return st;
     if (!X || !dY || !dW) return CBW_ERR_INVALID_ARG;
-    if (!aligned16(X) || !aligned16(dY) || !aligned16(dW) || ((uintptr_t)dy_mask & 3u))
+    if (!aligned16(X) || !aligned16(dY) || !aligned16(dW) || !aligned16(dy_mask))
         return CBW_ERR_UNSUPPORTED;
     if ((st = check_ws(workspace, workspace_bytes, plan.total)) != CBW_OK) return st;
     if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;

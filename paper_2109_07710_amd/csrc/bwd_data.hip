@@ -26,6 +26,7 @@
 // consecutive rows spread over all banks.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "footprint.hpp"
 #include "tiles.hpp"
 
 
@@ -75,30 +76,12 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
     if (MODE == MODE_GATHER) nrows = p.counts[ctile];
     if (row0 >= nrows) return;  // uniform across the workgroup
 
-    for (int i = tid; i < BN; i += NT) {
-        const int r = row0 + i;
-        int pix = -1;
-        if (r < nrows) pix = (MODE == MODE_GATHER) ? p.lists[(int64_t)ctile * p.npix + r] : r;
-        pix_s[i] = pix;
-    }
-    __syncthreads();
-
-    // Footprint bits of the tile (pixel row x 32-channel word), staged once;
-    // valid when every pixel's group of BM channels starts on a word.
-    const bool mask_lds = MODE != MODE_DENSE && (p.C % 32) == 0;
-    if (mask_lds) {
-        for (int i = tid; i < BN * (BM / 32); i += NT) {
-            const int pr = i / (BM / 32), wi = i - pr * (BM / 32);
-            const int pix = pix_s[pr];
-            uint32_t word = 0;
-            if (pix >= 0 && c0 + 32 * wi < p.C) word = p.mask[((int64_t)pix * p.C + c0) / 32 + wi];
-            msk_s[i] = word;
-        }
-    }
-
     const u32x4_t rs_wt = make_rsrc_words(p.wt, p.wt_bytes);
     const u32x4_t rs_dy = make_rsrc_words(p.dy, p.dy_bytes);
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const int kchunks = (p.K + BK - 1) / BK;
+    const int nsteps = p.R * p.S * kchunks;
+    const bool kfull = (p.K % BK) == 0;
 
     // Staging: every wave copies whole groups of 8 LDS rows (1 KB) straight
     // from global memory into LDS.  Row group g = wave + NW*j; lane l serves
@@ -114,6 +97,30 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
         a_lc[j] = lc;
         a_off[j] = (row < BM && c < p.C) ? (uint32_t)(c * p.K + lc * E) * ESZ : kOOB;
     }
+    // Queue the copies of step (tap, k0) into LDS buffer `buf`.  The A part
+    // (filters) does not depend on the pixel list, so step 0's is issued
+    // before the list is read.
+    auto load_a = [&](int buf, int tap, int k0) {
+        const uint32_t a_step = (uint32_t)((tap * p.C) * p.K + k0) * ESZ;
+#pragma unroll
+        for (int j = 0; j < IA; ++j) {
+            const int g = wave + NW * j;
+            if (IA * NW * 8 == BM || g * 8 < BM) {
+                const bool kin = kfull || (k0 + a_lc[j] * E < p.K);
+                buf_load16_lds(rs_wt, kin ? a_off[j] + a_step : kOOB,
+                               lds_addr(&As[buf][(wave_u + NW * j) * 8 * CH]));
+            }
+        }
+    };
+    load_a(0, 0, 0);
+
+    for (int i = tid; i < BN; i += NT) {
+        const int r = row0 + i;
+        int pix = -1;
+        if (r < nrows) pix = (MODE == MODE_GATHER) ? p.lists[(int64_t)ctile * p.npix + r] : r;
+        pix_s[i] = pix;
+    }
+    __syncthreads();
     int bn_[IB], bh_[IB], bw_[IB], bbase[IB], b_lc[IB];
 #pragma unroll
     for (int j = 0; j < IB; ++j) {
@@ -138,10 +145,6 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
     for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-    const int kchunks = (p.K + BK - 1) / BK;
-    const int nsteps = p.R * p.S * kchunks;
-    const bool kfull = (p.K % BK) == 0;
 
     uint32_t b_off[IB];   // B byte offset for the current tap, kOOB when the tap misses
     int ld_tap = 0, ld_kc = 0;  // next step to load
@@ -170,21 +173,8 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
         }
     };
 
-    // Queue the copies of the next step into LDS buffer `buf`.
-    auto load = [&](int buf) {
-        if (ld_kc == 0) set_tap(ld_tap);
-        const int k0 = ld_kc * BK;
-        const uint32_t a_step = (uint32_t)((ld_tap * p.C) * p.K + k0) * ESZ;
+    auto load_b = [&](int buf, int k0) {
         const uint32_t b_step = (uint32_t)k0 * ESZ;
-#pragma unroll
-        for (int j = 0; j < IA; ++j) {
-            const int g = wave + NW * j;
-            if (IA * NW * 8 == BM || g * 8 < BM) {
-                const bool kin = kfull || (k0 + a_lc[j] * E < p.K);
-                buf_load16_lds(rs_wt, kin ? a_off[j] + a_step : kOOB,
-                               lds_addr(&As[buf][(wave_u + NW * j) * 8 * CH]));
-            }
-        }
 #pragma unroll
         for (int j = 0; j < IB; ++j) {
             const int g = wave + NW * j;
@@ -194,6 +184,12 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
                                lds_addr(&Bs[buf][(wave_u + NW * j) * 8 * CH]));
             }
         }
+    };
+    auto load = [&](int buf) {
+        if (ld_kc == 0) set_tap(ld_tap);
+        const int k0 = ld_kc * BK;
+        load_a(buf, ld_tap, k0);
+        load_b(buf, k0);
         if (++ld_kc == kchunks) { ld_kc = 0; ++ld_tap; }
     };
 
@@ -219,7 +215,22 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
         }
     };
 
-    load(0);
+    // Prologue: step 0's B copies, then the footprint bits of the tile
+    // (pixel row x 32-channel word, valid when every pixel's group of BM
+    // channels starts on a word) while the copies are in flight.
+    set_tap(0);
+    load_b(0, 0);
+    if (++ld_kc == kchunks) { ld_kc = 0; ++ld_tap; }
+    const bool mask_lds = MODE != MODE_DENSE && (p.C % 32) == 0;
+    if (mask_lds) {
+        for (int i = tid; i < BN * (BM / 32); i += NT) {
+            const int pr = i / (BM / 32), wi = i - pr * (BM / 32);
+            const int pix = pix_s[pr];
+            uint32_t word = 0;
+            if (pix >= 0 && c0 + 32 * wi < p.C) word = p.mask[((int64_t)pix * p.C + c0) / 32 + wi];
+            msk_s[i] = word;
+        }
+    }
     wait_vmem();
     __syncthreads();
     for (int step = 0; step < nsteps; ++step) {
@@ -268,22 +279,48 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
     }
 }
 
-// Wt[tap][c][k] = W[k][tap][c] (KRSC) or W[k][c][tap] (KCRS).  Also stamps the
-// workspace header with the call's mode.
+// Wt[tap][c][k] = W[k][tap][c] (KRSC) or W[k][c][tap] (KCRS).  Threads run
+// along k (coalesced stores); a KRSC thread reads one 16-byte vector of E
+// channels, a KCRS thread the R*S taps of one (k, c).  Returns after its part.
 template <typename T>
-__global__ void transform_filters_kernel(const T* __restrict__ w, T* __restrict__ wt, int K, int C, int RS,
-                                         int krsc, int* header, int mode)
+__device__ __forceinline__ void transform_filters(const T* __restrict__ w, T* __restrict__ wt, int K, int C, int RS,
+                                                  int krsc, int64_t t)
 {
-    const int64_t total = (int64_t)K * C * RS;
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i == 0 && header) header[0] = mode;
-    if (i >= total) return;
-    const int k = (int)(i % K);
-    const int64_t tc = i / K;
-    const int c = (int)(tc % C);
-    const int tap = (int)(tc / C);
-    const int64_t srci = krsc ? ((int64_t)k * RS + tap) * C + c : ((int64_t)k * C + c) * RS + tap;
-    wt[i] = w[srci];
+    constexpr int E = Elem<T>::E;
+    if (krsc) {
+        const int CV = C / E;
+        if (t >= (int64_t)K * RS * CV) return;
+        const int k = (int)(t % K);
+        const int64_t rest = t / K;
+        const int cv = (int)(rest % CV);
+        const int tap = (int)(rest / CV);
+        const uint4 v = *reinterpret_cast<const uint4*>(w + ((int64_t)k * RS + tap) * C + cv * E);
+        const T* e = reinterpret_cast<const T*>(&v);
+#pragma unroll
+        for (int i = 0; i < E; ++i) wt[((int64_t)tap * C + cv * E + i) * K + k] = e[i];
+    } else {
+        if (t >= (int64_t)K * C) return;
+        const int k = (int)(t % K);
+        const int c = (int)(t / K);
+        for (int tap = 0; tap < RS; ++tap) wt[((int64_t)tap * C + c) * K + k] = w[((int64_t)k * C + c) * RS + tap];
+    }
+}
+
+// One launch for the data gradient's preparation: blocks [0, ntb) transform
+// the filters (block 0 also stamps the workspace header), the remaining
+// blocks count live pixels per compaction block (gather mode).
+template <typename T>
+__global__ __launch_bounds__(256) void data_prep_kernel(const T* __restrict__ w, T* __restrict__ wt, int K, int C,
+                                                        int RS, int krsc, int* header, int mode, int ntb,
+                                                        CompactParams cp)
+{
+    if ((int)blockIdx.x < ntb) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) header[0] = mode;
+        transform_filters<T>(w, wt, K, C, RS, krsc, (int64_t)blockIdx.x * 256 + threadIdx.x);
+        return;
+    }
+    const int b = blockIdx.x - ntb;
+    compact_count_block(cp, b % cp.nblk, b / cp.nblk);
 }
 
 }  // namespace
@@ -291,17 +328,24 @@ __global__ void transform_filters_kernel(const T* __restrict__ w, T* __restrict_
 int data_tile_channels() { return BM; }
 int data_tile_pixels() { return BN; }
 
-hipError_t launch_transform_filters(int dtype, const void* w, void* wt, int K, int C, int RS, int krsc,
-                                    int* header, int mode, hipStream_t stream)
+hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, int RS, int krsc, int* header,
+                            int mode, const CompactParams* cp, hipStream_t stream)
 {
-    const int64_t total = (int64_t)K * C * RS;
-    const int blocks = (int)((total + 255) / 256);
+    const int E = dtype == 1 ? 8 : 4;
+    const int64_t nthreads = krsc ? (int64_t)K * RS * (C / E) : (int64_t)K * C;
+    const int ntb = (int)((nthreads + 255) / 256);
+    CompactParams c{};
+    int ncb = 0;
+    if (cp) {
+        c = *cp;
+        ncb = c.nblk * c.groups;
+    }
     if (dtype == 1)
-        transform_filters_kernel<uint16_t><<<blocks, 256, 0, stream>>>(
-            (const uint16_t*)w, (uint16_t*)wt, K, C, RS, krsc, header, mode);
+        data_prep_kernel<uint16_t><<<ntb + ncb, 256, 0, stream>>>((const uint16_t*)w, (uint16_t*)wt, K, C, RS, krsc,
+                                                                  header, mode, ntb, c);
     else
-        transform_filters_kernel<float><<<blocks, 256, 0, stream>>>(
-            (const float*)w, (float*)wt, K, C, RS, krsc, header, mode);
+        data_prep_kernel<float><<<ntb + ncb, 256, 0, stream>>>((const float*)w, (float*)wt, K, C, RS, krsc, header,
+                                                               mode, ntb, c);
     return hipGetLastError();
 }
 

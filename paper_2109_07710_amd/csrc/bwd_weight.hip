@@ -35,6 +35,7 @@ constexpr int HT = NT / 2;      // staging threads per operand
 constexpr int TM = BM / WM, TN = BN / WN;
 constexpr int FM = TM / 16, FN = TN / 16;
 constexpr int CH = 8;           // 16-byte chunks per LDS row (128 bytes)
+constexpr int OCC_WIN = 1024;   // occupancy bytes cached per workgroup
 static_assert(BM == BN, "both operands share the staging layout");
 
 // Chunk swizzle: bijective on 16 consecutive rows (fragment reads) and
@@ -203,7 +204,21 @@ __global__ __launch_bounds__(NT) void bwd_weight_kernel(WeightParams p)
         }
     };
 
-    auto live = [&](int chunk) { return p.occ == nullptr || p.occ[(int64_t)chunk * p.ktiles + kt] != 0; };
+    // The occupancy bytes of this workgroup's chunk range are read once into
+    // LDS (up to OCC_WIN of them); the loop then tests them without a global
+    // read on its critical path.
+    __shared__ uint8_t occ_s[OCC_WIN];
+    if (p.occ) {
+        for (int i = tid; i < OCC_WIN && ch_begin + i < ch_end; i += NT)
+            occ_s[i] = p.occ[(int64_t)(ch_begin + i) * p.ktiles + kt];
+    }
+    __syncthreads();
+    auto live = [&](int chunk) {
+        if (p.occ == nullptr) return true;
+        const int i = chunk - ch_begin;
+        const int v = i < OCC_WIN ? occ_s[i] : p.occ[(int64_t)chunk * p.ktiles + kt];
+        return __builtin_amdgcn_readfirstlane(v) != 0;  // the same byte for the whole workgroup
+    };
     auto next_live = [&](int chunk) {
         while (chunk < ch_end && !live(chunk)) { ++chunk; ++skipped; }
         return chunk;
@@ -389,7 +404,21 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
         }
     };
 
-    auto live = [&](int chunk) { return p.occ == nullptr || p.occ[(int64_t)chunk * p.ktiles + kt] != 0; };
+    // The occupancy bytes of this workgroup's chunk range are read once into
+    // LDS (up to OCC_WIN of them); the loop then tests them without a global
+    // read on its critical path.
+    __shared__ uint8_t occ_s[OCC_WIN];
+    if (p.occ) {
+        for (int i = tid; i < OCC_WIN && ch_begin + i < ch_end; i += NT)
+            occ_s[i] = p.occ[(int64_t)(ch_begin + i) * p.ktiles + kt];
+    }
+    __syncthreads();
+    auto live = [&](int chunk) {
+        if (p.occ == nullptr) return true;
+        const int i = chunk - ch_begin;
+        const int v = i < OCC_WIN ? occ_s[i] : p.occ[(int64_t)chunk * p.ktiles + kt];
+        return __builtin_amdgcn_readfirstlane(v) != 0;  // the same byte for the whole workgroup
+    };
     int skipped = 0;
     auto next_live = [&](int chunk) {
         while (chunk < ch_end && !live(chunk)) { ++chunk; ++skipped; }

@@ -118,6 +118,7 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p)
 
 __device__ __forceinline__ void buf_load16_lds(const u32x4_t& rsrc, uint32_t off, uint32_t lds_base)
 {
+    lds_base = __builtin_amdgcn_readfirstlane(lds_base);  // wave-uniform by contract
     uint32_t saved;
     asm volatile(
         "s_mov_b32 %0, m0\n\t"

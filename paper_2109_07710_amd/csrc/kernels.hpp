@@ -66,10 +66,11 @@ int weight_tile_k();
 int weight_chunk(int dtype);
 int compact_block_pixels();
 
-hipError_t launch_transform_filters(int dtype, const void* w, void* wt, int K, int C, int RS, int krsc,
-                                    int* header, int mode, hipStream_t stream);
+// Filter transform (and, when cp is given, the compaction count) in one launch.
+hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, int RS, int krsc, int* header,
+                            int mode, const CompactParams* cp, hipStream_t stream);
 hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream);
-hipError_t launch_compact(const CompactParams& p, hipStream_t stream);
+hipError_t launch_compact_scatter(const CompactParams& p, hipStream_t stream);
 hipError_t launch_relu_mask_pack(int dtype, int64_t count, const void* x, uint32_t* bits, int relu,
                                  hipStream_t stream);
 hipError_t launch_occupancy(const OccParams& p, hipStream_t stream);

@@ -2,32 +2,14 @@
 // of live pixels, dY block occupancy and the split-K reduction of dW.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "footprint.hpp"
 
 namespace cbw {
 
 namespace {
 
-constexpr int CNT = 256;                 // threads per compaction block
-constexpr int PX_PER_THREAD = 4;
-constexpr int BLK_PX = CNT * PX_PER_THREAD;
-
-// Any bit set in the bit range [lo, hi) of a packed bitmap.
-__device__ __forceinline__ bool any_bits(const uint32_t* __restrict__ bits, int64_t lo, int64_t hi)
-{
-    if (lo >= hi) return false;
-    int64_t w0 = lo >> 5, w1 = (hi - 1) >> 5;
-    uint32_t acc = 0;
-    for (int64_t w = w0; w <= w1; ++w) {
-        uint32_t v = bits[w];
-        if (w == w0) v &= 0xffffffffu << (lo & 31);
-        if (w == w1) {
-            const int top = (int)((hi - 1) & 31);
-            v &= (top == 31) ? 0xffffffffu : ((2u << top) - 1u);
-        }
-        acc |= v;
-    }
-    return acc != 0;
-}
+constexpr int CNT = kCompactThreads;     // threads (= pixels) per compaction block
+constexpr int BLK_PX = CNT;
 
 // Bit per element: relu ? (value > 0) : (value != 0), over 16-byte vectors.
 template <typename T>
@@ -88,90 +70,48 @@ __global__ void mask_pack_kernel(const T* __restrict__ x, uint32_t* __restrict__
     if (lane % L == 0 && v < nvec) bits[v / L] = b;
 }
 
-__device__ __forceinline__ bool pixel_live(const CompactParams& p, int px, int g)
-{
-    if (px >= p.npix) return false;
-    const int64_t base = (int64_t)px * p.C;
-    const int lo = g * p.G;
-    const int hi = min(p.C, lo + p.G);
-    return any_bits(p.mask, base + lo, base + hi);
-}
 
-// Block sum of one int per thread (CNT threads, 4 waves).
-__device__ __forceinline__ int block_sum(int v, int* red)
-{
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    __syncthreads();
-    if (lane == 0) red[wave] = v;
-    __syncthreads();
-    return red[0] + red[1] + red[2] + red[3];
-}
-
-__global__ __launch_bounds__(CNT) void compact_count_kernel(CompactParams p)
-{
-    __shared__ int red[4];
-    const int blk = blockIdx.x, g = blockIdx.y;
-    int cnt = 0;
-#pragma unroll
-    for (int i = 0; i < PX_PER_THREAD; ++i)
-        cnt += pixel_live(p, blk * BLK_PX + threadIdx.x * PX_PER_THREAD + i, g) ? 1 : 0;
-    const int tot = block_sum(cnt, red);
-    if (threadIdx.x == 0) p.blk_counts[(int64_t)g * p.nblk + blk] = tot;
-}
-
-// Writes the ascending list of live pixels of group g and zero-fills the dX
-// rows of pixels dead for the whole group.
+// Writes the ascending list of live pixels of group g (rank = live pixels
+// before it in the block, by wave ballot and popcount, plus the counts of all
+// earlier blocks) and zero-fills the dX rows of pixels dead for the group.
 __global__ __launch_bounds__(CNT) void compact_scatter_kernel(CompactParams p)
 {
     __shared__ int red[4];
-    __shared__ int wsum[4];
+    __shared__ int wcnt[4];
     const int blk = blockIdx.x, g = blockIdx.y;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
     int before = 0;
     for (int b = tid; b < blk; b += CNT) before += p.blk_counts[(int64_t)g * p.nblk + b];
-    const int offset = block_sum(before, red);
+    for (int off = 32; off > 0; off >>= 1) before += __shfl_xor(before, off);
+    if (lane == 0) red[wave] = before;
 
-    bool live[PX_PER_THREAD];
-    int cnt = 0;
-    const int px0 = blk * BLK_PX + tid * PX_PER_THREAD;
-#pragma unroll
-    for (int i = 0; i < PX_PER_THREAD; ++i) {
-        live[i] = pixel_live(p, px0 + i, g);
-        cnt += live[i] ? 1 : 0;
-    }
-    // inclusive scan of cnt over the wave, then over waves
-    int inc = cnt;
-    for (int off = 1; off < 64; off <<= 1) {
-        const int o = __shfl_up(inc, off);
-        if (lane >= off) inc += o;
-    }
-    if (lane == 63) wsum[wave] = inc;
+    const int px = blk * CNT + tid;
+    const bool live = pixel_live(p, px, g);
+    const uint64_t bal = __ballot(live);
+    if (lane == 0) wcnt[wave] = __popcll(bal);
     __syncthreads();
+    const int offset = red[0] + red[1] + red[2] + red[3];
     int wbase = 0;
-    for (int w = 0; w < wave; ++w) wbase += wsum[w];
-    int pos = offset + wbase + inc - cnt;
-    int32_t* list = p.lists + (int64_t)g * p.npix;
-#pragma unroll
-    for (int i = 0; i < PX_PER_THREAD; ++i) {
-        const int px = px0 + i;
-        if (px >= p.npix) break;
-        if (live[i]) {
-            list[pos++] = px;
+    for (int w = 0; w < wave; ++w) wbase += wcnt[w];
+    const uint64_t lower = lane == 0 ? 0ull : (bal & ((~0ull) >> (64 - lane)));
+    const int rank = wbase + __popcll(lower);
+    if (px < p.npix) {
+        if (live) {
+            p.lists[(int64_t)g * p.npix + offset + rank] = px;
         } else {
             const int lo = g * p.G, hi = min(p.C, lo + p.G);
-            uint4* row = reinterpret_cast<uint4*>(static_cast<char*>(p.dx) +
-                                                  ((int64_t)px * p.C + lo) * p.elem_bytes);
+            uint4* row = reinterpret_cast<uint4*>(static_cast<char*>(p.dx) + ((int64_t)px * p.C + lo) * p.elem_bytes);
             const int nvec = (hi - lo) * p.elem_bytes / 16;
             for (int v = 0; v < nvec; ++v) row[v] = make_uint4(0, 0, 0, 0);
         }
     }
-    if (blk == p.nblk - 1 && tid == CNT - 1) p.counts[g] = offset + wbase + inc;
+    if (blk == p.nblk - 1 && tid == 0) p.counts[g] = offset + wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
 }
 
 // occ[chunk][kt] = 1 iff dY has a non-zero in pixels of the chunk and
-// channels of k-tile kt (from the packed footprint when given).
+// channels of k-tile kt (from the packed footprint when given: one pixel per
+// thread, the tile's words read as vectors when K is a multiple of 256).
 __global__ __launch_bounds__(256) void occupancy_kernel(OccParams p)
 {
     __shared__ int flags[1024];
@@ -181,12 +121,21 @@ __global__ __launch_bounds__(256) void occupancy_kernel(OccParams p)
     const int px0 = chunk * p.chunk;
     const int npx = min(p.chunk, p.npq - px0);
     if (p.bits) {
+        const bool vec = p.BNk == 256 && (p.K & 255) == 0;
         const int pairs = npx * p.ktiles;
         for (int i = threadIdx.x; i < pairs; i += blockDim.x) {
             const int px = px0 + i / p.ktiles, kt = i % p.ktiles;
             const int64_t base = (int64_t)px * p.K;
             const int lo = kt * p.BNk, hi = min(p.K, lo + p.BNk);
-            if (any_bits(p.bits, base + lo, base + hi)) atomicOr(&flags[kt], 1);
+            bool any;
+            if (vec) {
+                const uint4* w = reinterpret_cast<const uint4*>(p.bits + ((base + lo) >> 5));
+                const uint4 a = w[0], b = w[1];
+                any = ((a.x | a.y | a.z | a.w) | (b.x | b.y | b.z | b.w)) != 0;
+            } else {
+                any = any_bits(p.bits, base + lo, base + hi);
+            }
+            if (any) atomicOr(&flags[kt], 1);
         }
     } else {
         const int E = p.dtype == 1 ? 8 : 4;
@@ -254,12 +203,9 @@ hipError_t launch_relu_mask_pack(int dtype, int64_t count, const void* x, uint32
     return hipGetLastError();
 }
 
-hipError_t launch_compact(const CompactParams& p, hipStream_t stream)
+hipError_t launch_compact_scatter(const CompactParams& p, hipStream_t stream)
 {
     dim3 grid(p.nblk, p.groups);
-    compact_count_kernel<<<grid, CNT, 0, stream>>>(p);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
     compact_scatter_kernel<<<grid, CNT, 0, stream>>>(p);
     return hipGetLastError();
 }

@@ -15,7 +15,7 @@ constexpr int kDataTileC = CBW_DX_BM;   // channels per data-gradient tile = com
 constexpr int kDataTileP = CBW_DX_BN;   // pixels per data-gradient tile
 constexpr int kWeightTileC = CBW_DW_BM; // channels c per weight-gradient tile
 constexpr int kWeightTileK = CBW_DW_BN; // output channels k per weight-gradient tile
-constexpr int kCompactBlock = 1024;     // pixels per compaction block
+constexpr int kCompactBlock = 256;      // pixels per compaction block
 // Resident weight-gradient workgroups the split-K factor aims to fill exactly.
 constexpr int kWeightSlots = CBW_NUM_CUS * CBW_DW_OCC;
 

@@ -167,19 +167,22 @@ def draw(spec: LayerSpec, want=("x", "w", "dy")):
     if "x" in want:
         rng = _rng(cid, lid, 0)
         if spec.x_kind == "shifted_gauss":
-            g = rng.standard_normal((n, h, w_, c), dtype=np.float32)
-            x = np.maximum(g - np.float32(spec.x_param), np.float32(0.0))
+            x = rng.standard_normal((n, h, w_, c), dtype=np.float32)
+            x -= np.float32(spec.x_param)
+            np.maximum(x, np.float32(0.0), out=x)
         elif spec.x_kind in ("bernoulli", "clustered", "channel_shared"):
             fp = _footprint(rng, spec.x_kind, n, c, h, w_, spec.x_param)
-            mag = np.abs(rng.standard_normal((n, h, w_, c), dtype=np.float32))
-            x = np.where(fp, mag, np.float32(0.0))
+            x = rng.standard_normal((n, h, w_, c), dtype=np.float32)
+            np.abs(x, out=x)
+            x *= fp
         else:
             raise ValueError(spec.x_kind)
         out["x"] = _to_torch(x, spec.dtype)
     if "w" in want:
         rng = _rng(cid, lid, 1)
         std = sqrt(2.0 / (c * spec.R * spec.S))
-        wt = rng.standard_normal((k, spec.R, spec.S, c), dtype=np.float32) * np.float32(std)
+        wt = rng.standard_normal((k, spec.R, spec.S, c), dtype=np.float32)
+        wt *= np.float32(std)
         out["w"] = _to_torch(wt, spec.dtype)
     if "dy" in want:
         p, q = spec.P, spec.Q
@@ -197,7 +200,8 @@ def draw(spec: LayerSpec, want=("x", "w", "dy")):
             live = _footprint(rngm, spec.dy_kind, n, k, p, q, spec.dy_param)
         if spec.extra.get("maxpool_route"):
             live = _maxpool_route(rngm, live)
-        out["dy"] = _to_torch(np.where(live, vals, np.float32(0.0)), spec.dtype)
+        np.putmask(vals, ~live, np.float32(0.0))  # +0.0 where dead
+        out["dy"] = _to_torch(vals, spec.dtype)
     return out
 
 
