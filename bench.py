@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU baseline time budget")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 256 MiB device copy three times (reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -181,6 +183,14 @@ def main():
                 "kernel": {"dx_gemm": "bwd_data_kernel<bf16, gather>",
                            "dw_gemm": "bwd_weight_kernel<bf16>"}[dom],
                 "kernel_ms": round(kern[dom], 4), "flops_per_launch": dom_flops}
+
+    if args.copy_calibration:
+        a = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
 
     cpu = None
     if not args.no_cpu:
