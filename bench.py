@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU baseline time budget")
+    ap.add_argument("--sweep", choices=["config4", "config3", "config5"], default=None,
+                    help="instead of the main line, time the sparse and dense steps over a workload set "
+                         "(one JSON line per layer or density point)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 256 MiB device copy three times (reference for HBM byte counters)")
     return ap.parse_args()
@@ -57,6 +60,9 @@ def main():
         print("bench.py measures one GPU only: this build targets a single MI355X (data-parallel "
               "sharding over the batch is described in DESIGN.md, not run). Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
+    if args.sweep:
+        run_sweep(args)
+        return
 
     import numpy as np
     import torch
@@ -229,6 +235,100 @@ def main():
                          "simulated 32nm FP16 ASIC (not comparable hardware)",
     }
     print(json.dumps(out), flush=True)
+
+
+def layer_timing(cb, torch, spec, steps, warmup):
+    """Sparse and dense step times of one layer (same schedule as the main
+    line) plus the kernels' executed fractions."""
+    import workloads as wl
+    dev = torch.device("cuda:0")
+    t = wl.draw(spec)
+    x, w, dy = (t[k].to(dev) for k in ("x", "w", "dy"))
+    del t
+    desc = cb.ConvDesc.make(spec.N, spec.C, spec.H, spec.W, spec.K, spec.R, spec.S, spec.stride, spec.pad)
+    xm = torch.empty(cb.cbw_mask_words(desc), dtype=torch.int32, device=dev)
+    dym = torch.empty(cb.cbw_dy_mask_words(desc), dtype=torch.int32, device=dev)
+    cb.cbw_relu_mask_pack(desc, x, xm)
+    cb.cbw_nonzero_mask_pack(desc.dtype, dy.numel(), dy, dym)
+    dx = torch.empty_like(x)
+    dw = torch.empty((spec.K, spec.R, spec.S, spec.C), dtype=torch.float32, device=dev)
+    ws_m = cb.workspace(desc, cb.CBW_OP_BWD_DATA_MASKED, dev)
+    ws_d = cb.workspace(desc, cb.CBW_OP_BWD_DATA, dev)
+    ws_w = cb.workspace(desc, cb.CBW_OP_BWD_WEIGHT, dev)
+
+    def sparse():
+        if spec.need_dx:
+            if spec.masked:
+                cb.conv_bwd_data_masked(desc, dy, w, xm, dx, ws_m, 0)
+            else:
+                cb.conv_bwd_data(desc, dy, w, dx, ws_d)
+        cb.conv_bwd_weight_sparse(desc, x, dy, dym, dw, ws_w, 0)
+
+    def dense():
+        if spec.need_dx:
+            cb.conv_bwd_data(desc, dy, w, dx, ws_d)
+        cb.conv_bwd_weight_sparse(desc, x, dy, None, dw, ws_w, cb.CBW_FLAG_NO_SKIP)
+
+    def tm(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps
+
+    ms_s, ms_d = tm(sparse), tm(dense)
+    sparse()
+    torch.cuda.synchronize()
+    rec = {"layer": spec.name, "N": spec.N, "C": spec.C, "K": spec.K, "H": spec.H, "W": spec.W, "R": spec.R,
+           "masked_dx": bool(spec.need_dx and spec.masked), "need_dx": bool(spec.need_dx),
+           "x_density": round(float((x > 0).float().mean().item()), 4),
+           "dy_density": round(float((dy != 0).float().mean().item()), 4),
+           "sparse_ms": round(ms_s, 4), "dense_ms": round(ms_d, 4), "speedup_vs_dense": round(ms_d / ms_s, 4)}
+    f = spec.dense_flops()
+    nflops = f * (2 if spec.need_dx else 1)
+    rec["dense_equiv_tflops"] = round(nflops / (ms_s * 1e-3) / 1e12, 2)
+    useful = 2 * int(torch.count_nonzero(dy).item()) * spec.C * spec.R * spec.S
+    if spec.need_dx:
+        useful += (2 * int(torch.count_nonzero(x > 0).item()) * spec.K * spec.R * spec.S if spec.masked else f)
+    rec["useful_tflops"] = round(useful / (ms_s * 1e-3) / 1e12, 2)
+    if spec.need_dx and spec.masked:
+        st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_DATA_MASKED, ws_m)
+        rec["dx_rows_executed"] = round(st.rows_live / st.rows_total, 4)
+    st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws_w)
+    rec["dw_blocks_executed"] = round(1.0 - st.blocks_skipped / max(st.blocks_total, 1), 4)
+    return rec
+
+
+def run_sweep(args):
+    import torch
+
+    import paper_2109_07710_amd as cb
+    import workloads as wl
+    torch.cuda.set_device(0)
+    if args.sweep == "config4":
+        specs = [(kind, wl.config4(d, kind)[0]) for kind in ("bernoulli", "clustered", "channel_shared")
+                 for d in wl.SWEEP_DENSITIES]
+    elif args.sweep == "config3":
+        specs = [("bottleneck", s) for s in wl.config3()]
+    else:
+        specs = [("vgg16", s) for s in wl.config5()]
+    for tag, spec in specs:
+        d = cb.ConvDesc.make(spec.N, spec.C, spec.H, spec.W, spec.K, spec.R, spec.S, spec.stride, spec.pad)
+        if cb.cbw_validate_desc(d) != cb.CBW_OK:
+            print(json.dumps({"sweep": args.sweep, "kind": tag, "layer": spec.name,
+                              "skipped": "unsupported by the library (channel count)"}), flush=True)
+            continue
+        log("sweep point %s %s" % (tag, spec.name))
+        rec = layer_timing(cb, torch, spec, max(5, args.steps // 2), 10)
+        rec = {"sweep": args.sweep, "kind": tag, **rec}
+        if "density" in spec.extra:
+            rec["density"] = spec.extra["density"]
+        print(json.dumps(rec), flush=True)
 
 
 def traffic_for(kernel):
