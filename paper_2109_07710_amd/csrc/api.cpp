@@ -32,6 +32,8 @@ T* at(void* ws, const Region& r) { return reinterpret_cast<T*>(static_cast<char*
 
 bool tiles_consistent()
 {
+    static_assert(kDataMaxSplit >= 1, "split bound");
+    if (data_split(1, 1 << 20, kDataSlots, kDataMaxSplit) != host_data_split(1, 1 << 20)) return false;
     return data_tile_channels() == kDataTileC && data_tile_pixels() == kDataTileP &&
            weight_tile_channels() == kWeightTileC && weight_tile_k() == kWeightTileK &&
            compact_block_pixels() == kCompactBlock && weight_chunk(CBW_BF16) == weight_chunk_px(CBW_BF16) &&
@@ -85,6 +87,11 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
     void* wt = at<void>(ws, plan.wt);
     DataParams p = data_params(desc, dY, wt, dX, plan.npix, plan.groups);
     p.mask = x_mask;
+    p.ptiles = plan.ptiles;
+    p.nslots = kDataSlots;
+    p.smax = kDataMaxSplit;
+    p.split = gather ? 1 : plan.split;
+    p.partial = plan.partial.bytes ? at<float>(ws, plan.partial) : nullptr;
     CompactParams cp{};
     if (gather) {
         cp.mask = x_mask;

@@ -66,21 +66,50 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
 
-    const int t = xcd_remap(blockIdx.x, gridDim.x);
-    const int ptile = t / p.ctiles;
-    const int ctile = t - ptile * p.ctiles;
+    // Work items are (tile, reduction split).  In gather mode the number of
+    // live tiles T follows from the compaction counts; when T is small
+    // against the resident workgroups, each tile's reduction (taps x channel
+    // chunks) is split S ways and the partial tiles are summed afterwards
+    // (splitk_data_reduce_kernel) -- every workgroup derives the same S.
+    const int kchunks = (p.K + (CH * Elem<T>::E) - 1) / (CH * Elem<T>::E);
+    const int nsteps = p.R * p.S * kchunks;
+    int ntiles, nsplit;
+    if (MODE == MODE_GATHER) {
+        ntiles = 0;
+        for (int g = 0; g < p.ctiles; ++g) ntiles += (p.counts[g] + BN - 1) / BN;
+        nsplit = data_split(ntiles, nsteps, p.nslots, p.smax);
+    } else {
+        ntiles = p.ptiles * p.ctiles;
+        nsplit = p.split;
+    }
+    const int item = xcd_remap(blockIdx.x, gridDim.x);
+    if (item >= ntiles * nsplit) return;  // uniform across the workgroup
+    const int tile = item / nsplit, z = item - tile * nsplit;
+    int ctile, ptile;
+    if (MODE == MODE_GATHER) {
+        int g = 0, cum = 0;
+        while (true) {
+            const int tg = (p.counts[g] + BN - 1) / BN;
+            if (tile < cum + tg) break;
+            cum += tg;
+            ++g;
+        }
+        ctile = g;
+        ptile = tile - cum;
+    } else {
+        ptile = tile / p.ctiles;
+        ctile = tile - ptile * p.ctiles;
+    }
     const int c0 = ctile * BM;
     const int row0 = ptile * BN;
-
-    int nrows = p.npix;
-    if (MODE == MODE_GATHER) nrows = p.counts[ctile];
-    if (row0 >= nrows) return;  // uniform across the workgroup
+    const int nrows = MODE == MODE_GATHER ? p.counts[ctile] : p.npix;
+    const int st_begin = (int)((int64_t)z * nsteps / nsplit);
+    const int st_end = (int)((int64_t)(z + 1) * nsteps / nsplit);
+    const int nloc = st_end - st_begin;
 
     const u32x4_t rs_wt = make_rsrc_words(p.wt, p.wt_bytes);
     const u32x4_t rs_dy = make_rsrc_words(p.dy, p.dy_bytes);
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-    const int kchunks = (p.K + BK - 1) / BK;
-    const int nsteps = p.R * p.S * kchunks;
     const bool kfull = (p.K % BK) == 0;
 
     // Staging: every wave copies whole groups of 8 LDS rows (1 KB) straight
@@ -112,7 +141,7 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
             }
         }
     };
-    load_a(0, 0, 0);
+    load_a(0, st_begin / kchunks, (st_begin % kchunks) * BK);
 
     for (int i = tid; i < BN; i += NT) {
         const int r = row0 + i;
@@ -147,7 +176,7 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
         for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     uint32_t b_off[IB];   // B byte offset for the current tap, kOOB when the tap misses
-    int ld_tap = 0, ld_kc = 0;  // next step to load
+    int ld_tap = st_begin / kchunks, ld_kc = st_begin % kchunks;  // next step to load
 
     auto set_tap = [&](int tap) {
         const int r = tap / p.S, s = tap - r * p.S;
@@ -218,8 +247,8 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
     // Prologue: step 0's B copies, then the footprint bits of the tile
     // (pixel row x 32-channel word, valid when every pixel's group of BM
     // channels starts on a word) while the copies are in flight.
-    set_tap(0);
-    load_b(0, 0);
+    set_tap(ld_tap);
+    load_b(0, ld_kc * BK);
     if (++ld_kc == kchunks) { ld_kc = 0; ++ld_tap; }
     const bool mask_lds = MODE != MODE_DENSE && (p.C % 32) == 0;
     if (mask_lds) {
@@ -233,9 +262,9 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
     }
     wait_vmem();
     __syncthreads();
-    for (int step = 0; step < nsteps; ++step) {
+    for (int step = 0; step < nloc; ++step) {
         const int buf = step & 1;
-        if (step + 1 < nsteps) load(buf ^ 1);
+        if (step + 1 < nloc) load(buf ^ 1);
         compute(buf);
         wait_vmem();
         __syncthreads();
@@ -243,6 +272,20 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
 
     // Epilogue: lane holds channels c0 + wm*TM + i*16 + 4*(lane/16) + v of
     // pixel row wn*TN + j*16 + lane%16.
+    if (nsplit > 1) {
+        // partial tile [item][row][channel] in fp32, reduced afterwards
+        float* __restrict__ part = p.partial + (int64_t)item * BN * BM;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int pr = wn * TN + j * 16 + (lane & 15);
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int cl = wm * TM + i * 16 + 4 * (lane >> 4);
+                *reinterpret_cast<floatx4*>(part + (int64_t)pr * BM + cl) = acc[i][j];
+            }
+        }
+        return;
+    }
     T* __restrict__ dx = reinterpret_cast<T*>(p.dx);
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
@@ -323,6 +366,74 @@ __global__ __launch_bounds__(256) void data_prep_kernel(const T* __restrict__ w,
     compact_count_block(cp, b % cp.nblk, b / cp.nblk);
 }
 
+// Sums the nsplit partial tiles of every live tile in split order and writes
+// dX like the GEMM epilogue would (footprint select, rounding).  Runs with a
+// fixed grid; exits at once when the GEMM did not split.
+template <typename T, int MODE>
+__global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
+{
+    constexpr int E = Elem<T>::E;
+    const int kchunks = (p.K + CH * E - 1) / (CH * E);
+    const int nsteps = p.R * p.S * kchunks;
+    int ntiles, nsplit;
+    if (MODE == MODE_GATHER) {
+        ntiles = 0;
+        for (int g = 0; g < p.ctiles; ++g) ntiles += (p.counts[g] + BN - 1) / BN;
+        nsplit = data_split(ntiles, nsteps, p.nslots, p.smax);
+    } else {
+        ntiles = p.ptiles * p.ctiles;
+        nsplit = p.split;
+    }
+    if (nsplit <= 1) return;
+    const int64_t nvec = (int64_t)ntiles * BN * (BM / 4);
+    T* __restrict__ dx = reinterpret_cast<T*>(p.dx);
+    for (int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; v < nvec; v += (int64_t)gridDim.x * blockDim.x) {
+        const int tile = (int)(v / (BN * (BM / 4)));
+        const int rem = (int)(v - (int64_t)tile * BN * (BM / 4));
+        const int pr = rem / (BM / 4), cl = (rem - pr * (BM / 4)) * 4;
+        int ctile, ptile;
+        if (MODE == MODE_GATHER) {
+            int g = 0, cum = 0;
+            while (true) {
+                const int tg = (p.counts[g] + BN - 1) / BN;
+                if (tile < cum + tg) break;
+                cum += tg;
+                ++g;
+            }
+            ctile = g;
+            ptile = tile - cum;
+        } else {
+            ptile = tile / p.ctiles;
+            ctile = tile - ptile * p.ctiles;
+        }
+        const int r = ptile * BN + pr;
+        const int nrows = MODE == MODE_GATHER ? p.counts[ctile] : p.npix;
+        const int c = ctile * BM + cl;
+        if (r >= nrows || c >= p.C) continue;
+        const int pix = MODE == MODE_GATHER ? p.lists[(int64_t)ctile * p.npix + r] : r;
+        floatx4 s = *reinterpret_cast<const floatx4*>(p.partial + ((int64_t)tile * nsplit * BN + pr) * BM + cl);
+        for (int zz = 1; zz < nsplit; ++zz)
+            s += *reinterpret_cast<const floatx4*>(p.partial + (((int64_t)tile * nsplit + zz) * BN + pr) * BM + cl);
+        const int64_t o = (int64_t)pix * p.C + c;
+        uint32_t keep = 0xfu;
+        if (MODE != MODE_DENSE) keep = (p.mask[o >> 5] >> (o & 31)) & 0xfu;
+        if constexpr (sizeof(T) == 2) {
+            uint32_t h0 = (keep & 1u) ? f32_to_bf16_rne(s.x) : 0u;
+            uint32_t h1 = (keep & 2u) ? f32_to_bf16_rne(s.y) : 0u;
+            uint32_t h2 = (keep & 4u) ? f32_to_bf16_rne(s.z) : 0u;
+            uint32_t h3 = (keep & 8u) ? f32_to_bf16_rne(s.w) : 0u;
+            *reinterpret_cast<uint2*>(dx + o) = make_uint2(h0 | (h1 << 16), h2 | (h3 << 16));
+        } else {
+            uint4 u;
+            u.x = (keep & 1u) ? __float_as_uint(s.x) : 0u;
+            u.y = (keep & 2u) ? __float_as_uint(s.y) : 0u;
+            u.z = (keep & 4u) ? __float_as_uint(s.z) : 0u;
+            u.w = (keep & 8u) ? __float_as_uint(s.w) : 0u;
+            *reinterpret_cast<uint4*>(dx + o) = u;
+        }
+    }
+}
+
 }  // namespace
 
 int data_tile_channels() { return BM; }
@@ -351,8 +462,8 @@ hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, in
 
 hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream)
 {
-    const int ptiles = (p.npix + BN - 1) / BN;
-    const int nb = ptiles * p.ctiles;
+    // enough workgroups for every tile unsplit, or for nslots split items
+    const int nb = max(p.ptiles * p.ctiles, p.nslots);
     if (nb <= 0) return hipSuccess;
     const bool unit = p.stride_h == 1 && p.stride_w == 1;
 #define CBW_LAUNCH(T, M)                                                          \
@@ -370,7 +481,26 @@ hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t
         else CBW_LAUNCH(float, MODE_GATHER);
     }
 #undef CBW_LAUNCH
-    return hipGetLastError();
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // The reduction runs whenever a split can occur: in gather mode the
+    // split is only known on the device.
+    if (mode == MODE_GATHER || p.split > 1) {
+        const int rb = p.nslots;
+#define CBW_REDUCE(T, M) splitk_data_reduce_kernel<T, M><<<rb, 256, 0, stream>>>(p)
+        if (dtype == 1) {
+            if (mode == MODE_DENSE) CBW_REDUCE(uint16_t, MODE_DENSE);
+            else if (mode == MODE_SELECT) CBW_REDUCE(uint16_t, MODE_SELECT);
+            else CBW_REDUCE(uint16_t, MODE_GATHER);
+        } else {
+            if (mode == MODE_DENSE) CBW_REDUCE(float, MODE_DENSE);
+            else if (mode == MODE_SELECT) CBW_REDUCE(float, MODE_SELECT);
+            else CBW_REDUCE(float, MODE_GATHER);
+        }
+#undef CBW_REDUCE
+        e = hipGetLastError();
+    }
+    return e;
 }
 
 }  // namespace cbw

@@ -133,6 +133,18 @@ __device__ __forceinline__ void buf_load16_lds(const u32x4_t& rsrc, uint32_t off
 // Wait until all of this wave's vector memory operations have completed.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
+// Reduction split of the data-gradient GEMM: with T tiles and `slots`
+// resident workgroups, split every tile's `nsteps` reduction steps S ways
+// when at least two tiles' worth of workgroups would otherwise sit idle.
+__host__ __device__ inline int data_split(int T, int nsteps, int slots, int smax)
+{
+    if (T <= 0 || 2 * T > slots) return 1;
+    int sp = slots / T;
+    if (sp > smax) sp = smax;
+    if (sp > nsteps) sp = nsteps;
+    return sp < 1 ? 1 : sp;
+}
+
 // XCD-aware block order.  The dispatcher hands consecutive workgroups to the
 // eight XCDs in turn; this maps the j-th workgroup an XCD receives to the
 // j-th tile of a contiguous range owned by that XCD, so tiles that share

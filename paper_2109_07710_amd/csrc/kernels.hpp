@@ -21,6 +21,10 @@ struct DataParams {
     int stride_h, stride_w, pad_h, pad_w;
     int npix;                // N*H*W
     int ctiles;              // channel tiles = compaction groups
+    int ptiles;              // pixel tiles (dense / select modes)
+    int split;               // reduction split (dense / select modes; gather derives its own)
+    int nslots, smax;        // resident workgroups; largest split
+    float* partial;          // [item][BN][BM] fp32 partial tiles when split
     uint32_t dy_bytes, wt_bytes;
     FastDiv div_w, div_h;    // pixel -> (n, h, w)
 };

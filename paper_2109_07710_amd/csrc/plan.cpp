@@ -55,6 +55,10 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out)
     p.groups = (d->C + kDataTileC - 1) / kDataTileC;
     p.nblk = (int)((p.npix + kCompactBlock - 1) / kCompactBlock);
     size_t cur = 0;
+    p.ptiles = (int)((p.npix + kDataTileP - 1) / kDataTileP);
+    const int bk = 8 * (d->dtype == CBW_BF16 ? 8 : 4);
+    p.nsteps = d->R * d->S * ((d->K + bk - 1) / bk);
+    p.split = host_data_split(p.ptiles * p.groups, p.nsteps);
     p.header = take(&cur, 256);
     p.wt = take(&cur, (size_t)d->K * d->C * d->R * d->S * elem_bytes(d->dtype));
     if (masked) {
@@ -62,6 +66,12 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out)
         p.counts = take(&cur, (size_t)p.groups * 4);
         p.lists = take(&cur, (size_t)p.groups * p.npix * 4);
     }
+    // Split partial tiles.  Without skipping the host knows the split; with
+    // compaction it is decided on the device, bounded by one partial tile
+    // per resident workgroup.
+    const size_t tile_bytes = (size_t)kDataTileP * kDataTileC * 4;
+    if (masked) p.partial = take(&cur, (size_t)kDataSlots * tile_bytes);
+    else if (p.split > 1) p.partial = take(&cur, (size_t)p.ptiles * p.groups * p.split * tile_bytes);
     p.total = cur;
     *out = p;
     return CBW_OK;

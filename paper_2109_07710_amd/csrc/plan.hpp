@@ -28,9 +28,24 @@ struct Region {
 struct DataPlan {
     int64_t npix = 0;
     int groups = 0, nblk = 0;
-    Region header, wt, blk_counts, counts, lists;
+    int ptiles = 0, nsteps = 0;
+    int split = 1;          // dense / select: host-chosen reduction split
+    Region header, wt, blk_counts, counts, lists, partial;
     size_t total = 0;
 };
+
+constexpr int kDataSlots = CBW_NUM_CUS * CBW_DX_OCC;  // resident data-gradient workgroups
+constexpr int kDataMaxSplit = 16;
+
+// Same rule as the kernels' data_split (see common.hpp).
+inline int host_data_split(int T, int nsteps)
+{
+    if (T <= 0 || 2 * T > kDataSlots) return 1;
+    int sp = kDataSlots / T;
+    if (sp > kDataMaxSplit) sp = kDataMaxSplit;
+    if (sp > nsteps) sp = nsteps;
+    return sp < 1 ? 1 : sp;
+}
 
 struct WeightPlan {
     int64_t npq = 0;

@@ -15,7 +15,7 @@ import torch
 import oracle
 import paper_2109_07710_amd as cb
 import workloads as wl
-from parity import check_values, dx_bits_nchw, gpu_backward, tol_for
+from parity import check_values, dx_as_nchw, dx_bits_nchw, gpu_backward, tol_for
 
 pytestmark = pytest.mark.gpu
 
@@ -82,7 +82,15 @@ def _check_full(spec, flags_pairs=True):
         if spec.masked and flags_pairs:
             dense = gpu_backward(spec, t, masked=False)
             bd = dx_bits_nchw(dense["dx"])
-            assert np.array_equal(bits[mask], bd[mask]), "masked kernel differs from dense at live outputs"
+            stats = cb.cbw_read_stats(gpu["desc"], cb.CBW_OP_BWD_DATA_MASKED, gpu["ws_dx"])
+            if stats.rows_live == stats.rows_total:
+                # same rows, same reduction split: identical bits
+                assert np.array_equal(bits[mask], bd[mask]), "masked kernel differs from dense at live outputs"
+            else:
+                # compaction removed rows, so the reduction may be split differently
+                gm = dx_as_nchw(gpu["dx"])[mask]
+                dm = dx_as_nchw(dense["dx"])[mask]
+                assert np.max(np.abs(gm - dm)) <= 2.0 ** -7 * max(np.max(np.abs(dm)), 1e-30)
     cw = _dw_coords(spec, rng)
     o, absw, ntw = oracle.conv_bwd_weight_at(x64, dy64, (spec.R, spec.S), cw, st, pd)
     g = gpu["dw"].cpu().numpy()[cw[:, 0], cw[:, 2], cw[:, 3], cw[:, 1]].astype(np.float64)
