@@ -65,6 +65,7 @@ DataParams data_params(const cbw_conv_desc* d, const void* dY, const void* wt, v
     const int64_t esz = elem_bytes(d->dtype);
     p.dy_bytes = (uint32_t)((int64_t)d->N * d->P * d->Q * d->K * esz);
     p.wt_bytes = (uint32_t)((int64_t)d->R * d->S * d->C * d->K * esz);
+    p.dx_bytes = (uint32_t)(npix * d->C * esz);
     return p;
 }
 

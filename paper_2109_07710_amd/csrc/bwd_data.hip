@@ -24,6 +24,8 @@
 // barrier per reduction step).  LDS rows are 128 bytes (8 chunks of 16
 // bytes) with an XOR chunk swizzle so that the MFMA fragment reads of 16
 // consecutive rows spread over all banks.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "footprint.hpp"
@@ -244,29 +246,94 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
         }
     };
 
-    // Prologue: step 0's B copies, then the footprint bits of the tile
-    // (pixel row x 32-channel word, valid when every pixel's group of BM
-    // channels starts on a word) while the copies are in flight.
+    // Prologue: step 0's B copies.
     set_tap(ld_tap);
     load_b(0, ld_kc * BK);
     if (++ld_kc == kchunks) { ld_kc = 0; ++ld_tap; }
-    const bool mask_lds = MODE != MODE_DENSE && (p.C % 32) == 0;
-    if (mask_lds) {
-        for (int i = tid; i < BN * (BM / 32); i += NT) {
-            const int pr = i / (BM / 32), wi = i - pr * (BM / 32);
-            const int pix = pix_s[pr];
+
+    // Footprint words of the tile (pixel row x 32-channel word, valid when
+    // every pixel's group of BM channels starts on a word).  Only the
+    // epilogue needs them: they are fetched from inside the main loop, next
+    // to step 1's copies (so no wait is spent on them), held in registers
+    // and staged in LDS after the loop.
+    const bool mask_lds = MODE != MODE_DENSE && (p.C % 32) == 0 && nsplit == 1;
+    constexpr int MW = MODE == MODE_DENSE ? 0 : BN * (BM / 32);   // footprint words per tile
+    constexpr int MI = MW > 0 ? (MW + NT - 1) / NT : 1;          // per thread
+    uint32_t mwords[MI];
+    auto fetch_mask = [&]() {
+#pragma unroll
+        for (int u = 0; u < MI; ++u) {
+            const int i = tid + u * NT;
             uint32_t word = 0;
-            if (pix >= 0 && c0 + 32 * wi < p.C) word = p.mask[((int64_t)pix * p.C + c0) / 32 + wi];
-            msk_s[i] = word;
+            if (i < MW) {
+                const int pr = i / (BM / 32), wi = i - pr * (BM / 32);
+                const int pix = pix_s[pr];
+                if (pix >= 0 && c0 + 32 * wi < p.C) word = p.mask[((int64_t)pix * p.C + c0) / 32 + wi];
+            }
+            mwords[u] = word;
         }
-    }
+    };
+    const int mask_step = nloc > 1 ? 1 : 0;
     wait_vmem();
     __syncthreads();
+#if CBW_DX_PIPE
+    static_assert(CH == 8, "two chunk groups per step");
+    // Two register sets of fragments: while the MFMAs of one chunk group run,
+    // the fragments of the next one are already being read.  Group 1 of a
+    // step is read before the barrier, group 0 of the next step right after
+    // it (its copies have landed by then).
+    auto read_frags = [&](int buf, int kc, uint4 (&fa)[FM], uint4 (&fb)[FN]) {
+        const int chl = kc * 4 + (lane >> 4);
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int row = wm * TM + i * 16 + (lane & 15);
+            fa[i] = As[buf][row * CH + (chl ^ swz8(row))];
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int row = wn * TN + j * 16 + (lane & 15);
+            fb[j] = Bs[buf][row * CH + (chl ^ swz8(row))];
+        }
+    };
+    auto mma = [&](const uint4 (&fa)[FM], const uint4 (&fb)[FN]) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) acc[i][j] = mfma_chunk(acc[i][j], fa[i], fb[j], T{});
+    };
+    uint4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
+    read_frags(0, 0, fa0, fb0);
     for (int step = 0; step < nloc; ++step) {
         const int buf = step & 1;
         if (step + 1 < nloc) load(buf ^ 1);
+        if (mask_lds && step == mask_step) fetch_mask();
+        read_frags(buf, 1, fa1, fb1);
+        mma(fa0, fb0);
+        // keep the waits and the barrier behind this group's MFMAs
+        __builtin_amdgcn_sched_barrier(0);
+        wait_vmem_lds();
+        __syncthreads();
+        if (step + 1 < nloc) read_frags(buf ^ 1, 0, fa0, fb0);
+        mma(fa1, fb1);
+    }
+#else
+    for (int step = 0; step < nloc; ++step) {
+        const int buf = step & 1;
+        if (step + 1 < nloc) load(buf ^ 1);
+        if (mask_lds && step == mask_step) fetch_mask();
         compute(buf);
         wait_vmem();
+        __syncthreads();
+    }
+#endif
+
+    if (mask_lds) {
+        // msk_s is not an operand buffer: no barrier is needed before writing it
+#pragma unroll
+        for (int u = 0; u < MI; ++u) {
+            const int i = tid + u * NT;
+            if (i < MW) msk_s[i] = mwords[u];
+        }
         __syncthreads();
     }
 
@@ -286,40 +353,66 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
         }
         return;
     }
-    T* __restrict__ dx = reinterpret_cast<T*>(p.dx);
+    // Stores go through a buffer descriptor: a lane whose pixel or channel
+    // lies outside the tensor gets offset kOOB and the store is dropped,
+    // so the epilogue has no branches.  Footprint words are read from LDS
+    // in one batch first (a 16-channel block never straddles a word, so a
+    // lane needs TM/32 words per pixel row).
+    const __amdgpu_buffer_rsrc_t rs_dx = make_rsrc(p.dx, p.dx_bytes);
+    constexpr int MWJ = TM / 32 > 0 ? TM / 32 : 1;
+    uint32_t ew[FN][MWJ];
+    if (mask_lds) {
+        static_assert(TM % 32 == 0, "wave tile must cover whole footprint words");
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-        const int pr = wn * TN + j * 16 + (lane & 15);
-        const int pix = pix_s[pr];
-        if (pix < 0) continue;
+        for (int j = 0; j < FN; ++j) {
+            const int pr = wn * TN + j * 16 + (lane & 15);
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
-            const int cl = wm * TM + i * 16 + 4 * (lane >> 4);  // channel within the tile
-            const int c = c0 + cl;
-            if (c >= p.C) continue;
-            const int64_t o = (int64_t)pix * p.C + c;
-            floatx4 v = acc[i][j];
-            uint32_t keep = 0xfu;
-            if (MODE != MODE_DENSE) {
-                if (mask_lds) keep = (msk_s[pr * (BM / 32) + cl / 32] >> (cl & 31)) & 0xfu;
-                else keep = (p.mask[o >> 5] >> (o & 31)) & 0xfu;
-            }
-            if constexpr (sizeof(T) == 2) {
-                uint32_t h0 = (keep & 1u) ? f32_to_bf16_rne(v.x) : 0u;
-                uint32_t h1 = (keep & 2u) ? f32_to_bf16_rne(v.y) : 0u;
-                uint32_t h2 = (keep & 4u) ? f32_to_bf16_rne(v.z) : 0u;
-                uint32_t h3 = (keep & 8u) ? f32_to_bf16_rne(v.w) : 0u;
-                *reinterpret_cast<uint2*>(dx + o) = make_uint2(h0 | (h1 << 16), h2 | (h3 << 16));
-            } else {
-                uint4 u;
-                u.x = (keep & 1u) ? __float_as_uint(v.x) : 0u;
-                u.y = (keep & 2u) ? __float_as_uint(v.y) : 0u;
-                u.z = (keep & 4u) ? __float_as_uint(v.z) : 0u;
-                u.w = (keep & 8u) ? __float_as_uint(v.w) : 0u;
-                *reinterpret_cast<uint4*>(dx + o) = u;
-            }
+            for (int w = 0; w < MWJ; ++w) ew[j][w] = msk_s[pr * (BM / 32) + (wm * TM) / 32 + w];
         }
     }
+    // One straight-line body per footprint source (words staged in LDS, or
+    // read per element when C is not a multiple of 32); the choice is
+    // uniform across the workgroup.
+    auto epilogue = [&](auto lds_tag) {
+        constexpr bool LDSW = decltype(lds_tag)::value;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int pr = wn * TN + j * 16 + (lane & 15);
+            const int pix = pix_s[pr];
+            const int clane = wm * TM + 4 * (lane >> 4);   // first channel of the lane's block, i = 0
+            const uint32_t base = (uint32_t)(pix * p.C + c0 + clane) * ESZ;
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int cl = clane + i * 16;
+                const bool ok = pix >= 0 && c0 + cl < p.C;
+                const uint32_t off = ok ? base + (uint32_t)(i * 16) * ESZ : kOOB;
+                uint32_t keep = 0xfu;
+                if (MODE != MODE_DENSE) {
+                    if constexpr (LDSW) {
+                        keep = (ew[j][(i * 16) / 32] >> (cl & 31)) & 0xfu;
+                    } else {
+                        const int64_t o = ok ? (int64_t)pix * p.C + c0 + cl : 0;
+                        keep = (p.mask[o >> 5] >> (o & 31)) & 0xfu;
+                    }
+                }
+                const floatx4 v = acc[i][j];
+                if constexpr (sizeof(T) == 2) {
+                    const uint32_t m01 = ((0u - (keep & 1u)) & 0xffffu) | ((0u - ((keep >> 1) & 1u)) & 0xffff0000u);
+                    const uint32_t m23 = ((0u - ((keep >> 2) & 1u)) & 0xffffu) | ((0u - ((keep >> 3) & 1u)) & 0xffff0000u);
+                    const u32x2 d = {pack_bf16x2(v.x, v.y) & m01, pack_bf16x2(v.z, v.w) & m23};
+                    __builtin_amdgcn_raw_buffer_store_b64(d, rs_dx, off, 0, 0);
+                } else {
+                    const u32x4 d = {__float_as_uint(v.x) & (0u - (keep & 1u)),
+                                     __float_as_uint(v.y) & (0u - ((keep >> 1) & 1u)),
+                                     __float_as_uint(v.z) & (0u - ((keep >> 2) & 1u)),
+                                     __float_as_uint(v.w) & (0u - ((keep >> 3) & 1u))};
+                    __builtin_amdgcn_raw_buffer_store_b128(d, rs_dx, off, 0, 0);
+                }
+            }
+        }
+    };
+    if (MODE == MODE_DENSE || mask_lds) epilogue(std::true_type{});
+    else epilogue(std::false_type{});
 }
 
 // Wt[tap][c][k] = W[k][tap][c] (KRSC) or W[k][c][tap] (KCRS).  Threads run

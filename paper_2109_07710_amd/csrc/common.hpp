@@ -9,6 +9,10 @@ namespace cbw {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // Element traits.  bf16 is stored as its 16-bit pattern.  A "vector" is 16
 // bytes: E elements.  One MFMA "chunk step" consumes one 16-byte fragment of
@@ -49,6 +53,15 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f)
     return u >> 16;
 }
 
+// Two floats to packed bf16 (a in the low half) with round-to-nearest-even:
+// one v_cvt_pk_bf16_f32 on gfx950, identical to f32_to_bf16_rne for every
+// fp32 input (NaN and subnormal inputs included).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b)
+{
+    const floatx2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
 // Unsigned division by a runtime constant d (1 <= d < 2^31) for numerators
 // below 2^31: q = (mulhi(n, m) + n) >> s with s = ceil(log2 d) and
 // m = floor(2^32 (2^s - d) / d) + 1 (Granlund & Montgomery, 1994).
@@ -86,7 +99,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint3
 
 __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off)
 {
-    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
     const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
     return make_uint4(v.x, v.y, v.z, v.w);
 }
@@ -132,6 +144,8 @@ __device__ __forceinline__ void buf_load16_lds(const u32x4_t& rsrc, uint32_t off
 
 // Wait until all of this wave's vector memory operations have completed.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+// vmcnt(0) and lgkmcnt(0): this wave's copies have landed and its LDS reads are done.
+__device__ __forceinline__ void wait_vmem_lds() { __builtin_amdgcn_s_waitcnt(0x0070); }
 
 // Reduction split of the data-gradient GEMM: with T tiles and `slots`
 // resident workgroups, split every tile's `nsteps` reduction steps S ways

@@ -25,7 +25,7 @@ struct DataParams {
     int split;               // reduction split (dense / select modes; gather derives its own)
     int nslots, smax;        // resident workgroups; largest split
     float* partial;          // [item][BN][BM] fp32 partial tiles when split
-    uint32_t dy_bytes, wt_bytes;
+    uint32_t dy_bytes, wt_bytes, dx_bytes;
     FastDiv div_w, div_h;    // pixel -> (n, h, w)
 };
 

@@ -18,6 +18,9 @@
 #ifndef CBW_DX_OCC
 #define CBW_DX_OCC 1    // resident workgroups per CU
 #endif
+#ifndef CBW_DX_PIPE
+#define CBW_DX_PIPE 0   // data gradient: fragments of the next chunk group read during the MFMAs
+#endif
 #ifndef CBW_DW_BM
 #define CBW_DW_BM 256   // weight gradient: channels c per tile
 #endif
