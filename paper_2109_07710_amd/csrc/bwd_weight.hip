@@ -245,16 +245,18 @@ __global__ __launch_bounds__(NT) void bwd_weight_kernel(WeightParams p)
 
     // Epilogue: lane holds channels c0 + wm*TM + i*16 + 4*(lane/16) + v of
     // output channel k0 + wn*TN + j*16 + lane%16; written to [z][k][tap][c].
-    float* __restrict__ out = p.out + (int64_t)z * p.K * RS * p.C;
+    // Buffer stores over this split's [K][RS][C] region: lanes past K or C
+    // get offset kOOB and their stores are dropped (no branches).
+    const uint32_t split_bytes = (uint32_t)p.K * RS * p.C * 4u;
+    const __amdgpu_buffer_rsrc_t rs_out = make_rsrc(p.out + (int64_t)z * p.K * RS * p.C, split_bytes);
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
         const int k = k0 + wn * TN + j * 16 + (lane & 15);
-        if (k >= p.K) continue;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
             const int c = c0 + wm * TM + i * 16 + 4 * (lane >> 4);
-            if (c >= p.C) continue;
-            *reinterpret_cast<floatx4*>(out + (((int64_t)k * RS + tap) * p.C + c)) = acc[i][j];
+            const uint32_t off = (k < p.K && c < p.C) ? (uint32_t)((k * RS + tap) * p.C + c) * 4u : kOOB;
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[i][j]), rs_out, off, 0, 0);
         }
     }
 }
@@ -448,16 +450,18 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
 
     if (tid == 0) p.skip_slots[blockIdx.x] = skipped;
 
-    float* __restrict__ out = p.out + (int64_t)z * p.K * RS * p.C;
+    // Buffer stores over this split's [K][RS][C] region: lanes past K or C
+    // get offset kOOB and their stores are dropped (no branches).
+    const uint32_t split_bytes = (uint32_t)p.K * RS * p.C * 4u;
+    const __amdgpu_buffer_rsrc_t rs_out = make_rsrc(p.out + (int64_t)z * p.K * RS * p.C, split_bytes);
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
         const int k = k0 + wn * TN + j * 16 + (lane & 15);
-        if (k >= p.K) continue;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
             const int c = c0 + wm * TM + i * 16 + 4 * (lane >> 4);
-            if (c >= p.C) continue;
-            *reinterpret_cast<floatx4*>(out + (((int64_t)k * RS + tap) * p.C + c)) = acc[i][j];
+            const uint32_t off = (k < p.K && c < p.C) ? (uint32_t)((k * RS + tap) * p.C + c) * 4u : kOOB;
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[i][j]), rs_out, off, 0, 0);
         }
     }
 }

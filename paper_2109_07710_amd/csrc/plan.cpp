@@ -41,7 +41,8 @@ int validate_desc(const cbw_conv_desc* d)
     // every tensor the kernels read through a buffer descriptor stays below 2^31 bytes
     const int64_t esz = d->dtype == CBW_BF16 ? 2 : 4;
     if (npix * d->C * esz >= kMaxElems || npq * d->K * esz >= kMaxElems) return CBW_ERR_UNSUPPORTED;
-    if ((int64_t)d->K * d->C * d->R * d->S >= kMaxElems) return CBW_ERR_UNSUPPORTED;
+    // the fp32 weight gradient (and each split partial of it) stays below 2^31 bytes
+    if ((int64_t)d->K * d->C * d->R * d->S * 4 >= kMaxElems) return CBW_ERR_UNSUPPORTED;
     if (d->K > 1024 * kWeightTileK) return CBW_ERR_UNSUPPORTED;  // occupancy flags per chunk
     return CBW_OK;
 }

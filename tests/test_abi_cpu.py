@@ -70,6 +70,9 @@ def test_validation_codes(L):
     assert cb.cbw_validate_desc(_desc(act_layout="nchw")) == cb.CBW_ERR_UNSUPPORTED
     assert cb.cbw_validate_desc(_desc(w_layout="kcrs")) == cb.CBW_OK
     assert cb.cbw_validate_desc(_desc(N=4096, H=1024, W=1024, C=8)) == cb.CBW_ERR_UNSUPPORTED  # >= 2^31 elems
+    # the fp32 weight gradient must stay below 2^31 bytes: 7680^2*9*4 fits, 8192^2*9*4 does not
+    assert cb.cbw_validate_desc(_desc(N=1, H=4, W=4, C=7680, K=7680)) == cb.CBW_OK
+    assert cb.cbw_validate_desc(_desc(N=1, H=4, W=4, C=8192, K=8192)) == cb.CBW_ERR_UNSUPPORTED
     assert L.cbw_validate_desc(None) == cb.CBW_ERR_INVALID_ARG
     assert cb.cbw_validate_desc(_desc(H=1, R=3, pad=(0, 1))) == cb.CBW_ERR_INVALID_ARG  # empty output
 
