@@ -58,6 +58,8 @@ def _load():
     lib.oracle_conv_bwd_data_at.restype = None
     lib.oracle_conv_bwd_weight_at.argtypes = [sp, dp, dp, i32p, ctypes.c_int64, dp, dp, i64p]
     lib.oracle_conv_bwd_weight_at.restype = None
+    lib.oracle_conv_fwd_at.argtypes = [sp, dp, dp, i32p, ctypes.c_int64, dp, dp, i64p]
+    lib.oracle_conv_fwd_at.restype = None
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
@@ -101,6 +103,40 @@ def conv_fwd(x, w, stride=(1, 1), pad=(0, 0)):
     y = np.empty((N, K, sh.P, sh.Q), np.float64)
     _load().oracle_conv_fwd(ctypes.byref(sh), _dptr(x), _dptr(w), _dptr(y))
     return y
+
+
+def relu(z):
+    """The ReLU as the footprint definition reads it (Sec. III-B): z where
+    z > 0, else +0.0 (so non-positive and NaN inputs give +0.0)."""
+    z = np.asarray(z, dtype=np.float64)
+    return np.where(z > 0, z, 0.0)
+
+
+def conv_fwd_relu(x, w, stride=(1, 1), pad=(0, 0)):
+    """Forward convolution followed by the ReLU (Sec. II-A; the ReLU output is
+    the activation whose footprint the backward pass consumes, Sec. III-B).
+    Returns (z, y, abs_sum, nterms): z = conv_fwd(x, w), y = relu(z), and per
+    output the sum of |x*w| over its terms and their number (the
+    conditioning of each sum, for error bounds)."""
+    z = conv_fwd(x, w, stride, pad)
+    a = conv_fwd(np.abs(_f64(x)), np.abs(_f64(w)), stride, pad)
+    n = conv_fwd(np.ones(np.shape(x)), np.ones(np.shape(w)), stride, pad)
+    return z, relu(z), a, np.rint(n).astype(np.int64)
+
+
+def conv_fwd_at(x, w, coords, stride=(1, 1), pad=(0, 0)):
+    """Forward convolution at sampled (n,k,p,q) coordinates.
+    Returns (values, sum|X*W|, number of terms)."""
+    x, w = _f64(x), _f64(w)
+    N, C, H, W_ = x.shape
+    K, _, R, S = w.shape
+    sh = make_shape(N, C, H, W_, K, R, S, stride, pad)
+    c, cp = _coords(coords)
+    m = len(c)
+    out, absd, nt = np.empty(m), np.empty(m), np.empty(m, np.int64)
+    _load().oracle_conv_fwd_at(ctypes.byref(sh), _dptr(x), _dptr(w), cp, m, _dptr(out), _dptr(absd),
+                               nt.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
+    return out, absd, nt
 
 
 def conv_bwd_data(dy, w, hw, stride=(1, 1), pad=(0, 0), mask=None, with_bound=False):

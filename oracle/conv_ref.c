@@ -237,6 +237,35 @@ void oracle_conv_bwd_weight_at(const oracle_shape* sh, const double* X, const do
     }
 }
 
+/* Sampled forward convolution at `count` (n,k,p,q) coordinates (Sec. II-A),
+ * with sum |X*W| and the number of in-range terms per output. */
+void oracle_conv_fwd_at(const oracle_shape* sh, const double* X, const double* Wt,
+                        const int32_t* coords, int64_t count,
+                        double* out, double* abs_out, int64_t* nterms)
+{
+    const oracle_shape s = *sh;
+    #pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < count; ++i) {
+        const int n = coords[4 * i], k = coords[4 * i + 1], p = coords[4 * i + 2], q = coords[4 * i + 3];
+        double acc = 0.0, aacc = 0.0;
+        int64_t cnt = 0;
+        for (int c = 0; c < s.C; ++c)
+            for (int r = 0; r < s.R; ++r)
+                for (int t = 0; t < s.S; ++t) {
+                    int h = p * s.stride_h - s.pad_h + r;
+                    int w = q * s.stride_w - s.pad_w + t;
+                    if (h < 0 || h >= s.H || w < 0 || w >= s.W) continue;
+                    double prod = X[IX4(n, c, h, w, s.C, s.H, s.W)] * Wt[IX4(k, c, r, t, s.C, s.R, s.S)];
+                    acc += prod;
+                    aacc += fabs(prod);
+                    ++cnt;
+                }
+        out[i] = acc;
+        if (abs_out) abs_out[i] = aacc;
+        if (nterms) nterms[i] = cnt;
+    }
+}
+
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int oracle_num_threads(void)
 {

@@ -300,6 +300,60 @@ def test_sampled_entry_points_match_full():
     assert np.array_equal(t, ntw.reshape(-1))
 
 
+# --------------------------------------------- forward with the ReLU fused
+
+def _brute_fwd_terms(x, w, stride, pad):
+    """Pure-Python loops: per output (sum x*w, sum |x*w|, number of terms)."""
+    N, C, H, W = x.shape
+    K, _, R, S = w.shape
+    P = (H + 2 * pad[0] - R) // stride[0] + 1
+    Q = (W + 2 * pad[1] - S) // stride[1] + 1
+    z, a, n = np.zeros((N, K, P, Q)), np.zeros((N, K, P, Q)), np.zeros((N, K, P, Q), np.int64)
+    for nn, k, p, q in itertools.product(range(N), range(K), range(P), range(Q)):
+        for c, r, t in itertools.product(range(C), range(R), range(S)):
+            h, ww = p * stride[0] - pad[0] + r, q * stride[1] - pad[1] + t
+            if 0 <= h < H and 0 <= ww < W:
+                z[nn, k, p, q] += x[nn, c, h, ww] * w[k, c, r, t]
+                a[nn, k, p, q] += abs(x[nn, c, h, ww] * w[k, c, r, t])
+                n[nn, k, p, q] += 1
+    return z, a, n
+
+
+@pytest.mark.parametrize("sh", SHAPES[::5])
+def test_forward_relu_brute_force(sh):
+    rng = np.random.default_rng(17)
+    x = _rand(rng, (sh["N"], sh["C"], sh["H"], sh["W"]), 0.6)
+    w = _rand(rng, (sh["K"], sh["C"], sh["R"], sh["S"]))
+    z, y, a, n = oracle.conv_fwd_relu(x, w, sh["stride"], sh["pad"])
+    zb, ab, nb = _brute_fwd_terms(x, w, sh["stride"], sh["pad"])
+    assert _rel(z, zb) < 1e-12 and _rel(a, ab) < 1e-12
+    assert np.array_equal(n, nb)
+    assert np.array_equal(y > 0, zb > 0)                      # the footprint is the sign of the sum
+    assert np.all(y[zb <= 0] == 0) and _rel(y[zb > 0], zb[zb > 0]) < 1e-12
+    # the emitted footprint is the bitmap of the stored output
+    assert np.array_equal(oracle.relu_mask(y), y > 0)
+
+
+def test_relu_reading_of_zero_and_nan():
+    y = oracle.relu(np.array([-0.0, 0.0, -1.0, 2.0, np.nan, 1e-300, -1e-300]))
+    assert np.array_equal(np.signbit(y[:3]), [False, False, False])    # every zero is +0.0
+    assert y[3] == 2.0 and y[4] == 0.0 and y[5] == 1e-300 and y[6] == 0.0
+
+
+def test_sampled_forward_matches_full():
+    rng = np.random.default_rng(37)
+    N, C, K, H, W, R, S = 2, 3, 4, 6, 5, 3, 2
+    for st, pad in [((1, 1), (1, 1)), ((2, 1), (0, 1))]:
+        x = _rand(rng, (N, C, H, W), 0.5)
+        w = _rand(rng, (K, C, R, S))
+        z, _, a, n = oracle.conv_fwd_relu(x, w, st, pad)
+        P, Q = z.shape[2:]
+        co = np.stack(np.meshgrid(range(N), range(K), range(P), range(Q), indexing="ij"), -1).reshape(-1, 4)
+        v, av, nv = oracle.conv_fwd_at(x, w, co, st, pad)
+        assert _rel(v, z.reshape(-1)) < 1e-12 and _rel(av, a.reshape(-1)) < 1e-12
+        assert np.array_equal(nv, n.reshape(-1))
+
+
 # ---------------------------------------------------- bitmaps and indexing
 
 def test_pack_bits_brute_force():
