@@ -190,6 +190,21 @@ def main():
                            "dw_gemm": "bwd_weight_kernel<bf16>"}[dom],
                 "kernel_ms": round(kern[dom], 4), "flops_per_launch": dom_flops}
 
+    # The forward convolution with the ReLU and the footprint fused (the
+    # producer of this layer's footprint), timed as a whole call on the same layer.
+    log("timing %d forward calls" % args.steps)
+    y_fwd = torch.empty((spec.N, desc.P, desc.Q, spec.K), dtype=x.dtype, device=dev)
+    ym_fwd = torch.empty(max(cb.cbw_dy_mask_words(desc), 1), dtype=torch.int32, device=dev)
+    ws_f = cb.workspace(desc, cb.CBW_OP_FWD, dev)
+
+    def fwd():
+        cb.conv_fwd_relu_mask(desc, x, w, y_fwd, ym_fwd, ws_f)
+
+    for _ in range(max(args.warmup // 4, 5)):
+        fwd()
+    ms_fwd, _ = timed(fwd, args.steps)
+    del y_fwd, ym_fwd, ws_f
+
     if args.copy_calibration:
         a = torch.ones(64 << 20, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
@@ -228,6 +243,7 @@ def main():
         "kernels_ms": {"dx_gemm": round(ms_dx_gemm, 4), "dw_gemm": round(ms_dw_gemm, 4),
                        "step_with_events": round(ms_sparse_k, 4)},
         "mask_pack_ms": round(ms_pack, 4),
+        "forward_relu_mask": {"ms": round(ms_fwd, 4), "tflops": round(f_conv / (ms_fwd * 1e-3) / 1e12, 2)},
         "flops": {"dx_dense": f_conv, "dw_dense": f_conv, "dx_useful": f_useful_dx, "dw_useful": f_useful_dw},
         "roofline": roofline,
         "cpu_baseline": cpu,

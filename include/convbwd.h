@@ -80,7 +80,7 @@ typedef struct {
 } cbw_conv_desc;
 
 /* Operation selector for cbw_workspace_size / cbw_read_stats. */
-enum { CBW_OP_BWD_DATA = 0, CBW_OP_BWD_DATA_MASKED = 1, CBW_OP_BWD_WEIGHT = 2 };
+enum { CBW_OP_BWD_DATA = 0, CBW_OP_BWD_DATA_MASKED = 1, CBW_OP_BWD_WEIGHT = 2, CBW_OP_FWD = 3 };
 
 /* Flags. CBW_FLAG_NO_SKIP runs the same kernels with every skip disabled:
  * the masked data gradient computes all rows and applies the mask in its
@@ -140,6 +140,21 @@ int conv_bwd_data_masked(const cbw_conv_desc* desc, const void* dY, const void* 
                          const uint32_t* x_mask, void* dX,
                          void* workspace, size_t workspace_bytes, uint32_t flags, void* stream);
 
+/* Forward convolution with the ReLU and the footprint of its output fused
+ * into one launch (Sec. II-A forward operation; the output bitmap that the
+ * backward pass consumes is produced by the forward pass, Sec. IV-B).
+ * Y[N,P,Q,K] = relu(conv(X, W)) in desc->dtype: float32 accumulation,
+ * round-to-nearest-even to bf16, non-positive (and NaN) sums give +0.0.
+ * y_mask (nullable; cbw_dy_mask_words(desc) words, 16-byte aligned) receives
+ * the bits (Y > 0) in Y's linear order -- exactly what cbw_relu_mask_pack
+ * computes on Y -- which is the next layer's x_mask and, as the ReLU
+ * derivative, the footprint of this layer's dY.  X is NHWC, W KRSC or KCRS.
+ * Stride 1 only, with pad_h < R and pad_w < S; other shapes return
+ * CBW_ERR_UNSUPPORTED.  Y and y_mask are fully overwritten.
+ * Workspace: cbw_workspace_size(desc, CBW_OP_FWD). */
+int conv_fwd_relu_mask(const cbw_conv_desc* desc, const void* X, const void* W, void* Y, uint32_t* y_mask,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
 /* Weight gradient with input sparsity (Sec. III-B; weight-gradient phase of
  * Sec. IV-B): dW (float32, layout desc->w_layout) from X[N,H,W,C] and
  * dY[N,P,Q,K].  Blocks of (pixel chunk x output-channel tile) in which dY is
@@ -184,8 +199,8 @@ int cbw_read_occupancy(const cbw_conv_desc* desc, const void* workspace, size_t 
  * (a hipEvent_t as void*) on the call's stream right before the op's main
  * GEMM kernel is launched and `stop` right after it, so that
  * hipEventElapsedTime(start, stop) is that kernel's duration.  op is
- * CBW_OP_BWD_DATA (covers both data-gradient entry points) or
- * CBW_OP_BWD_WEIGHT; NULL events switch the hook off. */
+ * CBW_OP_BWD_DATA (covers both data-gradient entry points),
+ * CBW_OP_BWD_WEIGHT or CBW_OP_FWD; NULL events switch the hook off. */
 int cbw_set_profile_events(int op, void* start, void* stop);
 
 #ifdef __cplusplus

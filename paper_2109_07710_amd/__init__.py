@@ -22,12 +22,13 @@ CBW_OK, CBW_ERR_INVALID_ARG, CBW_ERR_UNSUPPORTED, CBW_ERR_WORKSPACE, CBW_ERR_HIP
 CBW_NCHW, CBW_NHWC = 0, 1
 CBW_KCRS, CBW_KRSC = 0, 1
 CBW_F32, CBW_BF16 = 0, 1
-CBW_OP_BWD_DATA, CBW_OP_BWD_DATA_MASKED, CBW_OP_BWD_WEIGHT = 0, 1, 2
+CBW_OP_BWD_DATA, CBW_OP_BWD_DATA_MASKED, CBW_OP_BWD_WEIGHT, CBW_OP_FWD = 0, 1, 2, 3
 CBW_FLAG_NO_SKIP = 1
 
 EXPORTS = ("cbw_status_string", "cbw_validate_desc", "cbw_mask_words", "cbw_dy_mask_words",
            "cbw_workspace_size", "cbw_relu_mask_pack", "cbw_nonzero_mask_pack", "conv_bwd_data",
-           "conv_bwd_data_masked", "conv_bwd_weight_sparse", "cbw_read_stats", "cbw_read_live_lists",
+           "conv_bwd_data_masked", "conv_fwd_relu_mask", "conv_bwd_weight_sparse", "cbw_read_stats",
+           "cbw_read_live_lists",
            "cbw_read_occupancy", "cbw_set_profile_events")
 
 
@@ -87,6 +88,7 @@ def lib():
     L.cbw_nonzero_mask_pack.argtypes = [ctypes.c_int32, ctypes.c_int64, vp, vp, vp]
     L.conv_bwd_data.argtypes = [dp, vp, vp, vp, vp, sz, vp]
     L.conv_bwd_data_masked.argtypes = [dp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
+    L.conv_fwd_relu_mask.argtypes = [dp, vp, vp, vp, vp, vp, sz, vp]
     L.conv_bwd_weight_sparse.argtypes = [dp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
     L.cbw_read_stats.argtypes = [dp, ctypes.c_int, vp, sz, ctypes.POINTER(Stats), vp]
     i32p = ctypes.POINTER(ctypes.c_int32)
@@ -177,6 +179,12 @@ def conv_bwd_data(desc, dY, W, dX, ws, stream=None):
 def conv_bwd_data_masked(desc, dY, W, x_mask, dX, ws, flags=0, stream=None):
     _check(lib().conv_bwd_data_masked(ctypes.byref(desc), _ptr(dY), _ptr(W), _ptr(x_mask), _ptr(dX),
                                       _ptr(ws), _nbytes(ws), flags, _stream(stream)), "conv_bwd_data_masked")
+
+
+def conv_fwd_relu_mask(desc, X, W, Y, y_mask, ws, stream=None):
+    """Y = relu(conv(X, W)) and, when y_mask is given, its footprint bits."""
+    _check(lib().conv_fwd_relu_mask(ctypes.byref(desc), _ptr(X), _ptr(W), _ptr(Y), _ptr(y_mask), _ptr(ws),
+                                    _nbytes(ws), _stream(stream)), "conv_fwd_relu_mask")
 
 
 def conv_bwd_weight_sparse(desc, X, dY, dy_mask, dW, ws, flags=0, stream=None):

@@ -12,8 +12,9 @@ namespace {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-// Profiling events per op family (0 = data gradient, 1 = weight gradient).
-thread_local hipEvent_t g_prof[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
+// Profiling events per op family (0 = data gradient, 1 = weight gradient,
+// 2 = forward).
+thread_local hipEvent_t g_prof[3][2] = {{nullptr, nullptr}, {nullptr, nullptr}, {nullptr, nullptr}};
 
 hipError_t prof_mark(int fam, int which, hipStream_t s)
 {
@@ -118,6 +119,44 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
     return hip_status(prof_mark(0, 1, s));
 }
 
+int run_fwd(const cbw_conv_desc* desc, const void* X, const void* W, void* Y, uint32_t* y_mask, void* ws,
+            size_t ws_bytes, void* stream)
+{
+    cbw_conv_desc vd;
+    int st = fwd_as_data_desc(desc, &vd);
+    if (st != CBW_OK) return st;
+    DataPlan plan;
+    if ((st = plan_data(&vd, false, &plan)) != CBW_OK) return st;
+    if (!X || !W || !Y) return CBW_ERR_INVALID_ARG;
+    if (!aligned16(X) || !aligned16(W) || !aligned16(Y) || (y_mask && !aligned16(y_mask)))
+        return CBW_ERR_UNSUPPORTED;
+    if ((st = check_ws(ws, ws_bytes, plan.total)) != CBW_OK) return st;
+    if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    int* header = at<int>(ws, plan.header);
+    void* wt = at<void>(ws, plan.wt);
+    DataParams p = data_params(&vd, X, wt, Y, plan.npix, plan.groups);
+    p.ptiles = plan.ptiles;
+    p.nslots = kDataSlots;
+    p.smax = kDataMaxSplit;
+    p.split = plan.split;
+    p.partial = plan.partial.bytes ? at<float>(ws, plan.partial) : nullptr;
+    p.out_mask = y_mask;
+    // footprint words are assembled whole in the GEMM epilogue when the
+    // output channel count is a multiple of 32 and nothing is split;
+    // otherwise they are OR-ed in and must start cleared
+    const int64_t words = ((int64_t)desc->N * desc->P * desc->Q * desc->K + 31) / 32;
+    const bool clear = y_mask && (desc->K % 32 != 0 || plan.split > 1);
+    hipError_t e = launch_fwd_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R, desc->S,
+                                   desc->w_layout == CBW_KRSC, header, clear ? y_mask : nullptr,
+                                   clear ? words : 0, s);
+    if (e != hipSuccess) return hip_status(e);
+    if ((e = prof_mark(2, 0, s)) != hipSuccess) return hip_status(e);
+    if ((e = launch_bwd_data(desc->dtype, MODE_FWD, p, s)) != hipSuccess) return hip_status(e);
+    return hip_status(prof_mark(2, 1, s));
+}
+
 }  // namespace
 
 extern "C" {
@@ -164,6 +203,14 @@ int cbw_workspace_size(const cbw_conv_desc* desc, int op, size_t* bytes)
         *bytes = p.total;
         return CBW_OK;
     }
+    if (op == CBW_OP_FWD) {
+        cbw_conv_desc vd;
+        DataPlan p;
+        if ((st = fwd_as_data_desc(desc, &vd)) != CBW_OK) return st;
+        if ((st = plan_data(&vd, false, &p)) != CBW_OK) return st;
+        *bytes = p.total;
+        return CBW_OK;
+    }
     return CBW_ERR_INVALID_ARG;
 }
 
@@ -196,6 +243,12 @@ int conv_bwd_data_masked(const cbw_conv_desc* desc, const void* dY, const void* 
                          void* dX, void* workspace, size_t workspace_bytes, uint32_t flags, void* stream)
 {
     return run_bwd_data(desc, dY, W, x_mask, dX, workspace, workspace_bytes, flags, stream, true);
+}
+
+int conv_fwd_relu_mask(const cbw_conv_desc* desc, const void* X, const void* W, void* Y, uint32_t* y_mask,
+                       void* workspace, size_t workspace_bytes, void* stream)
+{
+    return run_fwd(desc, X, W, Y, y_mask, workspace, workspace_bytes, stream);
 }
 
 int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void* dY, const uint32_t* dy_mask,
@@ -318,6 +371,7 @@ int cbw_set_profile_events(int op, void* start, void* stop)
     int fam;
     if (op == CBW_OP_BWD_DATA || op == CBW_OP_BWD_DATA_MASKED) fam = 0;
     else if (op == CBW_OP_BWD_WEIGHT) fam = 1;
+    else if (op == CBW_OP_FWD) fam = 2;
     else return CBW_ERR_INVALID_ARG;
     if ((start == nullptr) != (stop == nullptr)) return CBW_ERR_INVALID_ARG;
     g_prof[fam][0] = static_cast<hipEvent_t>(start);

@@ -62,7 +62,8 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
     __shared__ uint4 As[2][BM * CH];
     __shared__ uint4 Bs[2][BN * CH];
     __shared__ int pix_s[BN];
-    __shared__ uint32_t msk_s[MODE == MODE_DENSE ? 1 : BN * (BM / 32)];
+    constexpr bool SEL = MODE == MODE_SELECT || MODE == MODE_GATHER;   // footprint select in the epilogue
+    __shared__ uint32_t msk_s[SEL ? BN * (BM / 32) : 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -256,8 +257,8 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
     // epilogue needs them: they are fetched from inside the main loop, next
     // to step 1's copies (so no wait is spent on them), held in registers
     // and staged in LDS after the loop.
-    const bool mask_lds = MODE != MODE_DENSE && (p.C % 32) == 0 && nsplit == 1;
-    constexpr int MW = MODE == MODE_DENSE ? 0 : BN * (BM / 32);   // footprint words per tile
+    const bool mask_lds = SEL && (p.C % 32) == 0 && nsplit == 1;
+    constexpr int MW = SEL ? BN * (BM / 32) : 0;                  // footprint words per tile
     constexpr int MI = MW > 0 ? (MW + NT - 1) / NT : 1;          // per thread
     uint32_t mwords[MI];
     auto fetch_mask = [&]() {
@@ -370,6 +371,68 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
             for (int w = 0; w < MWJ; ++w) ew[j][w] = msk_s[pr * (BM / 32) + (wm * TM) / 32 + w];
         }
     }
+    // Forward: ReLU, rounding to the output type, and the footprint of the
+    // stored output (bit = stored value > 0, i.e. non-zero after the ReLU)
+    // in the same pass.  With the output channel count a multiple of 32 the
+    // 4-bit pieces of the four lanes that cover one 32-channel word (lanes
+    // l, l+16, l+32, l+48) are merged by two lane exchanges and stored as a
+    // whole word; otherwise each piece is OR-ed into its word atomically
+    // (those words were cleared by the preparation kernel).  Non-positive
+    // and NaN sums give +0.0.
+    auto fwd_epilogue = [&]() {
+        static_assert(FM % 2 == 0 && TM % 32 == 0, "two 16-channel blocks per footprint word");
+        const bool emit = p.out_mask != nullptr;
+        const bool whole_words = (p.C % 32) == 0;
+        const int q = lane >> 4;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int pr = wn * TN + j * 16 + (lane & 15);
+            const int pix = pix_s[pr];
+            const int clane = wm * TM + 4 * q;
+            const uint32_t base = (uint32_t)(pix * p.C + c0 + clane) * ESZ;
+            uint32_t nib[FM];
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const bool ok = pix >= 0 && c0 + clane + i * 16 < p.C;
+                const uint32_t off = ok ? base + (uint32_t)(i * 16) * ESZ : kOOB;
+                const floatx4 v = acc[i][j];
+                const float y0 = v.x > 0.f ? v.x : 0.f, y1 = v.y > 0.f ? v.y : 0.f;
+                const float y2 = v.z > 0.f ? v.z : 0.f, y3 = v.w > 0.f ? v.w : 0.f;
+                uint32_t bits;
+                if constexpr (sizeof(T) == 2) {
+                    const uint32_t h01 = pack_bf16x2(y0, y1), h23 = pack_bf16x2(y2, y3);
+                    __builtin_amdgcn_raw_buffer_store_b64(u32x2{h01, h23}, rs_dx, off, 0, 0);
+                    bits = (uint32_t)((h01 & 0xffffu) != 0) | ((uint32_t)((h01 >> 16) != 0) << 1) |
+                           ((uint32_t)((h23 & 0xffffu) != 0) << 2) | ((uint32_t)((h23 >> 16) != 0) << 3);
+                } else {
+                    const u32x4 d = {__float_as_uint(y0), __float_as_uint(y1), __float_as_uint(y2), __float_as_uint(y3)};
+                    __builtin_amdgcn_raw_buffer_store_b128(d, rs_dx, off, 0, 0);
+                    bits = (uint32_t)(y0 > 0.f) | ((uint32_t)(y1 > 0.f) << 1) | ((uint32_t)(y2 > 0.f) << 2) |
+                           ((uint32_t)(y3 > 0.f) << 3);
+                }
+                nib[i] = ok ? bits : 0u;
+            }
+            if (!emit) continue;
+            if (whole_words) {
+#pragma unroll
+                for (int w = 0; w < FM / 2; ++w) {
+                    uint32_t x = (nib[2 * w] << (4 * q)) | (nib[2 * w + 1] << (16 + 4 * q));
+                    x |= __shfl_xor(x, 16);
+                    x |= __shfl_xor(x, 32);
+                    const int cw = c0 + wm * TM + 32 * w;
+                    if (q == 0 && pix >= 0 && cw < p.C) p.out_mask[((int64_t)pix * p.C + cw) >> 5] = x;
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < FM; ++i) {
+                    if (nib[i] == 0) continue;
+                    const int64_t o = (int64_t)pix * p.C + c0 + clane + i * 16;
+                    atomicOr(&p.out_mask[o >> 5], nib[i] << (o & 31));
+                }
+            }
+        }
+    };
+
     // One straight-line body per footprint source (words staged in LDS, or
     // read per element when C is not a multiple of 32); the choice is
     // uniform across the workgroup.
@@ -387,7 +450,7 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
                 const bool ok = pix >= 0 && c0 + cl < p.C;
                 const uint32_t off = ok ? base + (uint32_t)(i * 16) * ESZ : kOOB;
                 uint32_t keep = 0xfu;
-                if (MODE != MODE_DENSE) {
+                if (SEL) {
                     if constexpr (LDSW) {
                         keep = (ew[j][(i * 16) / 32] >> (cl & 31)) & 0xfu;
                     } else {
@@ -411,6 +474,10 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
             }
         }
     };
+    if constexpr (MODE == MODE_FWD) {
+        fwd_epilogue();
+        return;
+    }
     if (MODE == MODE_DENSE || mask_lds) epilogue(std::true_type{});
     else epilogue(std::false_type{});
 }
@@ -457,6 +524,48 @@ __global__ __launch_bounds__(256) void data_prep_kernel(const T* __restrict__ w,
     }
     const int b = blockIdx.x - ntb;
     compact_count_block(cp, b % cp.nblk, b / cp.nblk);
+}
+
+// Forward preparation (launch_fwd_prep).  Blocks [0, ntb) build the GEMM
+// operand Wf[tap'][k][c] = W[k][tap][c] with tap' = (R-1-r)*S + (S-1-s): a
+// KRSC thread moves one 16-byte vector of E channels of (k, tap) (coalesced
+// on both sides), a KCRS thread the R*S taps of one (k, c).  The remaining
+// blocks clear zero_words footprint words.
+template <typename T>
+__global__ __launch_bounds__(256) void fwd_prep_kernel(const T* __restrict__ w, T* __restrict__ wt, int K, int C,
+                                                       int R, int S, int krsc, int* header, uint32_t* zero,
+                                                       int64_t zero_words, int ntb)
+{
+    constexpr int E = Elem<T>::E;
+    const int RS = R * S;
+    if ((int)blockIdx.x < ntb) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) header[0] = MODE_FWD;
+        const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+        if (krsc) {
+            const int CV = C / E;
+            if (t >= (int64_t)K * RS * CV) return;
+            const int cv = (int)(t % CV);
+            const int64_t rest = t / CV;
+            const int tap = (int)(rest % RS);
+            const int k = (int)(rest / RS);
+            const int r = tap / S, s = tap - r * S;
+            const int tf = (R - 1 - r) * S + (S - 1 - s);
+            *reinterpret_cast<uint4*>(wt + ((int64_t)tf * K + k) * C + cv * E) =
+                *reinterpret_cast<const uint4*>(w + ((int64_t)k * RS + tap) * C + cv * E);
+        } else {
+            if (t >= (int64_t)K * C) return;
+            const int c = (int)(t % C);
+            const int k = (int)(t / C);
+            for (int tap = 0; tap < RS; ++tap) {
+                const int r = tap / S, s = tap - r * S;
+                const int tf = (R - 1 - r) * S + (S - 1 - s);
+                wt[((int64_t)tf * K + k) * C + c] = w[((int64_t)k * C + c) * RS + tap];
+            }
+        }
+        return;
+    }
+    const int64_t stride = (int64_t)(gridDim.x - ntb) * 256;
+    for (int64_t i = (int64_t)(blockIdx.x - ntb) * 256 + threadIdx.x; i < zero_words; i += stride) zero[i] = 0u;
 }
 
 // Sums the nsplit partial tiles of every live tile in split order and writes
@@ -508,6 +617,26 @@ __global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
         for (int zz = 1; zz < nsplit; ++zz)
             s += *reinterpret_cast<const floatx4*>(p.partial + (((int64_t)tile * nsplit + zz) * BN + pr) * BM + cl);
         const int64_t o = (int64_t)pix * p.C + c;
+        if constexpr (MODE == MODE_FWD) {
+            // ReLU, rounding and footprint bits as in the GEMM's forward epilogue
+            // (the footprint words were cleared by the preparation kernel)
+            const float y0 = s.x > 0.f ? s.x : 0.f, y1 = s.y > 0.f ? s.y : 0.f;
+            const float y2 = s.z > 0.f ? s.z : 0.f, y3 = s.w > 0.f ? s.w : 0.f;
+            uint32_t bits;
+            if constexpr (sizeof(T) == 2) {
+                const uint32_t h01 = pack_bf16x2(y0, y1), h23 = pack_bf16x2(y2, y3);
+                *reinterpret_cast<uint2*>(dx + o) = make_uint2(h01, h23);
+                bits = (uint32_t)((h01 & 0xffffu) != 0) | ((uint32_t)((h01 >> 16) != 0) << 1) |
+                       ((uint32_t)((h23 & 0xffffu) != 0) << 2) | ((uint32_t)((h23 >> 16) != 0) << 3);
+            } else {
+                *reinterpret_cast<uint4*>(dx + o) =
+                    make_uint4(__float_as_uint(y0), __float_as_uint(y1), __float_as_uint(y2), __float_as_uint(y3));
+                bits = (uint32_t)(y0 > 0.f) | ((uint32_t)(y1 > 0.f) << 1) | ((uint32_t)(y2 > 0.f) << 2) |
+                       ((uint32_t)(y3 > 0.f) << 3);
+            }
+            if (p.out_mask != nullptr && bits != 0) atomicOr(&p.out_mask[o >> 5], bits << (o & 31));
+            continue;
+        }
         uint32_t keep = 0xfu;
         if (MODE != MODE_DENSE) keep = (p.mask[o >> 5] >> (o & 31)) & 0xfu;
         if constexpr (sizeof(T) == 2) {
@@ -553,6 +682,23 @@ hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, in
     return hipGetLastError();
 }
 
+hipError_t launch_fwd_prep(int dtype, const void* w, void* wt, int K, int C, int R, int S, int krsc, int* header,
+                           uint32_t* zero, int64_t zero_words, hipStream_t stream)
+{
+    const int E = dtype == 1 ? 8 : 4;
+    const int64_t nthreads = krsc ? (int64_t)K * R * S * (C / E) : (int64_t)K * C;
+    const int ntb = (int)((nthreads + 255) / 256);
+    const int64_t zb = (zero_words + 255) / 256;
+    const int nzb = zero_words > 0 ? (int)(zb < 1024 ? zb : 1024) : 0;
+    if (dtype == 1)
+        fwd_prep_kernel<uint16_t><<<ntb + nzb, 256, 0, stream>>>((const uint16_t*)w, (uint16_t*)wt, K, C, R, S, krsc,
+                                                                 header, zero, zero_words, ntb);
+    else
+        fwd_prep_kernel<float><<<ntb + nzb, 256, 0, stream>>>((const float*)w, (float*)wt, K, C, R, S, krsc, header,
+                                                              zero, zero_words, ntb);
+    return hipGetLastError();
+}
+
 hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream)
 {
     // enough workgroups for every tile unsplit, or for nslots split items
@@ -567,10 +713,12 @@ hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t
     if (dtype == 1) {
         if (mode == MODE_DENSE) CBW_LAUNCH(uint16_t, MODE_DENSE);
         else if (mode == MODE_SELECT) CBW_LAUNCH(uint16_t, MODE_SELECT);
+        else if (mode == MODE_FWD) CBW_LAUNCH(uint16_t, MODE_FWD);
         else CBW_LAUNCH(uint16_t, MODE_GATHER);
     } else {
         if (mode == MODE_DENSE) CBW_LAUNCH(float, MODE_DENSE);
         else if (mode == MODE_SELECT) CBW_LAUNCH(float, MODE_SELECT);
+        else if (mode == MODE_FWD) CBW_LAUNCH(float, MODE_FWD);
         else CBW_LAUNCH(float, MODE_GATHER);
     }
 #undef CBW_LAUNCH
@@ -584,10 +732,12 @@ hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t
         if (dtype == 1) {
             if (mode == MODE_DENSE) CBW_REDUCE(uint16_t, MODE_DENSE);
             else if (mode == MODE_SELECT) CBW_REDUCE(uint16_t, MODE_SELECT);
+            else if (mode == MODE_FWD) CBW_REDUCE(uint16_t, MODE_FWD);
             else CBW_REDUCE(uint16_t, MODE_GATHER);
         } else {
             if (mode == MODE_DENSE) CBW_REDUCE(float, MODE_DENSE);
             else if (mode == MODE_SELECT) CBW_REDUCE(float, MODE_SELECT);
+            else if (mode == MODE_FWD) CBW_REDUCE(float, MODE_FWD);
             else CBW_REDUCE(float, MODE_GATHER);
         }
 #undef CBW_REDUCE

@@ -8,7 +8,10 @@
 
 namespace cbw {
 
-enum { MODE_DENSE = 0, MODE_SELECT = 1, MODE_GATHER = 2 };
+// Data-gradient GEMM modes; MODE_FWD runs the same GEMM as the forward
+// convolution (flipped filters, padding R-1-pad, stride 1) with a ReLU
+// epilogue that also emits the output's footprint bits.
+enum { MODE_DENSE = 0, MODE_SELECT = 1, MODE_GATHER = 2, MODE_FWD = 3 };
 
 struct DataParams {
     const void* dy;          // [N*P*Q][K]
@@ -26,6 +29,7 @@ struct DataParams {
     int nslots, smax;        // resident workgroups; largest split
     float* partial;          // [item][BN][BM] fp32 partial tiles when split
     uint32_t dy_bytes, wt_bytes, dx_bytes;
+    uint32_t* out_mask;      // MODE_FWD: footprint bits of the output (nullable)
     FastDiv div_w, div_h;    // pixel -> (n, h, w)
 };
 
@@ -74,6 +78,11 @@ int compact_block_pixels();
 hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, int RS, int krsc, int* header,
                             int mode, const CompactParams* cp, hipStream_t stream);
 hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream);
+// Forward preparation: Wf[tap'][k][c] = W[k][tap][c] with tap' the flipped tap
+// (R-1-r, S-1-s), the workspace header stamped, and `zero_words` words of
+// `zero` cleared (footprint words filled by atomic OR), in one launch.
+hipError_t launch_fwd_prep(int dtype, const void* w, void* wt, int K, int C, int R, int S, int krsc, int* header,
+                           uint32_t* zero, int64_t zero_words, hipStream_t stream);
 hipError_t launch_compact_scatter(const CompactParams& p, hipStream_t stream);
 hipError_t launch_relu_mask_pack(int dtype, int64_t count, const void* x, uint32_t* bits, int relu,
                                  hipStream_t stream);

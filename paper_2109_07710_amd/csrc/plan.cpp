@@ -78,6 +78,23 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out)
     return CBW_OK;
 }
 
+int fwd_as_data_desc(const cbw_conv_desc* d, cbw_conv_desc* out)
+{
+    int st = validate_desc(d);
+    if (st != CBW_OK) return st;
+    if (d->stride_h != 1 || d->stride_w != 1) return CBW_ERR_UNSUPPORTED;
+    if (d->pad_h > d->R - 1 || d->pad_w > d->S - 1) return CBW_ERR_UNSUPPORTED;
+    cbw_conv_desc v = *d;
+    v.C = d->K; v.K = d->C;
+    v.H = d->P; v.W = d->Q;
+    v.P = d->H; v.Q = d->W;
+    v.pad_h = d->R - 1 - d->pad_h;
+    v.pad_w = d->S - 1 - d->pad_w;
+    if ((st = validate_desc(&v)) != CBW_OK) return st;
+    *out = v;
+    return CBW_OK;
+}
+
 int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
 {
     int st = validate_desc(d);

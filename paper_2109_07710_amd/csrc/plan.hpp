@@ -58,6 +58,12 @@ struct WeightPlan {
 int validate_desc(const cbw_conv_desc* d);
 int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out);
 int plan_weight(const cbw_conv_desc* d, WeightPlan* out);
+// The forward convolution as a data-gradient GEMM: for stride 1, Y = conv(X, W)
+// is the backward-data operation with the roles of C and K, of (H, W) and
+// (P, Q) interchanged, the filter taps flipped and padding R-1-pad.  Writes that
+// descriptor (validated) or returns CBW_ERR_UNSUPPORTED for stride > 1 or
+// pad > R-1 (S-1).
+int fwd_as_data_desc(const cbw_conv_desc* d, cbw_conv_desc* out);
 inline int elem_bytes(int dtype) { return dtype == CBW_BF16 ? 2 : 4; }
 
 }  // namespace cbw

@@ -102,6 +102,32 @@ def test_workspace_sizes(L):
     assert L.cbw_workspace_size(ctypes.byref(d), 0, None) == cb.CBW_ERR_INVALID_ARG
 
 
+def test_forward_descriptor_rules(L):
+    """The forward runs as the data-gradient GEMM with C and K, (H, W) and
+    (P, Q) interchanged, flipped taps and padding R-1-pad: stride 1 only."""
+    d = cb.ConvDesc.make(32, 256, 56, 56, 256, 3, 3, 1, 1)
+    fwd = cb.cbw_workspace_size(d, cb.CBW_OP_FWD)
+    assert fwd == cb.cbw_workspace_size(d, cb.CBW_OP_BWD_DATA)   # same shape with C = K
+    assert fwd >= 256 * 256 * 9 * 2 + 256
+    d2 = cb.ConvDesc.make(2, 64, 10, 12, 128, 3, 3, 1, 1)           # C != K: forward plans as (C, K) swapped
+    swapped = cb.ConvDesc.make(2, 128, 10, 12, 64, 3, 3, 1, 1)
+    assert cb.cbw_workspace_size(d2, cb.CBW_OP_FWD) == cb.cbw_workspace_size(swapped, cb.CBW_OP_BWD_DATA)
+    assert cb.cbw_workspace_size(_desc(R=1, S=1, pad=(0, 0)), cb.CBW_OP_FWD) > 0
+    n = ctypes.c_size_t(0)
+    for bad in (_desc(stride=(2, 1)), _desc(stride=(1, 2)), _desc(R=3, S=3, pad=(3, 1)), _desc(R=1, S=3, pad=(1, 1))):
+        assert L.cbw_workspace_size(ctypes.byref(bad), cb.CBW_OP_FWD, ctypes.byref(n)) == cb.CBW_ERR_UNSUPPORTED
+        assert L.conv_fwd_relu_mask(ctypes.byref(bad), None, None, None, None, None, 0, None) == \
+            cb.CBW_ERR_UNSUPPORTED
+    fake = ctypes.c_void_p(1 << 20)
+    assert L.conv_fwd_relu_mask(ctypes.byref(_desc()), None, fake, fake, None, None, 0, None) == \
+        cb.CBW_ERR_INVALID_ARG
+    assert L.conv_fwd_relu_mask(ctypes.byref(_desc()), fake, fake, fake, None, None, 0, None) == \
+        cb.CBW_ERR_WORKSPACE
+    misaligned = ctypes.c_void_p((1 << 20) + 4)
+    assert L.conv_fwd_relu_mask(ctypes.byref(_desc()), fake, fake, fake, misaligned, None, 0, None) == \
+        cb.CBW_ERR_UNSUPPORTED
+
+
 def test_null_arguments_rejected_without_gpu(L):
     d = _desc()
     n = ctypes.c_size_t(0)
