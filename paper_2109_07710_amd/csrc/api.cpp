@@ -35,8 +35,9 @@ bool tiles_consistent()
 {
     static_assert(kDataMaxSplit >= 1, "split bound");
     if (data_split(1, 1 << 20, kDataSlots, kDataMaxSplit) != host_data_split(1, 1 << 20)) return false;
-    return data_tile_channels() == kDataTileC && data_tile_pixels() == kDataTileP &&
-           weight_tile_channels() == kWeightTileC && weight_tile_k() == kWeightTileK &&
+    for (int t = 0; t < kDataTileCount; ++t)
+        if (data_tile_channels(t) != kDataTiles[t].bm || data_tile_pixels(t) != kDataTiles[t].bn) return false;
+    return weight_tile_channels() == kWeightTileC && weight_tile_k() == kWeightTileK &&
            compact_block_pixels() == kCompactBlock && weight_chunk(CBW_BF16) == weight_chunk_px(CBW_BF16) &&
            weight_chunk(CBW_F32) == weight_chunk_px(CBW_F32);
 }
@@ -88,6 +89,7 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
     int* header = at<int>(ws, plan.header);
     void* wt = at<void>(ws, plan.wt);
     DataParams p = data_params(desc, dY, wt, dX, plan.npix, plan.groups);
+    p.tile = plan.tile;
     p.mask = x_mask;
     p.ptiles = plan.ptiles;
     p.nslots = kDataSlots;
@@ -103,7 +105,7 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
         cp.dx = dX;
         cp.npix = (int)plan.npix;
         cp.C = desc->C;
-        cp.G = kDataTileC;
+        cp.G = plan.bm;
         cp.groups = plan.groups;
         cp.nblk = plan.nblk;
         cp.elem_bytes = elem_bytes(desc->dtype);
@@ -137,6 +139,7 @@ int run_fwd(const cbw_conv_desc* desc, const void* X, const void* W, void* Y, ui
     int* header = at<int>(ws, plan.header);
     void* wt = at<void>(ws, plan.wt);
     DataParams p = data_params(&vd, X, wt, Y, plan.npix, plan.groups);
+    p.tile = plan.tile;
     p.ptiles = plan.ptiles;
     p.nslots = kDataSlots;
     p.smax = kDataMaxSplit;
@@ -396,7 +399,7 @@ int cbw_read_live_lists(const cbw_conv_desc* desc, const void* workspace, size_t
     if (e != hipSuccess) return hip_status(e);
     if (n < 0 || n > plan.npix) return CBW_ERR_INVALID_ARG;  // workspace not written by a gather call
     *count = n;
-    *group_width = kDataTileC;
+    *group_width = plan.bm;
     if (pixels && n > 0) {
         e = hipMemcpyAsync(pixels, at<int32_t>(ws, plan.lists) + (int64_t)group * plan.npix,
                            (size_t)n * sizeof(int32_t), hipMemcpyDeviceToHost, s);

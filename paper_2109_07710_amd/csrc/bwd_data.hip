@@ -36,25 +36,34 @@ namespace cbw {
 
 namespace {
 
-constexpr int BM = CBW_DX_BM;     // channels per tile (= compaction group width)
-constexpr int BN = CBW_DX_BN;     // pixels per tile
-constexpr int WM = CBW_DX_WM;     // waves along channels
-constexpr int WN = CBW_DX_WN;     // waves along pixels
-constexpr int NT = 64 * WM * WN;
-constexpr int TM = BM / WM, TN = BN / WN;   // wave tile
-constexpr int FM = TM / 16, FN = TN / 16;   // 16x16 MFMA tiles per wave
-constexpr int CH = 8;                       // 16-byte chunks of reduction per row per step
-constexpr int NW = WM * WN;                 // waves
-constexpr int IA = (BM / 8 + NW - 1) / NW;  // 1 KB copy instructions per wave per step, A
-constexpr int IB = (BN / 8 + NW - 1) / NW;  // same for B
-static_assert(BM % 8 == 0 && BN % 8 == 0, "tiles are copied in groups of 8 rows");
-static_assert(TM % 16 == 0 && TN % 16 == 0, "wave tile must be a multiple of 16");
+constexpr int NT = 512;   // 8 waves (two per SIMD) for every tile shape
+constexpr int CH = 8;     // 16-byte chunks of reduction per row per step
+
+// Compile-time shape of data-gradient tile TI (kDataTiles[TI]).
+template <int TI>
+struct Tile {
+    static constexpr int BM = kDataTiles[TI].bm;       // channels per tile (= compaction group width)
+    static constexpr int BN = kDataTiles[TI].bn;       // pixels per tile
+    static constexpr int WM = kDataTiles[TI].wm;       // waves along channels
+    static constexpr int WN = kDataTiles[TI].wn;       // waves along pixels
+    static constexpr int NW = WM * WN;
+    static constexpr int TM = BM / WM, TN = BN / WN;   // wave tile
+    static constexpr int FM = TM / 16, FN = TN / 16;   // 16x16 MFMA tiles per wave
+    static constexpr int IA = (BM / 8 + NW - 1) / NW;  // 1 KB copy instructions per wave per step, A
+    static constexpr int IB = (BN / 8 + NW - 1) / NW;  // same for B
+    static_assert(NW * 64 == NT, "eight waves");
+    static_assert(BM % 8 == 0 && BN % 8 == 0, "tiles are copied in groups of 8 rows");
+    static_assert(TM % 16 == 0 && TN % 16 == 0, "wave tile must be a multiple of 16");
+};
 
 __device__ __forceinline__ int swz8(int row) { return (row >> 1) & 7; }
 
-template <typename T, int MODE, bool UNIT>
+template <typename T, int MODE, bool UNIT, int TI>
 __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
 {
+    using TL = Tile<TI>;
+    constexpr int BM = TL::BM, BN = TL::BN, WN = TL::WN, NW = TL::NW;
+    constexpr int TM = TL::TM, TN = TL::TN, FM = TL::FM, FN = TL::FN, IA = TL::IA, IB = TL::IB;
     constexpr int E = Elem<T>::E;
     constexpr int BK = CH * E;     // reduction elements per step
     constexpr uint32_t ESZ = sizeof(T);
@@ -277,47 +286,6 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
     const int mask_step = nloc > 1 ? 1 : 0;
     wait_vmem();
     __syncthreads();
-#if CBW_DX_PIPE
-    static_assert(CH == 8, "two chunk groups per step");
-    // Two register sets of fragments: while the MFMAs of one chunk group run,
-    // the fragments of the next one are already being read.  Group 1 of a
-    // step is read before the barrier, group 0 of the next step right after
-    // it (its copies have landed by then).
-    auto read_frags = [&](int buf, int kc, uint4 (&fa)[FM], uint4 (&fb)[FN]) {
-        const int chl = kc * 4 + (lane >> 4);
-#pragma unroll
-        for (int i = 0; i < FM; ++i) {
-            const int row = wm * TM + i * 16 + (lane & 15);
-            fa[i] = As[buf][row * CH + (chl ^ swz8(row))];
-        }
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const int row = wn * TN + j * 16 + (lane & 15);
-            fb[j] = Bs[buf][row * CH + (chl ^ swz8(row))];
-        }
-    };
-    auto mma = [&](const uint4 (&fa)[FM], const uint4 (&fb)[FN]) {
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-            for (int j = 0; j < FN; ++j) acc[i][j] = mfma_chunk(acc[i][j], fa[i], fb[j], T{});
-    };
-    uint4 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
-    read_frags(0, 0, fa0, fb0);
-    for (int step = 0; step < nloc; ++step) {
-        const int buf = step & 1;
-        if (step + 1 < nloc) load(buf ^ 1);
-        if (mask_lds && step == mask_step) fetch_mask();
-        read_frags(buf, 1, fa1, fb1);
-        mma(fa0, fb0);
-        // keep the waits and the barrier behind this group's MFMAs
-        __builtin_amdgcn_sched_barrier(0);
-        wait_vmem_lds();
-        __syncthreads();
-        if (step + 1 < nloc) read_frags(buf ^ 1, 0, fa0, fb0);
-        mma(fa1, fb1);
-    }
-#else
     for (int step = 0; step < nloc; ++step) {
         const int buf = step & 1;
         if (step + 1 < nloc) load(buf ^ 1);
@@ -326,7 +294,6 @@ __global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
         wait_vmem();
         __syncthreads();
     }
-#endif
 
     if (mask_lds) {
         // msk_s is not an operand buffer: no barrier is needed before writing it
@@ -571,9 +538,10 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const T* __restrict__ w, 
 // Sums the nsplit partial tiles of every live tile in split order and writes
 // dX like the GEMM epilogue would (footprint select, rounding).  Runs with a
 // fixed grid; exits at once when the GEMM did not split.
-template <typename T, int MODE>
+template <typename T, int MODE, int TI>
 __global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
 {
+    constexpr int BM = Tile<TI>::BM, BN = Tile<TI>::BN;
     constexpr int E = Elem<T>::E;
     const int kchunks = (p.K + CH * E - 1) / (CH * E);
     const int nsteps = p.R * p.S * kchunks;
@@ -658,8 +626,14 @@ __global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
 
 }  // namespace
 
-int data_tile_channels() { return BM; }
-int data_tile_pixels() { return BN; }
+int data_tile_channels(int tile)
+{
+    return tile == 0 ? Tile<0>::BM : tile == 1 ? Tile<1>::BM : Tile<2>::BM;
+}
+int data_tile_pixels(int tile)
+{
+    return tile == 0 ? Tile<0>::BN : tile == 1 ? Tile<1>::BN : Tile<2>::BN;
+}
 
 hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, int RS, int krsc, int* header,
                             int mode, const CompactParams* cp, hipStream_t stream)
@@ -699,51 +673,51 @@ hipError_t launch_fwd_prep(int dtype, const void* w, void* wt, int K, int C, int
     return hipGetLastError();
 }
 
+namespace {
+
+// GEMM (and, when the reduction may be split, the partial-tile reduction) of
+// one element type, mode and tile shape.
+template <typename T, int MODE, int TI>
+hipError_t launch_shape(const DataParams& p, int nb, hipStream_t stream)
+{
+    if (p.stride_h == 1 && p.stride_w == 1) bwd_data_kernel<T, MODE, true, TI><<<nb, NT, 0, stream>>>(p);
+    else bwd_data_kernel<T, MODE, false, TI><<<nb, NT, 0, stream>>>(p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // in gather mode the split is only known on the device
+    if (MODE == MODE_GATHER || p.split > 1) {
+        splitk_data_reduce_kernel<T, MODE, TI><<<p.nslots, 256, 0, stream>>>(p);
+        e = hipGetLastError();
+    }
+    return e;
+}
+
+template <typename T, int MODE>
+hipError_t launch_mode(const DataParams& p, int nb, hipStream_t stream)
+{
+    if (p.tile == 0) return launch_shape<T, MODE, 0>(p, nb, stream);
+    if (p.tile == 1) return launch_shape<T, MODE, 1>(p, nb, stream);
+    return launch_shape<T, MODE, 2>(p, nb, stream);
+}
+
+template <typename T>
+hipError_t launch_type(int mode, const DataParams& p, int nb, hipStream_t stream)
+{
+    if (mode == MODE_DENSE) return launch_mode<T, MODE_DENSE>(p, nb, stream);
+    if (mode == MODE_SELECT) return launch_mode<T, MODE_SELECT>(p, nb, stream);
+    if (mode == MODE_FWD) return launch_mode<T, MODE_FWD>(p, nb, stream);
+    return launch_mode<T, MODE_GATHER>(p, nb, stream);
+}
+
+}  // namespace
+
 hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream)
 {
     // enough workgroups for every tile unsplit, or for nslots split items
     const int nb = max(p.ptiles * p.ctiles, p.nslots);
     if (nb <= 0) return hipSuccess;
-    const bool unit = p.stride_h == 1 && p.stride_w == 1;
-#define CBW_LAUNCH(T, M)                                                          \
-    do {                                                                          \
-        if (unit) bwd_data_kernel<T, M, true><<<nb, NT, 0, stream>>>(p);          \
-        else bwd_data_kernel<T, M, false><<<nb, NT, 0, stream>>>(p);              \
-    } while (0)
-    if (dtype == 1) {
-        if (mode == MODE_DENSE) CBW_LAUNCH(uint16_t, MODE_DENSE);
-        else if (mode == MODE_SELECT) CBW_LAUNCH(uint16_t, MODE_SELECT);
-        else if (mode == MODE_FWD) CBW_LAUNCH(uint16_t, MODE_FWD);
-        else CBW_LAUNCH(uint16_t, MODE_GATHER);
-    } else {
-        if (mode == MODE_DENSE) CBW_LAUNCH(float, MODE_DENSE);
-        else if (mode == MODE_SELECT) CBW_LAUNCH(float, MODE_SELECT);
-        else if (mode == MODE_FWD) CBW_LAUNCH(float, MODE_FWD);
-        else CBW_LAUNCH(float, MODE_GATHER);
-    }
-#undef CBW_LAUNCH
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    // The reduction runs whenever a split can occur: in gather mode the
-    // split is only known on the device.
-    if (mode == MODE_GATHER || p.split > 1) {
-        const int rb = p.nslots;
-#define CBW_REDUCE(T, M) splitk_data_reduce_kernel<T, M><<<rb, 256, 0, stream>>>(p)
-        if (dtype == 1) {
-            if (mode == MODE_DENSE) CBW_REDUCE(uint16_t, MODE_DENSE);
-            else if (mode == MODE_SELECT) CBW_REDUCE(uint16_t, MODE_SELECT);
-            else if (mode == MODE_FWD) CBW_REDUCE(uint16_t, MODE_FWD);
-            else CBW_REDUCE(uint16_t, MODE_GATHER);
-        } else {
-            if (mode == MODE_DENSE) CBW_REDUCE(float, MODE_DENSE);
-            else if (mode == MODE_SELECT) CBW_REDUCE(float, MODE_SELECT);
-            else if (mode == MODE_FWD) CBW_REDUCE(float, MODE_FWD);
-            else CBW_REDUCE(float, MODE_GATHER);
-        }
-#undef CBW_REDUCE
-        e = hipGetLastError();
-    }
-    return e;
+    if (p.tile < 0 || p.tile >= kDataTileCount) return hipErrorInvalidValue;
+    return dtype == 1 ? launch_type<uint16_t>(mode, p, nb, stream) : launch_type<float>(mode, p, nb, stream);
 }
 
 }  // namespace cbw

@@ -30,6 +30,7 @@ struct DataParams {
     float* partial;          // [item][BN][BM] fp32 partial tiles when split
     uint32_t dy_bytes, wt_bytes, dx_bytes;
     uint32_t* out_mask;      // MODE_FWD: footprint bits of the output (nullable)
+    int tile;                // kDataTiles entry the plan chose
     FastDiv div_w, div_h;    // pixel -> (n, h, w)
 };
 
@@ -67,8 +68,8 @@ struct OccParams {
     int npq, K, chunk, BNk, ktiles, nchunks, dtype;
 };
 
-int data_tile_channels();
-int data_tile_pixels();
+int data_tile_channels(int tile);
+int data_tile_pixels(int tile);
 int weight_tile_channels();
 int weight_tile_k();
 int weight_chunk(int dtype);

@@ -47,16 +47,34 @@ int validate_desc(const cbw_conv_desc* d)
     return CBW_OK;
 }
 
+int data_tile_index(int C)
+{
+    int best = 0, best_waste = -1;
+    for (int t = 0; t < kDataTileCount; ++t) {
+        const int bm = kDataTiles[t].bm;
+        const int waste = (C + bm - 1) / bm * bm - C;
+        if (8 * waste <= C) return t;
+        if (best_waste < 0 || waste < best_waste) {
+            best = t;
+            best_waste = waste;
+        }
+    }
+    return best;
+}
+
 int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out)
 {
     int st = validate_desc(d);
     if (st != CBW_OK) return st;
     DataPlan p;
+    p.tile = data_tile_index(d->C);
+    p.bm = kDataTiles[p.tile].bm;
+    p.bn = kDataTiles[p.tile].bn;
     p.npix = (int64_t)d->N * d->H * d->W;
-    p.groups = (d->C + kDataTileC - 1) / kDataTileC;
+    p.groups = (d->C + p.bm - 1) / p.bm;
     p.nblk = (int)((p.npix + kCompactBlock - 1) / kCompactBlock);
     size_t cur = 0;
-    p.ptiles = (int)((p.npix + kDataTileP - 1) / kDataTileP);
+    p.ptiles = (int)((p.npix + p.bn - 1) / p.bn);
     const int bk = 8 * (d->dtype == CBW_BF16 ? 8 : 4);
     p.nsteps = d->R * d->S * ((d->K + bk - 1) / bk);
     p.split = host_data_split(p.ptiles * p.groups, p.nsteps);
@@ -70,7 +88,7 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out)
     // Split partial tiles.  Without skipping the host knows the split; with
     // compaction it is decided on the device, bounded by one partial tile
     // per resident workgroup.
-    const size_t tile_bytes = (size_t)kDataTileP * kDataTileC * 4;
+    const size_t tile_bytes = (size_t)p.bn * p.bm * 4;
     if (masked) p.partial = take(&cur, (size_t)kDataSlots * tile_bytes);
     else if (p.split > 1) p.partial = take(&cur, (size_t)p.ptiles * p.groups * p.split * tile_bytes);
     p.total = cur;

@@ -11,8 +11,6 @@
 namespace cbw {
 
 // Tile constants shared with the kernels (asserted equal at dispatch time).
-constexpr int kDataTileC = CBW_DX_BM;   // channels per data-gradient tile = compaction group width
-constexpr int kDataTileP = CBW_DX_BN;   // pixels per data-gradient tile
 constexpr int kWeightTileC = CBW_DW_BM; // channels c per weight-gradient tile
 constexpr int kWeightTileK = CBW_DW_BN; // output channels k per weight-gradient tile
 constexpr int kCompactBlock = 256;      // pixels per compaction block
@@ -25,7 +23,12 @@ struct Region {
     size_t off = 0, bytes = 0;
 };
 
+// Data-gradient tile for C output channels: the widest whose channel padding
+// stays within C/8, else the least padded (ties to the wider).
+int data_tile_index(int C);
+
 struct DataPlan {
+    int tile = 0, bm = 0, bn = 0;   // kDataTiles entry and its shape
     int64_t npix = 0;
     int groups = 0, nblk = 0;
     int ptiles = 0, nsteps = 0;

@@ -1,25 +1,10 @@
-// Tile shapes shared by the kernels and the host planner.  Each can be
-// overridden at build time (-DCBW_DX_BM=... etc.) for tuning sweeps; the
-// dispatcher refuses to run if kernels and planner disagree.
+// Tile shapes shared by the kernels and the host planner (the dispatcher
+// refuses to run if kernels and planner disagree).  The weight-gradient and
+// occupancy macros can be overridden at build time for tuning sweeps.
 #pragma once
 
-#ifndef CBW_DX_BM
-#define CBW_DX_BM 256   // data gradient: channels per tile = compaction group width
-#endif
-#ifndef CBW_DX_BN
-#define CBW_DX_BN 224   // data gradient: pixels per tile
-#endif
-#ifndef CBW_DX_WM
-#define CBW_DX_WM 4     // waves along channels
-#endif
-#ifndef CBW_DX_WN
-#define CBW_DX_WN 2     // waves along pixels
-#endif
 #ifndef CBW_DX_OCC
 #define CBW_DX_OCC 1    // resident workgroups per CU
-#endif
-#ifndef CBW_DX_PIPE
-#define CBW_DX_PIPE 0   // data gradient: fragments of the next chunk group read during the MFMAs
 #endif
 #ifndef CBW_DW_BM
 #define CBW_DW_BM 256   // weight gradient: channels c per tile
@@ -37,3 +22,14 @@
 #define CBW_DW_OCC 1
 #endif
 #define CBW_NUM_CUS 256
+
+// Data-gradient tiles: output channels x pixels, and the waves along each
+// (8 waves, two per SIMD, every wave a 64 x 112 or 64 x 64 block).  The
+// planner picks one per layer from the output channel count, so narrow
+// layers do not pad their channels to 256; the channel width is also the
+// compaction group width.
+struct DataTile {
+    int bm, bn, wm, wn;
+};
+constexpr int kDataTileCount = 3;
+constexpr DataTile kDataTiles[kDataTileCount] = {{256, 224, 4, 2}, {128, 448, 2, 4}, {64, 512, 1, 8}};

@@ -160,11 +160,14 @@ def test_relu_mask_pack_exact():
             assert np.array_equal(bits.cpu().numpy().view(np.uint32), ref_nz), (dtype, n)
 
 
+@pytest.mark.parametrize("C", [256, 128, 64])
 @pytest.mark.parametrize("kind,d", [("bernoulli", 0.01), ("clustered", 0.2), ("channel_shared", 0.3)])
-def test_compaction_lists_exact(kind, d):
+def test_compaction_lists_exact(kind, d, C):
+    """Live lists per channel group (the group is the tile's channel width:
+    256, 128 or 64 channels) equal the oracle's, and so do the row counts."""
     spec = wl.config4(d, kind, N=2, H=14)[0]
-    spec.C = spec.K = 256
-    _case("compaction %s d=%.2f" % (kind, d))
+    spec.C = spec.K = C
+    _case("compaction %s d=%.2f C=%d" % (kind, d, C))
     t = wl.draw(spec)
     gpu = gpu_backward(spec, t)
     desc = gpu["desc"]
