@@ -277,7 +277,7 @@ int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void*
         op.npq = (int)plan.npq;
         op.K = desc->K;
         op.chunk = weight_chunk_px(desc->dtype);
-        op.BNk = kWeightTileK;
+        op.BNk = plan.bk;
         op.ktiles = plan.ktiles;
         op.nchunks = plan.nchunks;
         op.dtype = desc->dtype;
@@ -299,6 +299,9 @@ int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void*
     p.ctiles = plan.ctiles;
     p.ktiles = plan.ktiles;
     p.nsplit = plan.nsplit;
+    p.bk = plan.bk;
+    p.tpg = plan.tpg;
+    p.tgroups = plan.tgroups;
     p.mode_flags = (int)flags;
     p.div_q = make_fastdiv((uint32_t)desc->Q);
     p.div_p = make_fastdiv((uint32_t)desc->P);
@@ -361,7 +364,7 @@ int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, siz
             if (e != hipSuccess) return hip_status(e);
             for (int i = 0; i < n; ++i) skipped += buf[i];
         }
-        r.blocks_skipped = skipped / ((int64_t)desc->R * desc->S * plan.ctiles);
+        r.blocks_skipped = skipped / ((int64_t)plan.tgroups * plan.ctiles);
     } else {
         return CBW_ERR_INVALID_ARG;
     }
@@ -421,7 +424,7 @@ int cbw_read_occupancy(const cbw_conv_desc* desc, const void* workspace, size_t 
     *nchunks = plan.nchunks;
     *ktiles = plan.ktiles;
     *chunk_pixels = weight_chunk_px(desc->dtype);
-    *ktile_width = kWeightTileK;
+    *ktile_width = plan.bk;
     if (occ) {
         hipStream_t s = static_cast<hipStream_t>(stream);
         hipError_t e = hipMemcpyAsync(occ, at<uint8_t>(const_cast<void*>(workspace), plan.occ),

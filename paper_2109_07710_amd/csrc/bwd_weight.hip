@@ -288,12 +288,30 @@ __device__ __forceinline__ uint2 ds_read_tr16(const void* lds)
 constexpr int TR_BK = 64;              // pixels per step
 constexpr int TR_ROW = BM / 8;         // 16-byte chunks per LDS row (one pixel)
 constexpr int TR_IA = TR_BK * BM * 2 / 1024 / (NT / 64);  // 1 KB copies per wave per step, per operand
-static_assert(BM == 256 && BN == 256, "the natural-layout kernel assumes 256-wide tiles");
+static_assert(BM == 256 && BN == 256, "the natural-layout kernel assumes 256-wide rows");
 
+// Tiling of the natural-layout kernel for BKT output channels per tile
+// (256, 128 or 64): the 8 waves split the 256 channel columns WM ways and the
+// BKT output channels WN ways, so every wave holds 64 output channels and
+// 256/WM channel columns.  The channel columns are tpg filter taps of C
+// channels each when taps are packed (C in {32, 64, 128}), else 256 channels
+// of one tap.  dY rows keep the 512-byte LDS layout; chunks past BKT are
+// copied as out-of-range zeros and never read.
+template <int BKT>
+struct WTile {
+    static constexpr int WN = BKT / 64, WM = (NT / 64) / WN;
+    static constexpr int TM = BM / WM, TN = BKT / WN;
+    static constexpr int FM = TM / 16, FN = TN / 16;
+    static_assert(WM * WN * 64 == NT && TN == 64, "64 output channels per wave");
+};
+
+template <int BKT>
 __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
 {
     constexpr uint32_t ESZ = 2;
     constexpr int NW = NT / 64;
+    constexpr int WN = WTile<BKT>::WN;
+    constexpr int TM = WTile<BKT>::TM, TN = WTile<BKT>::TN, FM = WTile<BKT>::FM, FN = WTile<BKT>::FN;
     __shared__ uint4 As[2][TR_BK * TR_ROW];
     __shared__ uint4 Bs[2][TR_BK * TR_ROW];
 
@@ -303,16 +321,16 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
 
     const int RS = p.R * p.S;
-    const int tiles = RS * p.ctiles * p.ktiles;
+    const int tiles = p.tgroups * p.ctiles * p.ktiles;
     const int t = xcd_remap(blockIdx.x, gridDim.x);
     const int z = t / tiles;
     int rem = t - z * tiles;
     const int kt = rem % p.ktiles;
     rem /= p.ktiles;
     const int ct = rem % p.ctiles;
-    const int tap = rem / p.ctiles;
-    const int r = tap / p.S, s = tap - r * p.S;
-    const int c0 = ct * BM, k0 = kt * BN;
+    const int tg = rem / p.ctiles;          // tap group: taps tg*tpg .. tg*tpg + tpg - 1
+    const int cg = BM / p.tpg;              // channel columns per packed tap
+    const int c0 = ct * BM, k0 = kt * BKT;
 
     if (blockIdx.x == 0 && tid == 0) p.header[0] = p.mode_flags;
 
@@ -324,9 +342,11 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
 
     // Copy assignment: instruction j of a wave fills LDS rows 2g, 2g+1 with
     // g = wave + NW*j; lane l serves row 2g + l/32 at physical chunk l%32,
-    // i.e. logical chunk (l%32) ^ trswz(row): channels 8*lc .. 8*lc+7.
+    // i.e. logical chunk (l%32) ^ trswz(row): columns 8*lc .. 8*lc+7, which
+    // are channels of one tap (cg is a multiple of 8).
     int rowj[TR_IA];
-    uint32_t xch[TR_IA], dych[TR_IA];   // channel byte offset, kOOB for channels past the end
+    uint32_t xch[TR_IA], dych[TR_IA];   // channel byte offset, kOOB for columns past C, R*S or BKT
+    int xr[TR_IA], xs[TR_IA];           // filter tap of the lane's X columns
     int xn[TR_IA], xp[TR_IA], xq[TR_IA];   // pixel coordinates of the row at the next chunk to load
     int dpix[TR_IA];
 #pragma unroll
@@ -334,8 +354,12 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
         const int row = 2 * (wave + NW * j) + (lane >> 5);
         const int lc = (lane & 31) ^ trswz(row);
         rowj[j] = row;
-        xch[j] = (c0 + 8 * lc < p.C) ? (uint32_t)(c0 + 8 * lc) * ESZ : kOOB;
-        dych[j] = (k0 + 8 * lc < p.K) ? (uint32_t)(k0 + 8 * lc) * ESZ : kOOB;
+        const int tl = (8 * lc) / cg, cc = (8 * lc) - tl * cg;
+        const int tap = tg * p.tpg + tl;
+        xr[j] = tap / p.S;
+        xs[j] = tap - xr[j] * p.S;
+        xch[j] = (tap < RS && c0 + cc < p.C) ? (uint32_t)(c0 + cc) * ESZ : kOOB;
+        dych[j] = (8 * lc < BKT && k0 + 8 * lc < p.K) ? (uint32_t)(k0 + 8 * lc) * ESZ : kOOB;
     }
     auto set_chunk = [&](int chunk) {
 #pragma unroll
@@ -353,9 +377,9 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
     auto load = [&](int buf) {
 #pragma unroll
         for (int j = 0; j < TR_IA; ++j) {
-            const int h = xp[j] * p.stride_h - p.pad_h + r;
-            const int w = xq[j] * p.stride_w - p.pad_w + s;
-            const bool ok = xn[j] < p.N && h >= 0 && h < p.H && w >= 0 && w < p.W;
+            const int h = xp[j] * p.stride_h - p.pad_h + xr[j];
+            const int w = xq[j] * p.stride_w - p.pad_w + xs[j];
+            const bool ok = xn[j] < p.N && h >= 0 && h < p.H && w >= 0 && w < p.W && xch[j] != kOOB;
             const uint32_t xo = ok ? (uint32_t)(((xn[j] * p.H + h) * p.W + w) * p.C) * ESZ + xch[j] : kOOB;
             buf_load16_lds(rs_x, xo, lds_addr(&As[buf][(wave_u + NW * j) * 2 * TR_ROW]));
             const uint32_t yo = dpix[j] < p.npq ? (uint32_t)(dpix[j] * p.K) * ESZ + dych[j] : kOOB;
@@ -364,8 +388,8 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
     };
 
     // Per-lane transpose-read addresses (bytes within a buffer): for fragment
-    // base channel cb and k-step kc, lane (kg = lane/16, q = lane%4,
-    // m = (lane%16)/4) reads row kc*32 + 8*kg + m (+4), channels cb+4q..+3.
+    // base column cb and k-step kc, lane (kg = lane/16, q = lane%4,
+    // m = (lane%16)/4) reads row kc*32 + 8*kg + m (+4), columns cb+4q..+3.
     const int kg = lane >> 4, q4 = lane & 3, m4 = (lane >> 2) & 3;
     auto tr_addr = [&](int row, int cb) {
         const int col = cb + 4 * q4;
@@ -450,8 +474,9 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
 
     if (tid == 0) p.skip_slots[blockIdx.x] = skipped;
 
-    // Buffer stores over this split's [K][RS][C] region: lanes past K or C
-    // get offset kOOB and their stores are dropped (no branches).
+    // Buffer stores over this split's [K][RS][C] region: lanes past K, C or
+    // the last tap get offset kOOB and their stores are dropped (no branches).
+    // A lane's 4 columns are channels of one tap (cg is a multiple of 16).
     const uint32_t split_bytes = (uint32_t)p.K * RS * p.C * 4u;
     const __amdgpu_buffer_rsrc_t rs_out = make_rsrc(p.out + (int64_t)z * p.K * RS * p.C, split_bytes);
 #pragma unroll
@@ -459,8 +484,10 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
         const int k = k0 + wn * TN + j * 16 + (lane & 15);
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
-            const int c = c0 + wm * TM + i * 16 + 4 * (lane >> 4);
-            const uint32_t off = (k < p.K && c < p.C) ? (uint32_t)((k * RS + tap) * p.C + c) * 4u : kOOB;
+            const int col = wm * TM + i * 16 + 4 * (lane >> 4);
+            const int tl = col / cg, cc = col - tl * cg;
+            const int tap = tg * p.tpg + tl, c = c0 + cc;
+            const uint32_t off = (k < p.K && c < p.C && tap < RS) ? (uint32_t)((k * RS + tap) * p.C + c) * 4u : kOOB;
             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[i][j]), rs_out, off, 0, 0);
         }
     }
@@ -474,8 +501,12 @@ int weight_chunk(int dtype) { return CH * (dtype == 1 ? 8 : 4); }
 
 hipError_t launch_bwd_weight(int dtype, const WeightParams& p, hipStream_t stream)
 {
-    const int nb = p.R * p.S * p.ctiles * p.ktiles * p.nsplit;
-    if (dtype == 1) bwd_weight_tr_kernel<<<nb, NT, 0, stream>>>(p);
+    const int nb = p.tgroups * p.ctiles * p.ktiles * p.nsplit;
+    if (dtype == 1) {
+        if (p.bk == 64) bwd_weight_tr_kernel<64><<<nb, NT, 0, stream>>>(p);
+        else if (p.bk == 128) bwd_weight_tr_kernel<128><<<nb, NT, 0, stream>>>(p);
+        else bwd_weight_tr_kernel<256><<<nb, NT, 0, stream>>>(p);
+    }
     else bwd_weight_kernel<float><<<nb, NT, 0, stream>>>(p);
     return hipGetLastError();
 }

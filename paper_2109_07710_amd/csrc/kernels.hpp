@@ -56,6 +56,8 @@ struct WeightParams {
     int nchunks;             // ceil(npq / chunk)
     int chunks_per_split;
     int ctiles, ktiles, nsplit;
+    int bk;                  // output channels per tile (64, 128, 256)
+    int tpg, tgroups;        // filter taps per 256-column channel tile, and tap groups
     int mode_flags;
     uint32_t x_bytes, dy_bytes;
     FastDiv div_q, div_p;    // pixel -> (n, p, q)

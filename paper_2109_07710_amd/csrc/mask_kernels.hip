@@ -154,20 +154,46 @@ __global__ __launch_bounds__(256) void occupancy_kernel(OccParams p)
         p.occ[(int64_t)chunk * p.ktiles + i] = (uint8_t)(flags[i] != 0);
 }
 
-// dW = sum over splits of the partials, in split order.  part is
-// [nsplit][K][RS][C]; dW is written in KRSC or KCRS.
-__global__ void splitk_reduce_kernel(const float* __restrict__ part, float* __restrict__ dw, int nsplit,
-                                     int K, int RS, int C, int krsc)
+// dW = sum over splits of the partials in a fixed order.  part is
+// [nsplit][K][RS][C]; dW is written in KRSC or KCRS.  A block covers 256/G
+// float4 outputs with G threads each: thread g sums the consecutive splits
+// [g*nsplit/G, (g+1)*nsplit/G) in order, then the G group sums are added in
+// group order.  G = 1 when there are enough outputs to fill the machine; a
+// larger G keeps small outputs with many splits from running one long
+// serial sum per thread.  The order depends only on (nsplit, G), so results
+// are reproducible.
+template <int G>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, float* __restrict__ dw,
+                                                           int nsplit, int K, int RS, int C, int krsc)
 {
+    constexpr int OPB = 256 / G;   // float4 outputs per block
+    __shared__ float4 red[G > 1 ? G : 1][OPB];
     const int64_t total = (int64_t)K * RS * C;
-    const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i4 * 4 >= total) return;
+    const int ol = threadIdx.x % OPB, g = threadIdx.x / OPB;
+    const int64_t i4 = (int64_t)blockIdx.x * OPB + ol;
     const float4* p4 = reinterpret_cast<const float4*>(part);
-    float4 s = p4[i4];
-    for (int z = 1; z < nsplit; ++z) {
-        const float4 v = p4[(int64_t)z * (total / 4) + i4];
-        s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    const int z0 = (int)((int64_t)g * nsplit / G), z1 = (int)((int64_t)(g + 1) * nsplit / G);
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (i4 * 4 < total) {
+        for (int z = z0; z < z1; ++z) {
+            const float4 v = p4[(int64_t)z * (total / 4) + i4];
+            if (z == z0) s = v;
+            else { s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w; }
+        }
     }
+    if (G > 1) {
+        red[g][ol] = s;
+        __syncthreads();
+        if (g != 0) return;
+        for (int gg = 1; gg < G; ++gg) {
+            const float4 v = red[gg][ol];
+            // groups with no splits (nsplit < G) hold zeros and add nothing
+            if ((int64_t)(gg + 1) * nsplit / G > (int64_t)gg * nsplit / G) {
+                s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+            }
+        }
+    }
+    if (i4 * 4 >= total) return;
     if (krsc) {
         reinterpret_cast<float4*>(dw)[i4] = s;
     } else {
@@ -220,7 +246,12 @@ hipError_t launch_splitk_reduce(const float* part, float* dw, int nsplit, int K,
                                 hipStream_t stream)
 {
     const int64_t n4 = (int64_t)K * RS * C / 4;
-    splitk_reduce_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, stream>>>(part, dw, nsplit, K, RS, C, krsc);
+    // one thread per output while that gives at least two blocks per CU,
+    // else 16 threads per output (each summing a sixteenth of the splits)
+    if (n4 >= 2 * 256 * 256 || nsplit < 32)
+        splitk_reduce_kernel<1><<<(unsigned)((n4 + 255) / 256), 256, 0, stream>>>(part, dw, nsplit, K, RS, C, krsc);
+    else
+        splitk_reduce_kernel<16><<<(unsigned)((n4 + 15) / 16), 256, 0, stream>>>(part, dw, nsplit, K, RS, C, krsc);
     return hipGetLastError();
 }
 

@@ -113,6 +113,23 @@ int fwd_as_data_desc(const cbw_conv_desc* d, cbw_conv_desc* out)
     return CBW_OK;
 }
 
+int weight_tile_k_for(const cbw_conv_desc* d)
+{
+    if (d->dtype != CBW_BF16) return kWeightTileK;   // the fp32 kernel keeps 256 x 256 tiles
+    if (d->K <= 64) return 64;
+    if (d->K <= 128) return 128;
+    return kWeightTileK;
+}
+
+int weight_taps_per_group(const cbw_conv_desc* d)
+{
+    const int rs = d->R * d->S;
+    if (d->dtype != CBW_BF16 || rs == 1) return 1;
+    if (d->C != 32 && d->C != 64 && d->C != 128) return 1;
+    const int t = kWeightTileC / d->C;
+    return t < rs ? t : rs;
+}
+
 int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
 {
     int st = validate_desc(d);
@@ -121,9 +138,12 @@ int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
     p.npq = (int64_t)d->N * d->P * d->Q;
     const int chunk = weight_chunk_px(d->dtype);
     p.nchunks = (int)((p.npq + chunk - 1) / chunk);
-    p.ctiles = (d->C + kWeightTileC - 1) / kWeightTileC;
-    p.ktiles = (d->K + kWeightTileK - 1) / kWeightTileK;
-    const int tiles = d->R * d->S * p.ctiles * p.ktiles;
+    p.bk = weight_tile_k_for(d);
+    p.tpg = weight_taps_per_group(d);
+    p.tgroups = (d->R * d->S + p.tpg - 1) / p.tpg;
+    p.ctiles = p.tpg > 1 ? 1 : (d->C + kWeightTileC - 1) / kWeightTileC;
+    p.ktiles = (d->K + p.bk - 1) / p.bk;
+    const int tiles = p.tgroups * p.ctiles * p.ktiles;
     // as many splits as fit in one round of resident workgroups
     int nsplit = kWeightSlots / tiles;
     int max_split = p.nchunks / 4;  // at least four chunks per workgroup
