@@ -308,7 +308,7 @@ def layer_timing(cb, torch, spec, steps, warmup):
     f = spec.dense_flops()
     nflops = f * (2 if spec.need_dx else 1)
     rec["dense_equiv_tflops"] = round(nflops / (ms_s * 1e-3) / 1e12, 2)
-    useful = 2 * int(torch.count_nonzero(dy).item()) * spec.C * spec.R * spec.S
+    useful = 2 * int(torch.count_nonzero(dy).item()) * spec.extra.get("true_c", spec.C) * spec.R * spec.S
     if spec.need_dx:
         useful += (2 * int(torch.count_nonzero(x > 0).item()) * spec.K * spec.R * spec.S if spec.masked else f)
     rec["useful_tflops"] = round(useful / (ms_s * 1e-3) / 1e12, 2)

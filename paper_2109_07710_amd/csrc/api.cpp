@@ -302,6 +302,7 @@ int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void*
     p.bk = plan.bk;
     p.tpg = plan.tpg;
     p.tgroups = plan.tgroups;
+    p.cg = plan.cg;
     p.mode_flags = (int)flags;
     p.div_q = make_fastdiv((uint32_t)desc->Q);
     p.div_p = make_fastdiv((uint32_t)desc->P);

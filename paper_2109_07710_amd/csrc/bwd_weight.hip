@@ -294,8 +294,8 @@ static_assert(BM == 256 && BN == 256, "the natural-layout kernel assumes 256-wid
 // (256, 128 or 64): the 8 waves split the 256 channel columns WM ways and the
 // BKT output channels WN ways, so every wave holds 64 output channels and
 // 256/WM channel columns.  The channel columns are tpg filter taps of C
-// channels each when taps are packed (C in {32, 64, 128}), else 256 channels
-// of one tap.  dY rows keep the 512-byte LDS layout; chunks past BKT are
+// channels each when taps are packed (C <= 128; columns past tpg*C are
+// empty), else 256 channels of one tap.  dY rows keep the 512-byte LDS layout; chunks past BKT are
 // copied as out-of-range zeros and never read.
 template <int BKT>
 struct WTile {
@@ -329,7 +329,7 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
     rem /= p.ktiles;
     const int ct = rem % p.ctiles;
     const int tg = rem / p.ctiles;          // tap group: taps tg*tpg .. tg*tpg + tpg - 1
-    const int cg = BM / p.tpg;              // channel columns per packed tap
+    const int cg = p.cg;                    // channel columns per packed tap (a multiple of 8)
     const int c0 = ct * BM, k0 = kt * BKT;
 
     if (blockIdx.x == 0 && tid == 0) p.header[0] = p.mode_flags;
@@ -358,7 +358,7 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
         const int tap = tg * p.tpg + tl;
         xr[j] = tap / p.S;
         xs[j] = tap - xr[j] * p.S;
-        xch[j] = (tap < RS && c0 + cc < p.C) ? (uint32_t)(c0 + cc) * ESZ : kOOB;
+        xch[j] = (tl < p.tpg && tap < RS && c0 + cc < p.C) ? (uint32_t)(c0 + cc) * ESZ : kOOB;
         dych[j] = (8 * lc < BKT && k0 + 8 * lc < p.K) ? (uint32_t)(k0 + 8 * lc) * ESZ : kOOB;
     }
     auto set_chunk = [&](int chunk) {
@@ -487,7 +487,8 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
             const int col = wm * TM + i * 16 + 4 * (lane >> 4);
             const int tl = col / cg, cc = col - tl * cg;
             const int tap = tg * p.tpg + tl, c = c0 + cc;
-            const uint32_t off = (k < p.K && c < p.C && tap < RS) ? (uint32_t)((k * RS + tap) * p.C + c) * 4u : kOOB;
+            const bool ok = k < p.K && c < p.C && tl < p.tpg && tap < RS;
+            const uint32_t off = ok ? (uint32_t)((k * RS + tap) * p.C + c) * 4u : kOOB;
             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[i][j]), rs_out, off, 0, 0);
         }
     }

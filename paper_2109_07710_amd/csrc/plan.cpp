@@ -124,8 +124,7 @@ int weight_tile_k_for(const cbw_conv_desc* d)
 int weight_taps_per_group(const cbw_conv_desc* d)
 {
     const int rs = d->R * d->S;
-    if (d->dtype != CBW_BF16 || rs == 1) return 1;
-    if (d->C != 32 && d->C != 64 && d->C != 128) return 1;
+    if (d->dtype != CBW_BF16 || rs == 1 || 2 * d->C > kWeightTileC) return 1;
     const int t = kWeightTileC / d->C;
     return t < rs ? t : rs;
 }
@@ -140,6 +139,7 @@ int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
     p.nchunks = (int)((p.npq + chunk - 1) / chunk);
     p.bk = weight_tile_k_for(d);
     p.tpg = weight_taps_per_group(d);
+    p.cg = p.tpg > 1 ? d->C : kWeightTileC;
     p.tgroups = (d->R * d->S + p.tpg - 1) / p.tpg;
     p.ctiles = p.tpg > 1 ? 1 : (d->C + kWeightTileC - 1) / kWeightTileC;
     p.ktiles = (d->K + p.bk - 1) / p.bk;

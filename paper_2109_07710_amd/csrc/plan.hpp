@@ -51,14 +51,16 @@ inline int host_data_split(int T, int nsteps)
 }
 
 // Weight-gradient tiling (bf16): output channels per tile (64, 128 or 256,
-// from K) and filter taps packed side by side in one 256-column channel tile
-// when C divides 256 (C in {32, 64, 128}), so narrow layers fill the tile.
+// from K) and, when C <= 128, floor(256/C) filter taps (at most R*S) packed
+// side by side in one 256-column channel tile, C columns each, so narrow
+// layers fill the tile.
 int weight_tile_k_for(const cbw_conv_desc* d);
 int weight_taps_per_group(const cbw_conv_desc* d);
 
 struct WeightPlan {
     int64_t npq = 0;
     int bk = 0, tpg = 1, tgroups = 0;   // output-channel tile width, taps per group, tap groups
+    int cg = 0;                         // channel columns per packed tap (C, or 256 without packing)
     int nchunks = 0, ctiles = 0, ktiles = 0, nsplit = 0, chunks_per_split = 0, grid = 0;
     bool direct = false;  // partial of the single split is dW itself
     Region header, occ, skip_slots, partials;

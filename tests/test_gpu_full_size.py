@@ -127,9 +127,17 @@ def test_full_spatial_config5_conv1_2():
     _check_full(wl.config5(N=4)[1], flags_pairs=False)
 
 
-def test_full_config5_first_layer_unsupported_channels():
-    """conv1_1 reads the 3-channel image: C = 3 is not a multiple of the
-    16-byte vector, which the library reports instead of computing."""
-    spec = wl.config5()[0]
-    d = cb.ConvDesc.make(spec.N, spec.C, spec.H, spec.W, spec.K, spec.R, spec.S, spec.stride, spec.pad)
-    assert cb.cbw_validate_desc(d) == cb.CBW_ERR_UNSUPPORTED
+def test_full_config5_first_layer_padded_image():
+    """conv1_1 reads the 3-channel image.  C = 3 is not a multiple of the
+    16-byte vector, which the library reports instead of computing; the
+    workload stores the image with its channels zero-padded to 8, and the
+    weight gradient of the padding must come out exactly zero.  Full 224 x 224
+    size with 4 of the 32 images."""
+    spec = wl.config5(N=4)[0]
+    d3 = cb.ConvDesc.make(spec.N, 3, spec.H, spec.W, spec.K, spec.R, spec.S, spec.stride, spec.pad)
+    assert cb.cbw_validate_desc(d3) == cb.CBW_ERR_UNSUPPORTED
+    assert spec.C == 8 and spec.extra["true_c"] == 3 and not spec.need_dx
+    _check_full(spec, flags_pairs=False)
+    t = wl.draw(spec)
+    gpu = gpu_backward(spec, t, dy_mask=True)
+    assert not gpu["dw"][..., 3:].any().item(), "weight gradient of the zero channels"

@@ -103,6 +103,18 @@ def test_strides_pads_shapes(R, S, st, pad, C, K, dt):
     _run_and_check(spec)
 
 
+@pytest.mark.parametrize("C,K,R,S", [(8, 64, 3, 3), (24, 72, 3, 3), (96, 136, 3, 3), (16, 200, 5, 5),
+                                     (128, 64, 3, 3), (40, 128, 3, 2), (64, 64, 1, 1)])
+def test_narrow_channel_tilings(C, K, R, S):
+    """Layer widths that select the narrow tiles: channel tiles of 64 or 128,
+    output-channel tiles of 64 or 128 in the weight gradient, and filter taps
+    packed into one channel tile (C <= 128, with columns past the packed taps
+    left empty, e.g. C = 96 or 40)."""
+    spec = wl.LayerSpec("narrow", 9, 1, N=2, C=C, H=13, W=11, K=K, R=R, S=S, stride=1, pad=R // 2,
+                        dtype="bf16", x_kind="shifted_gauss", x_param=0.1, dy_kind="bernoulli", dy_param=0.5)
+    _run_and_check(spec)
+
+
 def test_kcrs_filter_layout():
     spec = wl.config2(N=1, H=10)[0]
     _run_and_check(spec, w_layout="kcrs")

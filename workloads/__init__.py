@@ -88,8 +88,10 @@ class LayerSpec:
         return (self.W + 2 * self.pad - self.S) // self.stride + 1
 
     def dense_flops(self):
-        """Conventional FLOP count of one gradient GEMM, 2*N*K*P*Q*C*R*S."""
-        return 2 * self.N * self.K * self.P * self.Q * self.C * self.R * self.S
+        """Conventional FLOP count of one gradient GEMM, 2*N*K*P*Q*C*R*S, with
+        the layer's true channel count when its input is stored padded."""
+        c = self.extra.get("true_c", self.C)
+        return 2 * self.N * self.K * self.P * self.Q * c * self.R * self.S
 
 
 def _rng(cfg, layer, tensor):
@@ -162,6 +164,9 @@ def draw(spec: LayerSpec, want=("x", "w", "dy")):
     """Draw the layer's tensors.  Returns a dict of CPU torch tensors:
     x [N,H,W,C], w [K,R,S,C], dy [N,P,Q,K] in spec.dtype."""
     n, c, h, w_, k = spec.N, spec.C, spec.H, spec.W, spec.K
+    # an input stored with zero-padded channels (the 3-channel image as 8
+    # channels): the tensors are drawn at the true width and padded after
+    c_store, c = c, spec.extra.get("true_c", c)
     out = {}
     cid, lid = spec.config_id, spec.layer_id
     if "x" in want:
@@ -177,12 +182,16 @@ def draw(spec: LayerSpec, want=("x", "w", "dy")):
             x *= fp
         else:
             raise ValueError(spec.x_kind)
+        if c_store != c:
+            x = np.concatenate([x, np.zeros((n, h, w_, c_store - c), np.float32)], axis=3)
         out["x"] = _to_torch(x, spec.dtype)
     if "w" in want:
         rng = _rng(cid, lid, 1)
         std = sqrt(2.0 / (c * spec.R * spec.S))
         wt = rng.standard_normal((k, spec.R, spec.S, c), dtype=np.float32)
         wt *= np.float32(std)
+        if c_store != c:
+            wt = np.concatenate([wt, np.zeros((k, spec.R, spec.S, c_store - c), np.float32)], axis=3)
         out["w"] = _to_torch(wt, spec.dtype)
     if "dy" in want:
         p, q = spec.P, spec.Q
@@ -275,12 +284,19 @@ def config5(N=32, scale=1):
         hw_s = max(2, hw // scale)
         after_pool = l in (3, 5, 8, 11)
         d_in = vgg_density(l - 1) if l > 1 else 1.0
+        extra = {"maxpool_route": pool}
+        if c % 8:
+            # the image: stored with its channels zero-padded to a multiple of 8
+            # (the 16-byte vector of 8 bf16), which leaves the weight gradient of
+            # the real channels unchanged and gives exact zeros for the padding
+            extra["true_c"] = c
+            c = (c + 7) // 8 * 8
         spec = LayerSpec(f"vgg16_{name}", 5, l, N=N, C=c, H=hw_s, W=hw_s, K=k, R=3, S=3,
                          masked=(l > 1 and not after_pool), need_dx=(l > 1),
                          x_kind="shifted_gauss",
                          x_param=threshold_for_density(d_in) if l > 1 else -10.0,
                          dy_kind="bernoulli", dy_param=vgg_density(l),
-                         extra={"maxpool_route": pool})
+                         extra=extra)
         specs.append(spec)
     return specs
 
