@@ -186,8 +186,8 @@ def main():
     achieved = dom_flops / (kern[dom] * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_for(dom),
-                "kernel": {"dx_gemm": "bwd_data_kernel<bf16, gather>",
-                           "dw_gemm": "bwd_weight_kernel<bf16>"}[dom],
+                "kernel": {"dx_gemm": "bwd_data_kernel<unsigned short, 2, true, 0> (bf16, gather, 256x224 tile)",
+                           "dw_gemm": "bwd_weight_tr_kernel<256> (bf16, 256-wide output-channel tile)"}[dom],
                 "kernel_ms": round(kern[dom], 4), "flops_per_launch": dom_flops}
 
     # The forward convolution with the ReLU and the footprint fused (the

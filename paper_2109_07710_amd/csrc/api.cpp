@@ -16,9 +16,12 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 // 2 = forward).
 thread_local hipEvent_t g_prof[3][2] = {{nullptr, nullptr}, {nullptr, nullptr}, {nullptr, nullptr}};
 
-hipError_t prof_mark(int fam, int which, hipStream_t s)
+ProfEvents prof_events(int fam)
 {
-    return g_prof[fam][which] ? hipEventRecord(g_prof[fam][which], s) : hipSuccess;
+    ProfEvents ev;
+    ev.start = g_prof[fam][0];
+    ev.stop = g_prof[fam][1];
+    return ev;
 }
 
 int hip_status(hipError_t e)
@@ -116,9 +119,7 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
                                     desc->w_layout == CBW_KRSC, header, mode, gather ? &cp : nullptr, s);
     if (e != hipSuccess) return hip_status(e);
     if (gather && (e = launch_compact_scatter(cp, s)) != hipSuccess) return hip_status(e);
-    if ((e = prof_mark(0, 0, s)) != hipSuccess) return hip_status(e);
-    if ((e = launch_bwd_data(desc->dtype, mode, p, s)) != hipSuccess) return hip_status(e);
-    return hip_status(prof_mark(0, 1, s));
+    return hip_status(launch_bwd_data(desc->dtype, mode, p, s, prof_events(0)));
 }
 
 int run_fwd(const cbw_conv_desc* desc, const void* X, const void* W, void* Y, uint32_t* y_mask, void* ws,
@@ -155,9 +156,7 @@ int run_fwd(const cbw_conv_desc* desc, const void* X, const void* W, void* Y, ui
                                    desc->w_layout == CBW_KRSC, header, clear ? y_mask : nullptr,
                                    clear ? words : 0, s);
     if (e != hipSuccess) return hip_status(e);
-    if ((e = prof_mark(2, 0, s)) != hipSuccess) return hip_status(e);
-    if ((e = launch_bwd_data(desc->dtype, MODE_FWD, p, s)) != hipSuccess) return hip_status(e);
-    return hip_status(prof_mark(2, 1, s));
+    return hip_status(launch_bwd_data(desc->dtype, MODE_FWD, p, s, prof_events(2)));
 }
 
 }  // namespace
@@ -308,9 +307,7 @@ int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void*
     p.div_p = make_fastdiv((uint32_t)desc->P);
     p.x_bytes = (uint32_t)((int64_t)desc->N * desc->H * desc->W * desc->C * elem_bytes(desc->dtype));
     p.dy_bytes = (uint32_t)(plan.npq * desc->K * elem_bytes(desc->dtype));
-    if ((e = prof_mark(1, 0, s)) != hipSuccess) return hip_status(e);
-    if ((e = launch_bwd_weight(desc->dtype, p, s)) != hipSuccess) return hip_status(e);
-    if ((e = prof_mark(1, 1, s)) != hipSuccess) return hip_status(e);
+    if ((e = launch_bwd_weight(desc->dtype, p, s, prof_events(1))) != hipSuccess) return hip_status(e);
     if (!plan.direct) {
         e = launch_splitk_reduce(p.out, dW, plan.nsplit, desc->K, desc->R * desc->S, desc->C,
                                  desc->w_layout == CBW_KRSC, s);

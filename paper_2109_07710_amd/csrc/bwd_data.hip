@@ -26,6 +26,8 @@
 // consecutive rows spread over all banks.
 #include <type_traits>
 
+#include <hip/hip_ext.h>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "footprint.hpp"
@@ -678,10 +680,12 @@ namespace {
 // GEMM (and, when the reduction may be split, the partial-tile reduction) of
 // one element type, mode and tile shape.
 template <typename T, int MODE, int TI>
-hipError_t launch_shape(const DataParams& p, int nb, hipStream_t stream)
+hipError_t launch_shape(const DataParams& p, int nb, hipStream_t stream, const ProfEvents& ev)
 {
-    if (p.stride_h == 1 && p.stride_w == 1) bwd_data_kernel<T, MODE, true, TI><<<nb, NT, 0, stream>>>(p);
-    else bwd_data_kernel<T, MODE, false, TI><<<nb, NT, 0, stream>>>(p);
+    if (p.stride_h == 1 && p.stride_w == 1)
+        hipExtLaunchKernelGGL(bwd_data_kernel<T, MODE, true, TI>, dim3(nb), dim3(NT), 0, stream, ev.start, ev.stop, 0, p);
+    else
+        hipExtLaunchKernelGGL(bwd_data_kernel<T, MODE, false, TI>, dim3(nb), dim3(NT), 0, stream, ev.start, ev.stop, 0, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     // in gather mode the split is only known on the device
@@ -693,31 +697,32 @@ hipError_t launch_shape(const DataParams& p, int nb, hipStream_t stream)
 }
 
 template <typename T, int MODE>
-hipError_t launch_mode(const DataParams& p, int nb, hipStream_t stream)
+hipError_t launch_mode(const DataParams& p, int nb, hipStream_t stream, const ProfEvents& ev)
 {
-    if (p.tile == 0) return launch_shape<T, MODE, 0>(p, nb, stream);
-    if (p.tile == 1) return launch_shape<T, MODE, 1>(p, nb, stream);
-    return launch_shape<T, MODE, 2>(p, nb, stream);
+    if (p.tile == 0) return launch_shape<T, MODE, 0>(p, nb, stream, ev);
+    if (p.tile == 1) return launch_shape<T, MODE, 1>(p, nb, stream, ev);
+    return launch_shape<T, MODE, 2>(p, nb, stream, ev);
 }
 
 template <typename T>
-hipError_t launch_type(int mode, const DataParams& p, int nb, hipStream_t stream)
+hipError_t launch_type(int mode, const DataParams& p, int nb, hipStream_t stream, const ProfEvents& ev)
 {
-    if (mode == MODE_DENSE) return launch_mode<T, MODE_DENSE>(p, nb, stream);
-    if (mode == MODE_SELECT) return launch_mode<T, MODE_SELECT>(p, nb, stream);
-    if (mode == MODE_FWD) return launch_mode<T, MODE_FWD>(p, nb, stream);
-    return launch_mode<T, MODE_GATHER>(p, nb, stream);
+    if (mode == MODE_DENSE) return launch_mode<T, MODE_DENSE>(p, nb, stream, ev);
+    if (mode == MODE_SELECT) return launch_mode<T, MODE_SELECT>(p, nb, stream, ev);
+    if (mode == MODE_FWD) return launch_mode<T, MODE_FWD>(p, nb, stream, ev);
+    return launch_mode<T, MODE_GATHER>(p, nb, stream, ev);
 }
 
 }  // namespace
 
-hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream)
+hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream, const ProfEvents& ev)
 {
     // enough workgroups for every tile unsplit, or for nslots split items
     const int nb = max(p.ptiles * p.ctiles, p.nslots);
     if (nb <= 0) return hipSuccess;
     if (p.tile < 0 || p.tile >= kDataTileCount) return hipErrorInvalidValue;
-    return dtype == 1 ? launch_type<uint16_t>(mode, p, nb, stream) : launch_type<float>(mode, p, nb, stream);
+    return dtype == 1 ? launch_type<uint16_t>(mode, p, nb, stream, ev)
+                      : launch_type<float>(mode, p, nb, stream, ev);
 }
 
 }  // namespace cbw

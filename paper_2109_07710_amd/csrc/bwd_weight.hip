@@ -18,6 +18,8 @@
 // Split-K: the pixel chunks are divided among nsplit workgroups per output
 // tile; each writes a float32 partial tile, reduced afterwards in a fixed
 // order (deterministic).
+#include <hip/hip_ext.h>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "tiles.hpp"
@@ -500,15 +502,16 @@ int weight_tile_channels() { return BM; }
 int weight_tile_k() { return BN; }
 int weight_chunk(int dtype) { return CH * (dtype == 1 ? 8 : 4); }
 
-hipError_t launch_bwd_weight(int dtype, const WeightParams& p, hipStream_t stream)
+hipError_t launch_bwd_weight(int dtype, const WeightParams& p, hipStream_t stream, const ProfEvents& ev)
 {
     const int nb = p.tgroups * p.ctiles * p.ktiles * p.nsplit;
+    const dim3 grid(nb), block(NT);
     if (dtype == 1) {
-        if (p.bk == 64) bwd_weight_tr_kernel<64><<<nb, NT, 0, stream>>>(p);
-        else if (p.bk == 128) bwd_weight_tr_kernel<128><<<nb, NT, 0, stream>>>(p);
-        else bwd_weight_tr_kernel<256><<<nb, NT, 0, stream>>>(p);
+        if (p.bk == 64) hipExtLaunchKernelGGL(bwd_weight_tr_kernel<64>, grid, block, 0, stream, ev.start, ev.stop, 0, p);
+        else if (p.bk == 128) hipExtLaunchKernelGGL(bwd_weight_tr_kernel<128>, grid, block, 0, stream, ev.start, ev.stop, 0, p);
+        else hipExtLaunchKernelGGL(bwd_weight_tr_kernel<256>, grid, block, 0, stream, ev.start, ev.stop, 0, p);
     }
-    else bwd_weight_kernel<float><<<nb, NT, 0, stream>>>(p);
+    else hipExtLaunchKernelGGL(bwd_weight_kernel<float>, grid, block, 0, stream, ev.start, ev.stop, 0, p);
     return hipGetLastError();
 }
 

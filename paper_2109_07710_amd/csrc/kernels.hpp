@@ -81,7 +81,12 @@ int compact_block_pixels();
 // Filter transform (and, when cp is given, the compaction count) in one launch.
 hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, int RS, int krsc, int* header,
                             int mode, const CompactParams* cp, hipStream_t stream);
-hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream);
+// Optional timing events attached to the dispatch of a GEMM kernel (both
+// may be null): they record the kernel's own begin and end.
+struct ProfEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream, const ProfEvents& ev);
 // Forward preparation: Wf[tap'][k][c] = W[k][tap][c] with tap' the flipped tap
 // (R-1-r, S-1-s), the workspace header stamped, and `zero_words` words of
 // `zero` cleared (footprint words filled by atomic OR), in one launch.
@@ -91,7 +96,7 @@ hipError_t launch_compact_scatter(const CompactParams& p, hipStream_t stream);
 hipError_t launch_relu_mask_pack(int dtype, int64_t count, const void* x, uint32_t* bits, int relu,
                                  hipStream_t stream);
 hipError_t launch_occupancy(const OccParams& p, hipStream_t stream);
-hipError_t launch_bwd_weight(int dtype, const WeightParams& p, hipStream_t stream);
+hipError_t launch_bwd_weight(int dtype, const WeightParams& p, hipStream_t stream, const ProfEvents& ev);
 hipError_t launch_splitk_reduce(const float* part, float* dw, int nsplit, int K, int RS, int C, int krsc,
                                 hipStream_t stream);
 
