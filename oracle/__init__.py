@@ -12,6 +12,8 @@ Contents
 * the ReLU mask bitmap (Sec. III-B, boxed derivative; Sec. IV-B output
   bitmap), the per-channel-group live-pixel lists that stand for the paper's
   non-zero indexing (Sec. IV-B), and the dY block occupancy, in numpy;
+* 2x2 max-pool forward/backward, for the exactness of the pooled-footprint
+  mask at MaxPool -> CONV boundaries;
 * pure layout permutations between NHWC/KRSC storage and the logical order.
 
 Parity pins for every function live in tests/test_oracle_pins.py.
@@ -263,6 +265,38 @@ def relu_mask(x):
     here is the output footprint: live iff the ReLU output is > 0.
     """
     return np.asarray(x) > 0
+
+
+def maxpool2x2(a):
+    """2x2 max-pool, stride 2, over the spatial axes of an [N][C][H][W]
+    tensor with even H and W (the pooling between the VGG-16 stages, the
+    network of the paper's layer-wise results in Sec. VI).  Returns (pooled,
+    arg): arg[n,c,i,j] in 0..3 is the row-major window position of the first
+    maximum, the position max-pool backward routes the gradient to."""
+    a = np.asarray(a, dtype=np.float64)
+    N, C, H, W = a.shape
+    assert H % 2 == 0 and W % 2 == 0
+    pooled = np.empty((N, C, H // 2, W // 2))
+    arg = np.empty((N, C, H // 2, W // 2), np.int64)
+    for i in range(H // 2):
+        for j in range(W // 2):
+            win = np.stack([a[:, :, 2 * i, 2 * j], a[:, :, 2 * i, 2 * j + 1],
+                            a[:, :, 2 * i + 1, 2 * j], a[:, :, 2 * i + 1, 2 * j + 1]], axis=-1)
+            arg[:, :, i, j] = np.argmax(win, axis=-1)   # first maximum
+            pooled[:, :, i, j] = np.max(win, axis=-1)
+    return pooled, arg
+
+
+def maxpool2x2_backward(g, arg):
+    """Max-pool backward: each pooled gradient g[n,c,i,j] goes to window
+    position arg[n,c,i,j] of the 2x2 window, every other position gets 0."""
+    g = np.asarray(g, dtype=np.float64)
+    N, C, h, w = g.shape
+    out = np.zeros((N, C, 2 * h, 2 * w))
+    for pos in range(4):
+        sel = arg == pos
+        out[:, :, pos // 2::2, pos % 2::2] = np.where(sel, g, 0.0)
+    return out
 
 
 def pack_bits(live_linear):

@@ -121,6 +121,12 @@ def test_full_config5_vgg_layers(layer):
     _check_full(wl.config5()[layer - 1])
 
 
+@pytest.mark.parametrize("layer", [3, 11])
+def test_full_config5_pooled_mask(layer):
+    """conv2_1 and conv5_1 at full size with the pooled > 0 mask."""
+    _check_full(wl.config5(pooled_mask=True)[layer - 1])
+
+
 def test_full_spatial_config5_conv1_2():
     """conv1_2 at its full 224 x 224 size (64 -> 64 channels) with 4 of the 32
     images, to keep input generation short."""

@@ -83,6 +83,16 @@ def test_config5_vgg_layers_reduced(layer):
     print(errs)
 
 
+@pytest.mark.parametrize("layer", [3, 5, 8, 11])
+def test_config5_pooled_mask_reduced(layer):
+    """The four layers after a max-pool with their data gradient masked by
+    pooled > 0 (the pooled ReLU output is the conv's X)."""
+    spec = wl.config5(N=2, scale=8, pooled_mask=True)[layer - 1]
+    assert spec.masked and spec.x_kind == "pooled_gauss"
+    errs, _, _ = _run_and_check(spec)
+    print(errs)
+
+
 # ------------------------------------------------------- shapes / strides
 
 def _shape_cases():

@@ -199,6 +199,53 @@ def test_masked_equals_dense_times_mask_with_positive_zeros():
     assert np.array_equal(all_live, dense)
 
 
+def test_maxpool_matches_torch_cpu():
+    """The 2x2 max-pool and its backward against torch's CPU fp64 max_pool2d
+    and its autograd (continuous values, so the maximum is unique)."""
+    rng = np.random.default_rng(23)
+    a = rng.standard_normal((2, 3, 6, 8))
+    pooled, arg = oracle.maxpool2x2(a)
+    ta = torch.from_numpy(a).requires_grad_(True)
+    tp = torch.nn.functional.max_pool2d(ta, 2, 2)
+    assert np.array_equal(pooled, tp.detach().numpy())
+    g = rng.standard_normal(pooled.shape)
+    tp.backward(torch.from_numpy(g))
+    assert np.array_equal(oracle.maxpool2x2_backward(g, arg), ta.grad.numpy())
+
+
+def test_maxpool_ties_route_to_first_position():
+    """A window of equal values (e.g. four ReLU zeros) routes to its first position."""
+    pooled, arg = oracle.maxpool2x2(np.zeros((1, 1, 2, 4)))
+    assert pooled.shape == (1, 1, 1, 2) and np.all(pooled == 0) and np.all(arg == 0)
+    back = oracle.maxpool2x2_backward(np.array([[[[5.0, -2.0]]]]), arg)
+    assert back.tolist() == [[[[5.0, 0.0, -2.0, 0.0], [0.0, 0.0, 0.0, 0.0]]]]
+
+
+def test_pooled_footprint_mask_is_exact():
+    """MaxPool -> CONV boundary (the layers after a pool in Sec. VI, where the
+    paper applies no output sparsity): masking the conv's data gradient by
+    pooled > 0 leaves the gradient that reaches the pre-pool ReLU unchanged,
+    bit for bit.  A pooled value of 0 means every ReLU output of its window
+    is 0, so the ReLU derivative (mask = output > 0) kills whatever max-pool
+    backward routes there."""
+    rng = np.random.default_rng(29)
+    N, C, K, H, W = 2, 4, 3, 4, 6          # pooled size; the pre-pool map is 2H x 2W
+    z = rng.standard_normal((N, C, 2 * H, 2 * W)) - 0.8   # pre-activation: most windows all dead
+    a = oracle.relu(z)
+    x, arg = oracle.maxpool2x2(a)
+    w = _rand(rng, (K, C, 3, 3))
+    dy = _rand(rng, (N, K, H, W), 0.6)
+    dense = oracle.conv_bwd_data(dy, w, (H, W), pad=(1, 1))
+    masked = oracle.conv_bwd_data(dy, w, (H, W), pad=(1, 1), mask=oracle.relu_mask(x))
+    assert np.any((dense != 0) & ~(x > 0)), "the mask must remove something"
+    relu_deriv = oracle.relu_mask(a)
+    g_dense = np.where(relu_deriv, oracle.maxpool2x2_backward(dense, arg), 0.0)
+    g_masked = np.where(relu_deriv, oracle.maxpool2x2_backward(masked, arg), 0.0)
+    assert np.array_equal(g_dense, g_masked)
+    # and the masked gradient is the dense one with the pooled-dead outputs at zero
+    assert np.array_equal(np.where(x > 0, dense, 0.0), masked)
+
+
 def test_relu_mask_reading_at_zero():
     """mask = (ReLU output > 0): exact zeros of either sign are killed."""
     x = np.array([-1.0, -0.0, 0.0, 1e-300, 2.0])

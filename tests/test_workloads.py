@@ -112,6 +112,27 @@ def test_config5_layers():
     assert wl.vgg_density(1) == 0.5 and abs(wl.vgg_density(13) - 0.15) < 1e-12
 
 
+def test_config5_pooled_inputs():
+    """The inputs after a max-pool are pooled ReLU outputs: density
+    1 - (1 - d)^4 of the layer before (i.i.d. footprint), every value the
+    maximum of a 2x2 window; with pooled_mask the four post-pool layers are
+    masked (by pooled > 0), the others unchanged."""
+    specs = wl.config5(N=2, scale=4)
+    pooled = wl.config5(N=2, scale=4, pooled_mask=True)
+    after = {3, 5, 8, 11}
+    assert [s.masked for s in pooled] == [s.masked or s.layer_id in after for s in specs]
+    for s in specs:
+        assert (s.x_kind == "pooled_gauss") == (s.layer_id in after)
+    for l in (3, 11):
+        s = specs[l - 1]
+        x = wl.draw(s, want=("x",))["x"].float().numpy()
+        assert x.shape == (s.N, s.H, s.W, s.C) and np.all(x >= 0)
+        d = 1 - (1 - wl.vgg_density(l - 1)) ** 4
+        assert _within(np.mean(x > 0), d, x.size)
+        assert torch.equal(wl.draw(pooled[l - 1], want=("x",))["x"].view(torch.uint8),
+                           wl.draw(s, want=("x",))["x"].view(torch.uint8))
+
+
 def test_dense_flops_config2():
     s = wl.config2()[0]
     assert s.dense_flops() == 2 * 32 * 256 * 56 * 56 * 256 * 9

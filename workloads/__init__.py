@@ -73,7 +73,7 @@ class LayerSpec:
     dtype: str = "bf16"           # "bf16" or "f32" for X, W, dY (and dX)
     masked: bool = True           # data gradient restricted by X's ReLU footprint
     need_dx: bool = True          # False for a network's first layer
-    x_kind: str = "shifted_gauss"  # how X is drawn, see _draw_x
+    x_kind: str = "shifted_gauss"  # how X is drawn, see draw()
     x_param: float = 0.0
     dy_kind: str = "bernoulli"    # how dY's footprint is drawn
     dy_param: float = 0.5
@@ -175,6 +175,14 @@ def draw(spec: LayerSpec, want=("x", "w", "dy")):
             x = rng.standard_normal((n, h, w_, c), dtype=np.float32)
             x -= np.float32(spec.x_param)
             np.maximum(x, np.float32(0.0), out=x)
+        elif spec.x_kind == "pooled_gauss":
+            # the input of a layer that follows a 2x2 max-pool: the previous
+            # layer's ReLU output, drawn at twice the size, then pooled
+            z = rng.standard_normal((n, 2 * h, 2 * w_, c), dtype=np.float32)
+            z -= np.float32(spec.x_param)
+            np.maximum(z, np.float32(0.0), out=z)
+            x = z.reshape(n, h, 2, w_, 2, c).max(axis=(2, 4))
+            del z
         elif spec.x_kind in ("bernoulli", "clustered", "channel_shared"):
             fp = _footprint(rng, spec.x_kind, n, c, h, w_, spec.x_param)
             x = rng.standard_normal((n, h, w_, c), dtype=np.float32)
@@ -276,8 +284,13 @@ def vgg_density(l):
     return 0.5 - 0.35 * (l - 1) / 12.0
 
 
-def config5(N=32, scale=1):
-    """VGG-16 conv stack; scale > 1 divides every spatial size (test sizes)."""
+def config5(N=32, scale=1, pooled_mask=False):
+    """VGG-16 conv stack; scale > 1 divides every spatial size (test sizes).
+
+    The inputs of the four layers after a max-pool are the pooled ReLU output
+    of the layer before (density 1 - (1 - d)^4 for i.i.d. footprints).  Their
+    data gradient is dense (the paper applies no output sparsity there) unless
+    pooled_mask is set, in which case it is masked by pooled > 0."""
     specs = []
     for i, (name, c, k, hw, pool) in enumerate(VGG16):
         l = i + 1
@@ -292,8 +305,8 @@ def config5(N=32, scale=1):
             extra["true_c"] = c
             c = (c + 7) // 8 * 8
         spec = LayerSpec(f"vgg16_{name}", 5, l, N=N, C=c, H=hw_s, W=hw_s, K=k, R=3, S=3,
-                         masked=(l > 1 and not after_pool), need_dx=(l > 1),
-                         x_kind="shifted_gauss",
+                         masked=(l > 1 and (pooled_mask or not after_pool)), need_dx=(l > 1),
+                         x_kind="pooled_gauss" if after_pool else "shifted_gauss",
                          x_param=threshold_for_density(d_in) if l > 1 else -10.0,
                          dy_kind="bernoulli", dy_param=vgg_density(l),
                          extra=extra)
