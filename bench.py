@@ -280,6 +280,15 @@ def layer_timing(cb, torch, spec, steps, warmup):
                 cb.conv_bwd_data(desc, dy, w, dx, ws_d)
         cb.conv_bwd_weight_sparse(desc, x, dy, dym, dw, ws_w, 0)
 
+    def sparse_x():
+        # as sparse(), with the weight gradient also skipping all-zero X blocks
+        if spec.need_dx:
+            if spec.masked:
+                cb.conv_bwd_data_masked(desc, dy, w, xm, dx, ws_m, 0)
+            else:
+                cb.conv_bwd_data(desc, dy, w, dx, ws_d)
+        cb.conv_bwd_weight_sparse_x(desc, x, dy, xm, dym, dw, ws_w, 0)
+
     def dense():
         if spec.need_dx:
             cb.conv_bwd_data(desc, dy, w, dx, ws_d)
@@ -299,11 +308,15 @@ def layer_timing(cb, torch, spec, steps, warmup):
     # input generation), then timed alternately; the faster of two rounds counts.
     for _ in range(warmup):
         sparse()
+        sparse_x()
         dense()
-    ms_s, ms_d = float("inf"), float("inf")
+    ms_s, ms_x, ms_d = float("inf"), float("inf"), float("inf")
     for _ in range(2):
         ms_s = min(ms_s, tm(sparse))
+        ms_x = min(ms_x, tm(sparse_x))
         ms_d = min(ms_d, tm(dense))
+    sparse_x()
+    st_x = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws_w)
     sparse()
     torch.cuda.synchronize()
     rec = {"layer": spec.name, "N": spec.N, "C": spec.C, "K": spec.K, "H": spec.H, "W": spec.W, "R": spec.R,
@@ -323,6 +336,10 @@ def layer_timing(cb, torch, spec, steps, warmup):
         rec["dx_rows_executed"] = round(st.rows_live / st.rows_total, 4)
     st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws_w)
     rec["dw_blocks_executed"] = round(1.0 - st.blocks_skipped / max(st.blocks_total, 1), 4)
+    # the variant whose weight gradient also skips all-zero X blocks
+    rec["sparse_x_ms"] = round(ms_x, 4)
+    rec["speedup_x_vs_dense"] = round(ms_d / ms_x, 4)
+    rec["dw_blocks_executed_x"] = round(1.0 - st_x.blocks_skipped / max(st_x.blocks_total, 1), 4)
     return rec
 
 

@@ -91,8 +91,8 @@ enum { CBW_OP_BWD_DATA = 0, CBW_OP_BWD_DATA_MASKED = 1, CBW_OP_BWD_WEIGHT = 2, C
 typedef struct {
     int64_t rows_total;      /* GEMM rows (pixel x channel-group) the dense path would compute */
     int64_t rows_live;       /* rows actually computed                                        */
-    int64_t blocks_total;    /* dW (pixel-chunk x k-tile) blocks                               */
-    int64_t blocks_skipped;  /* dW blocks skipped because dY was all zero there                 */
+    int64_t blocks_total;    /* dW GEMM blocks: pixel chunk x k tile x tap group x channel tile */
+    int64_t blocks_skipped;  /* dW blocks skipped (dY, or with the _x variant X, all zero)     */
 } cbw_stats;
 
 /* Human-readable name of a cbw_status value (static storage). */
@@ -167,6 +167,23 @@ int conv_fwd_relu_mask(const cbw_conv_desc* desc, const void* X, const void* W, 
 int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void* dY,
                            const uint32_t* dy_mask, float* dW,
                            void* workspace, size_t workspace_bytes, uint32_t flags, void* stream);
+
+/* Weight gradient that also skips blocks whose X operand is entirely zero:
+ * activation sparsity used as input sparsity in the weight-gradient phase
+ * (Sec. III-A, sources of sparsity; Sec. VI, weight-gradient results).  A
+ * (pixel chunk x filter taps x channel tile) block is skipped when dY is zero
+ * over the chunk's output channels of the tile (as conv_bwd_weight_sparse
+ * does) or when X is zero over the chunk's tap-shifted pixels and the tile's
+ * channels; both skips drop only products that are exactly zero (finite
+ * inputs).  x_mask (nullable, 16-byte aligned): packed X footprint in X's
+ * linear order, cbw_mask_words(desc) words, any superset of X's non-zeros
+ * (cbw_nonzero_mask_pack; for a ReLU output X the cbw_relu_mask_pack bitmap);
+ * when NULL the X occupancy is read from X itself.  Otherwise as
+ * conv_bwd_weight_sparse (same workspace size, deterministic, dW fully
+ * overwritten); CBW_FLAG_NO_SKIP disables both skips. */
+int conv_bwd_weight_sparse_x(const cbw_conv_desc* desc, const void* X, const void* dY,
+                             const uint32_t* x_mask, const uint32_t* dy_mask, float* dW,
+                             void* workspace, size_t workspace_bytes, uint32_t flags, void* stream);
 
 /* Copy the statistics of the last `op` call that used `workspace` to the host
  * (waits for `stream`). */

@@ -299,6 +299,49 @@ def maxpool2x2_backward(g, arg):
     return out
 
 
+def weight_block_liveness(x_live, dy_live, rs, stride, pad, chunk, ktile, ctile, tpg):
+    """Which blocks of the weight-gradient GEMM have a non-zero in both of
+    their operands (input sparsity in the weight-gradient phase: a block whose
+    dY operand or whose X operand is entirely zero contributes only zero
+    products, so it can be skipped; a live block may still have only zero
+    products when the non-zeros of its two operands do not meet).
+
+    x_live [N][C][H][W] and dy_live [N][K][P][Q] are boolean footprints.
+    Output pixels are taken in (n, p, q) order and cut into chunks of
+    `chunk`; output channels into tiles of `ktile`; input channels into
+    tiles of `ctile`; filter taps (r*S + s) into groups of `tpg`.  Block
+    (g, ct, kt, b) is live iff dY is non-zero somewhere in chunk b x k tile
+    kt AND X is non-zero somewhere at the chunk's pixels shifted by one of
+    the group's taps (inside the image) x channel tile ct.
+    Returns bool [groups][ctiles][ktiles][chunks]."""
+    x_live, dy_live = np.asarray(x_live, bool), np.asarray(dy_live, bool)
+    N, C, H, W = x_live.shape
+    _, K, P, Q = dy_live.shape
+    R, S = rs
+    npq = N * P * Q
+    nch = -(-npq // chunk)
+    nkt, nct, ngr = -(-K // ktile), -(-C // ctile), -(-(R * S) // tpg)
+    n_i, p_i, q_i = np.meshgrid(np.arange(N), np.arange(P), np.arange(Q), indexing="ij")
+    n_i, p_i, q_i = n_i.ravel(), p_i.ravel(), q_i.ravel()       # pixel order (n, p, q)
+    blk = np.arange(npq) // chunk
+    dy_pix = dy_live.transpose(0, 2, 3, 1).reshape(npq, K)
+    dy_any = np.zeros((nch, nkt), bool)
+    for kt in range(nkt):
+        np.logical_or.at(dy_any[:, kt], blk, dy_pix[:, kt * ktile:(kt + 1) * ktile].any(axis=1))
+    x_any = np.zeros((ngr, nct, nch), bool)
+    for tap in range(R * S):
+        r, s = divmod(tap, S)
+        h = p_i * stride[0] - pad[0] + r
+        w = q_i * stride[1] - pad[1] + s
+        inside = (h >= 0) & (h < H) & (w >= 0) & (w < W)
+        for ct in range(nct):
+            v = np.zeros(npq, bool)
+            sub = x_live[:, ct * ctile:(ct + 1) * ctile]
+            v[inside] = sub[n_i[inside], :, h[inside], w[inside]].any(axis=1)
+            np.logical_or.at(x_any[tap // tpg, ct], blk, v)
+    return x_any[:, :, None, :] & dy_any.T[None, None, :, :]
+
+
 def pack_bits(live_linear):
     """Bit i of 32-bit word i//32 = live_linear[i] (little-endian bit order),
     trailing bits of the last word 0.  This is the output bitmap of

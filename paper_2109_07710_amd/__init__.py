@@ -27,7 +27,8 @@ CBW_FLAG_NO_SKIP = 1
 
 EXPORTS = ("cbw_status_string", "cbw_validate_desc", "cbw_mask_words", "cbw_dy_mask_words",
            "cbw_workspace_size", "cbw_relu_mask_pack", "cbw_nonzero_mask_pack", "conv_bwd_data",
-           "conv_bwd_data_masked", "conv_fwd_relu_mask", "conv_bwd_weight_sparse", "cbw_read_stats",
+           "conv_bwd_data_masked", "conv_fwd_relu_mask", "conv_bwd_weight_sparse", "conv_bwd_weight_sparse_x",
+           "cbw_read_stats",
            "cbw_read_live_lists",
            "cbw_read_occupancy", "cbw_set_profile_events")
 
@@ -90,6 +91,7 @@ def lib():
     L.conv_bwd_data_masked.argtypes = [dp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
     L.conv_fwd_relu_mask.argtypes = [dp, vp, vp, vp, vp, vp, sz, vp]
     L.conv_bwd_weight_sparse.argtypes = [dp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
+    L.conv_bwd_weight_sparse_x.argtypes = [dp, vp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
     L.cbw_read_stats.argtypes = [dp, ctypes.c_int, vp, sz, ctypes.POINTER(Stats), vp]
     i32p = ctypes.POINTER(ctypes.c_int32)
     L.cbw_read_live_lists.argtypes = [dp, vp, sz, ctypes.c_int, vp, i32p, i32p, vp]
@@ -191,6 +193,12 @@ def conv_bwd_weight_sparse(desc, X, dY, dy_mask, dW, ws, flags=0, stream=None):
     _check(lib().conv_bwd_weight_sparse(ctypes.byref(desc), _ptr(X), _ptr(dY), _ptr(dy_mask), _ptr(dW),
                                         _ptr(ws), _nbytes(ws), flags, _stream(stream)),
            "conv_bwd_weight_sparse")
+
+
+def conv_bwd_weight_sparse_x(desc, X, dY, x_mask, dy_mask, dW, ws, flags=0, stream=None):
+    _check(lib().conv_bwd_weight_sparse_x(ctypes.byref(desc), _ptr(X), _ptr(dY), _ptr(x_mask), _ptr(dy_mask),
+                                          _ptr(dW), _ptr(ws), _nbytes(ws), flags, _stream(stream)),
+           "conv_bwd_weight_sparse_x")
 
 
 def cbw_read_stats(desc, op, ws, stream=None):

@@ -253,14 +253,16 @@ int conv_fwd_relu_mask(const cbw_conv_desc* desc, const void* X, const void* W, 
     return run_fwd(desc, X, W, Y, y_mask, workspace, workspace_bytes, stream);
 }
 
-int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void* dY, const uint32_t* dy_mask,
-                           float* dW, void* workspace, size_t workspace_bytes, uint32_t flags, void* stream)
+// Weight gradient; x_skip also skips blocks whose X operand is all zero.
+static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, const uint32_t* x_mask,
+               const uint32_t* dy_mask, bool x_skip, float* dW, void* workspace, size_t workspace_bytes,
+               uint32_t flags, void* stream)
 {
     WeightPlan plan;
     int st = plan_weight(desc, &plan);
     if (st != CBW_OK) return st;
     if (!X || !dY || !dW) return CBW_ERR_INVALID_ARG;
-    if (!aligned16(X) || !aligned16(dY) || !aligned16(dW) || !aligned16(dy_mask))
+    if (!aligned16(X) || !aligned16(dY) || !aligned16(dW) || !aligned16(dy_mask) || !aligned16(x_mask))
         return CBW_ERR_UNSUPPORTED;
     if ((st = check_ws(workspace, workspace_bytes, plan.total)) != CBW_OK) return st;
     if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;
@@ -280,6 +282,16 @@ int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void*
         op.ktiles = plan.ktiles;
         op.nchunks = plan.nchunks;
         op.dtype = desc->dtype;
+        if (x_skip) {
+            op.x = X;
+            op.xbits = x_mask;
+            op.xocc = at<uint8_t>(workspace, plan.xocc);
+            op.npix_x = desc->N * desc->H * desc->W;
+            op.C = desc->C;
+            op.xct = weight_tile_channels();
+            op.xctiles = plan.ctiles;
+            op.xpb = (op.npix_x + plan.nchunks - 1) / plan.nchunks;
+        }
         if ((e = launch_occupancy(op, s)) != hipSuccess) return hip_status(e);
     }
     WeightParams p{};
@@ -287,6 +299,7 @@ int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void*
     p.dy = dY;
     p.out = plan.direct ? dW : at<float>(workspace, plan.partials);
     p.occ = skip ? occ : nullptr;
+    p.xocc = skip && x_skip ? at<uint8_t>(workspace, plan.xocc) : nullptr;
     p.skip_slots = at<int32_t>(workspace, plan.skip_slots);
     p.header = at<int>(workspace, plan.header);
     p.N = desc->N; p.H = desc->H; p.W = desc->W; p.C = desc->C; p.K = desc->K; p.R = desc->R; p.S = desc->S;
@@ -314,6 +327,19 @@ int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void*
         if (e != hipSuccess) return hip_status(e);
     }
     return CBW_OK;
+}
+
+int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void* dY, const uint32_t* dy_mask,
+                           float* dW, void* workspace, size_t workspace_bytes, uint32_t flags, void* stream)
+{
+    return run_weight(desc, X, dY, nullptr, dy_mask, false, dW, workspace, workspace_bytes, flags, stream);
+}
+
+int conv_bwd_weight_sparse_x(const cbw_conv_desc* desc, const void* X, const void* dY, const uint32_t* x_mask,
+                             const uint32_t* dy_mask, float* dW, void* workspace, size_t workspace_bytes,
+                             uint32_t flags, void* stream)
+{
+    return run_weight(desc, X, dY, x_mask, dy_mask, true, dW, workspace, workspace_bytes, flags, stream);
 }
 
 int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, size_t workspace_bytes,
@@ -351,7 +377,7 @@ int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, siz
         WeightPlan plan;
         if ((st = plan_weight(desc, &plan)) != CBW_OK) return st;
         if (workspace_bytes < plan.total) return CBW_ERR_WORKSPACE;
-        r.blocks_total = (int64_t)plan.nchunks * plan.ktiles;
+        r.blocks_total = (int64_t)plan.nchunks * plan.ktiles * plan.tgroups * plan.ctiles;
         int64_t skipped = 0;
         int32_t buf[256];
         const int32_t* slots = at<int32_t>(const_cast<void*>(workspace), plan.skip_slots);
@@ -362,7 +388,7 @@ int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, siz
             if (e != hipSuccess) return hip_status(e);
             for (int i = 0; i < n; ++i) skipped += buf[i];
         }
-        r.blocks_skipped = skipped / ((int64_t)plan.tgroups * plan.ctiles);
+        r.blocks_skipped = skipped;
     } else {
         return CBW_ERR_INVALID_ARG;
     }

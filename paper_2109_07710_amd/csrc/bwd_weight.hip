@@ -38,6 +38,56 @@ constexpr int TM = BM / WM, TN = BN / WN;
 constexpr int FM = TM / 16, FN = TN / 16;
 constexpr int CH = 8;           // 16-byte chunks per LDS row (128 bytes)
 constexpr int OCC_WIN = 1024;   // occupancy bytes cached per workgroup
+
+// X-operand liveness of chunks [ch_begin, ch_begin + nwin) for a tile over
+// filter taps [tap0, tap0 + ntaps) and channel tile ct: chunk i is live when
+// one of its dY pixels has, at one of those taps, an X pixel inside the image
+// whose channel tile holds a non-zero (xocc).  A chunk that is not live
+// multiplies an all-zero X operand, so skipping it changes no sum.  Every
+// writer stores 1, so concurrent stores to one byte agree.  Called by the
+// whole workgroup.
+__device__ void x_liveness(const WeightParams& p, int ch_begin, int nwin, int chunk_px, int tap0, int ntaps,
+                           int ct, uint8_t* xlive)
+{
+    constexpr int U = 4;   // pixels per thread per round, their loads issued together
+    const int tap_end = min(tap0 + ntaps, p.R * p.S);
+    for (int i = threadIdx.x; i < nwin; i += blockDim.x) xlive[i] = 0;
+    __syncthreads();
+    const int total = nwin * chunk_px;
+    for (int base = threadIdx.x; base < total; base += blockDim.x * U) {
+        int ci[U], nn[U], pp[U], qq[U];
+        bool ok[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int idx = base + u * (int)blockDim.x;
+            ci[u] = idx / chunk_px;
+            const int pix = (ch_begin + ci[u]) * chunk_px + (idx - ci[u] * chunk_px);
+            ok[u] = idx < total && pix < p.npq;
+            const uint32_t px = ok[u] ? (uint32_t)pix : 0u;
+            const uint32_t nq = fdiv(px, p.div_q);
+            qq[u] = (int)px - (int)nq * p.Q;
+            const uint32_t n = fdiv(nq, p.div_p);
+            pp[u] = (int)nq - (int)n * p.P;
+            nn[u] = (int)n;
+        }
+        uint32_t any = 0;   // bit u: pixel u sees a non-zero X
+        for (int tap = tap0; tap < tap_end; ++tap) {
+            const int r = tap / p.S, s = tap - r * p.S;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int h = pp[u] * p.stride_h - p.pad_h + r, w = qq[u] * p.stride_w - p.pad_w + s;
+                const bool in = ok[u] && h >= 0 && h < p.H && w >= 0 && w < p.W;
+                const int64_t a = in ? ((int64_t)(nn[u] * p.H + h) * p.W + w) * p.ctiles + ct : 0;
+                const uint8_t v = in ? p.xocc[a] : (uint8_t)0;
+                any |= (uint32_t)(v != 0) << u;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if ((any >> u) & 1u) xlive[ci[u]] = 1;
+    }
+    __syncthreads();
+}
 static_assert(BM == BN, "both operands share the staging layout");
 
 // Chunk swizzle: bijective on 16 consecutive rows (fragment reads) and
@@ -210,15 +260,21 @@ __global__ __launch_bounds__(NT) void bwd_weight_kernel(WeightParams p)
     // LDS (up to OCC_WIN of them); the loop then tests them without a global
     // read on its critical path.
     __shared__ uint8_t occ_s[OCC_WIN];
+    __shared__ uint8_t xlive_s[OCC_WIN];
     if (p.occ) {
         for (int i = tid; i < OCC_WIN && ch_begin + i < ch_end; i += NT)
             occ_s[i] = p.occ[(int64_t)(ch_begin + i) * p.ktiles + kt];
     }
     __syncthreads();
+    // Blocks whose X operand is entirely zero are skipped as well when the X
+    // occupancy is given (chunks past the cached window count as X-live).
+    const int nwin = min(OCC_WIN, max(ch_end - ch_begin, 0));
+    if (p.xocc) x_liveness(p, ch_begin, nwin, BK, tap, 1, ct, xlive_s);
     auto live = [&](int chunk) {
         if (p.occ == nullptr) return true;
         const int i = chunk - ch_begin;
-        const int v = i < OCC_WIN ? occ_s[i] : p.occ[(int64_t)chunk * p.ktiles + kt];
+        int v = i < OCC_WIN ? occ_s[i] : p.occ[(int64_t)chunk * p.ktiles + kt];
+        if (p.xocc && i < OCC_WIN) v &= xlive_s[i];
         return __builtin_amdgcn_readfirstlane(v) != 0;  // the same byte for the whole workgroup
     };
     auto next_live = [&](int chunk) {
@@ -436,15 +492,21 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
     // LDS (up to OCC_WIN of them); the loop then tests them without a global
     // read on its critical path.
     __shared__ uint8_t occ_s[OCC_WIN];
+    __shared__ uint8_t xlive_s[OCC_WIN];
     if (p.occ) {
         for (int i = tid; i < OCC_WIN && ch_begin + i < ch_end; i += NT)
             occ_s[i] = p.occ[(int64_t)(ch_begin + i) * p.ktiles + kt];
     }
     __syncthreads();
+    // Blocks whose X operand is entirely zero are skipped as well when the X
+    // occupancy is given (chunks past the cached window count as X-live).
+    const int nwin = min(OCC_WIN, max(ch_end - ch_begin, 0));
+    if (p.xocc) x_liveness(p, ch_begin, nwin, TR_BK, tg * p.tpg, p.tpg, ct, xlive_s);
     auto live = [&](int chunk) {
         if (p.occ == nullptr) return true;
         const int i = chunk - ch_begin;
-        const int v = i < OCC_WIN ? occ_s[i] : p.occ[(int64_t)chunk * p.ktiles + kt];
+        int v = i < OCC_WIN ? occ_s[i] : p.occ[(int64_t)chunk * p.ktiles + kt];
+        if (p.xocc && i < OCC_WIN) v &= xlive_s[i];
         return __builtin_amdgcn_readfirstlane(v) != 0;  // the same byte for the whole workgroup
     };
     int skipped = 0;

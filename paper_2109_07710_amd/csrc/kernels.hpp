@@ -48,6 +48,7 @@ struct WeightParams {
     const void* dy;          // [N*P*Q][K]
     float* out;              // [nsplit][K][R*S][C] partials, or dW (KRSC) when nsplit == 1
     const uint8_t* occ;      // [nchunks][ktiles] block occupancy, or null (no skipping)
+    const uint8_t* xocc;     // [N*H*W][ctiles] X pixel occupancy, or null (no X-block skipping)
     int32_t* skip_slots;     // [grid] skipped-block count per workgroup
     int* header;
     int N, H, W, C, K, R, S, P, Q;
@@ -69,6 +70,13 @@ struct OccParams {
     const uint32_t* bits;    // packed dY footprint, or null
     uint8_t* occ;            // [nchunks][ktiles]
     int npq, K, chunk, BNk, ktiles, nchunks, dtype;
+    // X pixel occupancy (only when xocc is set): xocc[px][ct] for X pixels
+    // px < npix_x and channel tiles of xct channels; block b covers X pixels
+    // [b*xpb, (b+1)*xpb).
+    const void* x;           // values [npix_x][C] (used when xbits == null)
+    const uint32_t* xbits;   // packed X footprint, or null
+    uint8_t* xocc;
+    int npix_x, C, xct, xctiles, xpb;
 };
 
 int data_tile_channels(int tile);

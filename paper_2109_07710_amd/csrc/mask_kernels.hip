@@ -152,6 +152,29 @@ __global__ __launch_bounds__(256) void occupancy_kernel(OccParams p)
     __syncthreads();
     for (int i = threadIdx.x; i < p.ktiles; i += blockDim.x)
         p.occ[(int64_t)chunk * p.ktiles + i] = (uint8_t)(flags[i] != 0);
+
+    // X occupancy: xocc[px][ct] = 1 iff X pixel px has a non-zero among
+    // channels [ct*xct, min(C, ct*xct + xct)) (packed footprint when given).
+    if (p.xocc) {
+        const int pairs = p.xpb * p.xctiles;
+        const int E = p.dtype == 1 ? 8 : 4;
+        for (int i = threadIdx.x; i < pairs; i += blockDim.x) {
+            const int64_t px = (int64_t)chunk * p.xpb + i / p.xctiles;
+            const int ct = i % p.xctiles;
+            if (px >= p.npix_x) continue;
+            const int lo = ct * p.xct, hi = min(p.C, lo + p.xct);
+            bool any = false;
+            if (p.xbits) {
+                any = any_bits(p.xbits, px * p.C + lo, px * p.C + hi);
+            } else {
+                const uint4* v4 = reinterpret_cast<const uint4*>(static_cast<const char*>(p.x) +
+                                                                 (px * p.C + lo) * (p.dtype == 1 ? 2 : 4));
+                for (int v = 0; v < (hi - lo) / E && !any; ++v)
+                    any = (p.dtype == 1 ? vec_bits<uint16_t>(v4[v], false) : vec_bits<float>(v4[v], false)) != 0;
+            }
+            p.xocc[px * p.xctiles + ct] = (uint8_t)any;
+        }
+    }
 }
 
 // dW = sum over splits of the partials in a fixed order.  part is

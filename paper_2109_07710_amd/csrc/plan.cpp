@@ -157,6 +157,7 @@ int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
     size_t cur = 0;
     p.header = take(&cur, 256);
     p.occ = take(&cur, (size_t)p.nchunks * p.ktiles);
+    p.xocc = take(&cur, (size_t)d->N * d->H * d->W * p.ctiles);
     p.skip_slots = take(&cur, (size_t)p.grid * 4);
     if (!p.direct) p.partials = take(&cur, (size_t)p.nsplit * d->K * d->R * d->S * d->C * 4);
     p.total = cur;

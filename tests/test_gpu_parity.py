@@ -15,7 +15,7 @@ import oracle
 import paper_2109_07710_amd as cb
 import workloads as wl
 from parity import (check_layer, check_values, check_zero_pattern, desc_of, dw_as_kcrs, dx_as_nchw,
-                    dx_bits_nchw, gpu_backward, oracle_backward, tol_for)
+                    dx_bits_nchw, gpu_backward, oracle_backward, oracle_inputs, to_dev, tol_for)
 
 pytestmark = pytest.mark.gpu
 
@@ -224,12 +224,85 @@ def test_occupancy_and_block_skip(use_bits):
     ref = oracle.block_occupancy(flat.float().numpy(), chunk, kw)
     assert np.array_equal(occ, ref)
     st = cb.cbw_read_stats(gpu["desc"], cb.CBW_OP_BWD_WEIGHT, gpu["ws_dw"])
-    assert st.blocks_total == ref.size and st.blocks_skipped == int((ref == 0).sum()) > 0
+    tiles = spec.R * spec.S          # C = 256: one tap per tile, one channel tile
+    assert st.blocks_total == ref.size * tiles and st.blocks_skipped == int((ref == 0).sum()) * tiles > 0
     ref_full = oracle_backward(spec, t)
     check_values(dw_as_kcrs(gpu["dw"]), ref_full["dw"], ref_full["dw_abs"], ref_full["dw_n"], tol_for("bf16"),
                  False, "dW with skipped blocks")
     g2 = gpu_backward(spec, t, flags=cb.CBW_FLAG_NO_SKIP)
     assert torch.equal(gpu["dw"], g2["dw"])
+
+
+def _x_skip_case(N, C, H, W, K, R, S, stride, pad, dtype, seed):
+    """Inputs with whole zero regions in both operands: X dead over a band of
+    rows of every image and over the upper channel tile of a few pixels, dY
+    dead over chunks and over one output-channel tile."""
+    rng = np.random.default_rng(seed)
+    spec = wl.LayerSpec("xskip", 0, 0, N=N, C=C, H=H, W=W, K=K, R=R, S=S, stride=stride, pad=pad, dtype=dtype)
+    x = np.maximum(rng.standard_normal((N, H, W, C), dtype=np.float32) - 0.25, 0)
+    x[:, 2:H // 2 + 3] = 0
+    x[0, H - 2:, :, C // 2:] = 0
+    dy = rng.standard_normal((N, spec.P, spec.Q, K), dtype=np.float32) * (rng.random((N, spec.P, spec.Q, K)) < 0.4)
+    flat = dy.reshape(-1, K)
+    flat[: flat.shape[0] // 3, : K // 2] = 0
+    flat[-flat.shape[0] // 4:] = 0
+    w = rng.standard_normal((K, R, S, C), dtype=np.float32) * 0.1
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    t = {"x": torch.from_numpy(x).to(tdt), "dy": torch.from_numpy(dy).to(tdt), "w": torch.from_numpy(w).to(tdt)}
+    return spec, t
+
+
+@pytest.mark.parametrize("case", [
+    (2, 256, 16, 16, 256, 3, 3, 1, 1, "bf16"),     # one tap per tile
+    (2, 64, 12, 14, 64, 3, 3, 1, 1, "bf16"),       # four taps packed per tile
+    (2, 48, 13, 11, 40, 3, 3, 2, 1, "bf16"),       # stride 2, five taps packed, ragged tiles
+    (2, 320, 9, 9, 72, 1, 1, 1, 0, "bf16"),        # 1x1, two channel tiles
+    (2, 32, 10, 10, 24, 3, 3, 1, 1, "f32"),        # float32 kernel
+], ids=["c256", "c64_packed", "stride2", "c320_1x1", "f32"])
+@pytest.mark.parametrize("use_bits", [True, False])
+def test_x_block_skip(case, use_bits):
+    """conv_bwd_weight_sparse_x: blocks whose dY or X operand is all zero are
+    skipped; the number skipped equals the oracle's count of dead blocks
+    (exact), dW matches the oracle and equals the non-skipping result."""
+    N, C, H, W, K, R, S, st, pd, dt = case
+    spec, t = _x_skip_case(N, C, H, W, K, R, S, st, pd, dt, seed=C + K)
+    _case("x-skip %s bits=%s" % (case, use_bits))
+    desc = desc_of(spec)
+    d = to_dev(t, "cuda")
+    xm = dym = None
+    if use_bits:
+        xm = torch.zeros(max(cb.cbw_mask_words(desc), 1), dtype=torch.int32, device="cuda")
+        cb.cbw_nonzero_mask_pack(desc.dtype, d["x"].numel(), d["x"], xm)
+        dym = torch.zeros(max(cb.cbw_dy_mask_words(desc), 1), dtype=torch.int32, device="cuda")
+        cb.cbw_nonzero_mask_pack(desc.dtype, d["dy"].numel(), d["dy"], dym)
+    ws = cb.workspace(desc, cb.CBW_OP_BWD_WEIGHT, "cuda")
+    dw = torch.empty((K, R, S, C), dtype=torch.float32, device="cuda")
+    cb.conv_bwd_weight_sparse_x(desc, d["x"], d["dy"], xm, dym, dw, ws)
+    st_x = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws)
+    occ, chunk, kw = cb.cbw_read_occupancy(desc, ws)
+    dw_y = torch.empty_like(dw)
+    cb.conv_bwd_weight_sparse(desc, d["x"], d["dy"], dym, dw_y, ws)
+    st_y = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws)
+    dw_n = torch.empty_like(dw)
+    cb.conv_bwd_weight_sparse_x(desc, d["x"], d["dy"], xm, dym, dw_n, ws, cb.CBW_FLAG_NO_SKIP)
+    torch.cuda.synchronize()
+    # the tiling: filter taps packed side by side for bf16 when two or more
+    # channel tiles fit in 256 columns, else one tap per 256-channel tile
+    packed = dt == "bf16" and R * S > 1 and 2 * C <= 256
+    tpg = min(256 // C, R * S) if packed else 1
+    ctile = C if packed else 256
+    x64, _, dy64 = oracle_inputs(t)
+    live = oracle.weight_block_liveness(x64 != 0, dy64 != 0, (R, S), (st, st), (pd, pd), chunk, kw, ctile, tpg)
+    live_y = oracle.weight_block_liveness(np.ones_like(x64, bool), dy64 != 0, (R, S), (st, st), (pd, pd),
+                                          chunk, kw, ctile, tpg)
+    assert st_x.blocks_total == live.size == st_y.blocks_total
+    assert st_x.blocks_skipped == int((~live).sum())
+    assert st_y.blocks_skipped == int((~live_y).sum()) > 0
+    if (C, st) in ((256, 1), (64, 1), (32, 1)):   # cases where the zero band empties whole X windows
+        assert st_x.blocks_skipped > st_y.blocks_skipped
+    ref_dw, ref_abs, ref_n = oracle.conv_bwd_weight(x64, dy64, (R, S), (st, st), (pd, pd), with_bound=True)
+    check_values(dw_as_kcrs(dw), ref_dw, ref_abs, ref_n, tol_for(dt), False, "dW with X-block skipping")
+    assert torch.equal(dw, dw_n) and torch.equal(dw, dw_y)
 
 
 def test_guard_bands_untouched():

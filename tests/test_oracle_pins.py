@@ -403,6 +403,45 @@ def test_sampled_forward_matches_full():
 
 # ---------------------------------------------------- bitmaps and indexing
 
+@pytest.mark.parametrize("stride,pad,tpg,chunk,ktile,ctile", [((1, 1), (1, 1), 1, 8, 4, 4), ((2, 1), (0, 2), 4, 5, 3, 8),
+                                                               ((1, 2), (1, 0), 9, 16, 8, 2)])
+def test_weight_block_liveness_brute_force(stride, pad, tpg, chunk, ktile, ctile):
+    """The weight-gradient block liveness against nested loops over every
+    operand element of every block: live iff both the block's dY operand and
+    its (tap-shifted) X operand hold a non-zero; and every product of a dead
+    block vanishes, so skipping it changes no sum."""
+    rng = np.random.default_rng(31)
+    N, C, H, W, K, R, S = 2, 8, 6, 7, 6, 3, 3
+    x = _rand(rng, (N, C, H, W), 0.3)
+    x[:, :, 1:4] = 0
+    dy_shape = (N, K, oracle.out_size(H, R, stride[0], pad[0]), oracle.out_size(W, S, stride[1], pad[1]))
+    dy = _rand(rng, dy_shape, 0.2)
+    dy[0] = 0
+    P, Q = dy_shape[2:]
+    live = oracle.weight_block_liveness(x != 0, dy != 0, (R, S), stride, pad, chunk, ktile, ctile, tpg)
+    nch = -(-N * P * Q // chunk)
+    assert live.shape == (-(-R * S // tpg), -(-C // ctile), -(-K // ktile), nch)
+    for g, ct, kt, b in itertools.product(*map(range, live.shape)):
+        dy_nz = x_nz = prod_nz = False
+        for pix in range(b * chunk, min((b + 1) * chunk, N * P * Q)):
+            n, rem = divmod(pix, P * Q)
+            p, q = divmod(rem, Q)
+            for k in range(kt * ktile, min((kt + 1) * ktile, K)):
+                dy_nz |= dy[n, k, p, q] != 0
+            for tap in range(g * tpg, min((g + 1) * tpg, R * S)):
+                r, s = divmod(tap, S)
+                h, w = p * stride[0] - pad[0] + r, q * stride[1] - pad[1] + s
+                if not (0 <= h < H and 0 <= w < W):
+                    continue
+                for c in range(ct * ctile, min((ct + 1) * ctile, C)):
+                    x_nz |= x[n, c, h, w] != 0
+                    for k in range(kt * ktile, min((kt + 1) * ktile, K)):
+                        prod_nz |= dy[n, k, p, q] * x[n, c, h, w] != 0
+        assert live[g, ct, kt, b] == (dy_nz and x_nz), (g, ct, kt, b)
+        assert live[g, ct, kt, b] or not prod_nz
+    assert live.any() and not live.all()
+
+
 def test_pack_bits_brute_force():
     rng = np.random.default_rng(37)
     for n in [1, 31, 32, 33, 100, 257]:
