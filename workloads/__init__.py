@@ -222,6 +222,30 @@ def draw(spec: LayerSpec, want=("x", "w", "dy")):
     return out
 
 
+def draw_on_device(spec: LayerSpec, device="cuda"):
+    """The layer's tensors drawn directly in device memory with torch's
+    seeded device generator: for sizes whose host-side generation would take
+    minutes (the largest tensors a buffer descriptor can address).  Same
+    recipe as draw() for "shifted_gauss" X and "bernoulli" dY (values differ
+    from draw(): another generator).  bf16 only."""
+    assert spec.dtype == "bf16" and spec.x_kind == "shifted_gauss" and spec.dy_kind == "bernoulli"
+    g = torch.Generator(device=device)
+    g.manual_seed(ROOT_SEED * 1000 + spec.config_id * 100 + spec.layer_id)
+    n, c, h, w_, k = spec.N, spec.C, spec.H, spec.W, spec.K
+    x = torch.randn((n, h, w_, c), generator=g, device=device, dtype=torch.float32)
+    x.sub_(spec.x_param).clamp_(min=0.0)
+    x = x.to(torch.bfloat16)
+    wt = torch.randn((k, spec.R, spec.S, c), generator=g, device=device, dtype=torch.float32)
+    wt.mul_(sqrt(2.0 / (c * spec.R * spec.S)))
+    wt = wt.to(torch.bfloat16)
+    dy = torch.randn((n, spec.P, spec.Q, k), generator=g, device=device, dtype=torch.float32)
+    live = torch.rand((n, spec.P, spec.Q, k), generator=g, device=device) < spec.dy_param
+    dy.mul_(live)
+    dy.masked_fill_(~live, 0.0)          # +0.0 where dead
+    dy = dy.to(torch.bfloat16)
+    return {"x": x, "w": wt, "dy": dy}
+
+
 # ------------------------------------------------------------ configurations
 
 def config1():
