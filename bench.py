@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU baseline time budget")
-    ap.add_argument("--sweep", choices=["config4", "config3", "config5", "config5_pooled"], default=None,
+    ap.add_argument("--sweep", choices=["config4", "config3", "config5", "config5_pooled", "elementwise"], default=None,
                     help="instead of the main line, time the sparse and dense steps over a workload set "
                          "(one JSON line per layer or density point)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -343,8 +343,88 @@ def layer_timing(cb, torch, spec, steps, warmup):
     return rec
 
 
+def elementwise_sweep(args):
+    """Break-even of the per-element data gradient (vector ALUs, every zero dY
+    entry and every dead pixel skipped) against the matrix-core masked path,
+    data gradient only, on i.i.d. footprints with mask density = dY density
+    = d (configuration 4's layer and configuration 2's layer)."""
+    import torch
+    import paper_2109_07710_amd as cb
+    import workloads as wl
+    dev = torch.device("cuda:0")
+    for make, tag in ((lambda d: wl.config4(d, "bernoulli")[0], "conv3x3_c512_14x14_N128"),
+                      (lambda d: wl.LayerSpec("vgg_conv3x3_c256_56x56", 2, 0, N=32, C=256, H=56, W=56, K=256, R=3, S=3,
+                                              x_kind="shifted_gauss", x_param=wl.threshold_for_density(d),
+                                              dy_kind="bernoulli", dy_param=d), "conv3x3_c256_56x56_N32")):
+        for d in (0.01, 0.02, 0.03, 0.05, 0.1, 0.2, 0.4):
+            spec = make(d)
+            log("elementwise sweep %s d=%.2f" % (tag, d))
+            t = wl.draw(spec)
+            x, w, dy = (t[k].to(dev) for k in ("x", "w", "dy"))
+            del t
+            desc = cb.ConvDesc.make(spec.N, spec.C, spec.H, spec.W, spec.K, spec.R, spec.S, spec.stride, spec.pad)
+            xm = torch.zeros(cb.cbw_mask_words(desc), dtype=torch.int32, device=dev)
+            cb.cbw_relu_mask_pack(desc, x, xm)
+            dx = torch.empty_like(x)
+            ws_m = cb.workspace(desc, cb.CBW_OP_BWD_DATA_MASKED, dev)
+            ws_e = cb.workspace(desc, cb.CBW_OP_BWD_DATA_ELEMENTWISE, dev)
+
+            def mfma():
+                cb.conv_bwd_data_masked(desc, dy, w, xm, dx, ws_m, 0)
+
+            def valu():
+                cb.conv_bwd_data_elementwise(desc, dy, w, xm, dx, ws_e)
+
+            def tm(fn, n):
+                torch.cuda.synchronize()
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                for _ in range(n):
+                    fn()
+                b.record()
+                torch.cuda.synchronize()
+                return a.elapsed_time(b) / n
+
+            for _ in range(10):
+                mfma()
+                valu()
+            ms_m, ms_v = float("inf"), float("inf")
+            for _ in range(2):
+                ms_m = min(ms_m, tm(mfma, 10))
+                ms_v = min(ms_v, tm(valu, 10))
+            _, products = cb.cbw_read_pixel_counts(desc, ws_e)
+            f_useful = 2 * int(useful_products(x, dy, spec))
+            print(json.dumps({"sweep": "elementwise", "layer": tag, "density": d,
+                              "mfma_masked_dx_ms": round(ms_m, 4), "valu_elementwise_dx_ms": round(ms_v, 4),
+                              "valu_over_mfma": round(ms_v / ms_m, 3),
+                              "valu_products_executed": products,
+                              "valu_executed_gflop": round(2 * products * spec.C / 1e9, 3),
+                              "useful_gflop": round(f_useful / 1e9, 3),
+                              "dense_gflop": round(spec.dense_flops() / 1e9, 3)}), flush=True)
+            del x, w, dy, xm, dx, ws_m, ws_e
+
+
+def useful_products(x, dy, spec):
+    """Multiply-adds of the data gradient that have a live output and a
+    non-zero dY operand (IN+OUT useful work), counted on the device from the
+    tensors: for each output pixel, live channels x non-zero dY entries over
+    its in-range taps (stride 1)."""
+    import torch
+    live_c = (x > 0).sum(dim=3).double()                      # [N,H,W] live channels per pixel
+    nz = (dy != 0).sum(dim=3).double()                        # [N,P,Q] non-zeros per source pixel
+    pad = torch.nn.functional.pad(nz, (spec.pad, spec.pad, spec.pad, spec.pad))
+    tot = torch.zeros_like(live_c)
+    for r in range(spec.R):
+        for s in range(spec.S):
+            # output (h, w) reads source (h + pad - r, w + pad - s)
+            tot += pad[:, 2 * spec.pad - r:2 * spec.pad - r + spec.H, 2 * spec.pad - s:2 * spec.pad - s + spec.W]
+    return (tot * live_c).sum().item()
+
+
 def run_sweep(args):
     import torch
+    if args.sweep == "elementwise":
+        return elementwise_sweep(args)
 
     import paper_2109_07710_amd as cb
     import workloads as wl

@@ -80,7 +80,8 @@ typedef struct {
 } cbw_conv_desc;
 
 /* Operation selector for cbw_workspace_size / cbw_read_stats. */
-enum { CBW_OP_BWD_DATA = 0, CBW_OP_BWD_DATA_MASKED = 1, CBW_OP_BWD_WEIGHT = 2, CBW_OP_FWD = 3 };
+enum { CBW_OP_BWD_DATA = 0, CBW_OP_BWD_DATA_MASKED = 1, CBW_OP_BWD_WEIGHT = 2, CBW_OP_FWD = 3,
+       CBW_OP_BWD_DATA_ELEMENTWISE = 4 };
 
 /* Flags. CBW_FLAG_NO_SKIP runs the same kernels with every skip disabled:
  * the masked data gradient computes all rows and applies the mask in its
@@ -184,6 +185,29 @@ int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void*
 int conv_bwd_weight_sparse_x(const cbw_conv_desc* desc, const void* X, const void* dY,
                              const uint32_t* x_mask, const uint32_t* dy_mask, float* dW,
                              void* workspace, size_t workspace_bytes, uint32_t flags, void* stream);
+
+/* Data gradient with per-element input and output sparsity on the vector
+ * ALUs (Sec. III-B, input and output sparsity; Sec. IV-B, lanes that walk
+ * only the non-zero offsets of their gradient column).  Same result as
+ * conv_bwd_data_masked up to summation order: dX = x_mask ? sum over the
+ * non-zero dY entries only : +0.0.  A pixel whose footprint row is entirely
+ * dead costs one zero store; every other pixel sums, per filter tap, only the
+ * non-zero entries of its source dY row.  For very sparse inputs, where the
+ * matrix-core path cannot skip anything.  Supported: bf16, NHWC, KRSC filters,
+ * C in {64, 128, 256, 512}, K < 65536; other descriptors return
+ * CBW_ERR_UNSUPPORTED.  Deterministic.  dX is fully overwritten.
+ * Workspace: cbw_workspace_size(desc, CBW_OP_BWD_DATA_ELEMENTWISE); after
+ * the call it holds, per output pixel, the number of (tap, k) products
+ * executed (cbw_read_pixel_counts). */
+int conv_bwd_data_elementwise(const cbw_conv_desc* desc, const void* dY, const void* W,
+                              const uint32_t* x_mask, void* dX, void* workspace, size_t workspace_bytes,
+                              void* stream);
+
+/* After conv_bwd_data_elementwise on `workspace`: copies the per-pixel
+ * product counts (N*H*W int32 in pixel order; `counts` may be NULL) and
+ * their sum to the host (waits for `stream`). */
+int cbw_read_pixel_counts(const cbw_conv_desc* desc, const void* workspace, size_t workspace_bytes,
+                          int32_t* counts, int64_t* total, void* stream);
 
 /* Copy the statistics of the last `op` call that used `workspace` to the host
  * (waits for `stream`). */

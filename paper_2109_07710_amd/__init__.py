@@ -22,13 +22,13 @@ CBW_OK, CBW_ERR_INVALID_ARG, CBW_ERR_UNSUPPORTED, CBW_ERR_WORKSPACE, CBW_ERR_HIP
 CBW_NCHW, CBW_NHWC = 0, 1
 CBW_KCRS, CBW_KRSC = 0, 1
 CBW_F32, CBW_BF16 = 0, 1
-CBW_OP_BWD_DATA, CBW_OP_BWD_DATA_MASKED, CBW_OP_BWD_WEIGHT, CBW_OP_FWD = 0, 1, 2, 3
+CBW_OP_BWD_DATA, CBW_OP_BWD_DATA_MASKED, CBW_OP_BWD_WEIGHT, CBW_OP_FWD, CBW_OP_BWD_DATA_ELEMENTWISE = 0, 1, 2, 3, 4
 CBW_FLAG_NO_SKIP = 1
 
 EXPORTS = ("cbw_status_string", "cbw_validate_desc", "cbw_mask_words", "cbw_dy_mask_words",
            "cbw_workspace_size", "cbw_relu_mask_pack", "cbw_nonzero_mask_pack", "conv_bwd_data",
            "conv_bwd_data_masked", "conv_fwd_relu_mask", "conv_bwd_weight_sparse", "conv_bwd_weight_sparse_x",
-           "cbw_read_stats",
+           "conv_bwd_data_elementwise", "cbw_read_pixel_counts", "cbw_read_stats",
            "cbw_read_live_lists",
            "cbw_read_occupancy", "cbw_set_profile_events")
 
@@ -92,6 +92,8 @@ def lib():
     L.conv_fwd_relu_mask.argtypes = [dp, vp, vp, vp, vp, vp, sz, vp]
     L.conv_bwd_weight_sparse.argtypes = [dp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
     L.conv_bwd_weight_sparse_x.argtypes = [dp, vp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
+    L.conv_bwd_data_elementwise.argtypes = [dp, vp, vp, vp, vp, vp, sz, vp]
+    L.cbw_read_pixel_counts.argtypes = [dp, vp, sz, vp, ctypes.POINTER(ctypes.c_int64), vp]
     L.cbw_read_stats.argtypes = [dp, ctypes.c_int, vp, sz, ctypes.POINTER(Stats), vp]
     i32p = ctypes.POINTER(ctypes.c_int32)
     L.cbw_read_live_lists.argtypes = [dp, vp, sz, ctypes.c_int, vp, i32p, i32p, vp]
@@ -199,6 +201,23 @@ def conv_bwd_weight_sparse_x(desc, X, dY, x_mask, dy_mask, dW, ws, flags=0, stre
     _check(lib().conv_bwd_weight_sparse_x(ctypes.byref(desc), _ptr(X), _ptr(dY), _ptr(x_mask), _ptr(dy_mask),
                                           _ptr(dW), _ptr(ws), _nbytes(ws), flags, _stream(stream)),
            "conv_bwd_weight_sparse_x")
+
+
+def conv_bwd_data_elementwise(desc, dY, W, x_mask, dX, ws, stream=None):
+    _check(lib().conv_bwd_data_elementwise(ctypes.byref(desc), _ptr(dY), _ptr(W), _ptr(x_mask), _ptr(dX),
+                                           _ptr(ws), _nbytes(ws), _stream(stream)), "conv_bwd_data_elementwise")
+
+
+def cbw_read_pixel_counts(desc, ws, stream=None):
+    """Per-pixel (tap, k) product counts of the last conv_bwd_data_elementwise
+    call on ws (numpy int32 [N*H*W]) and their sum."""
+    import numpy as np
+    out = np.zeros(desc.N * desc.H * desc.W, np.int32)
+    tot = ctypes.c_int64(0)
+    _check(lib().cbw_read_pixel_counts(ctypes.byref(desc), _ptr(ws), _nbytes(ws),
+                                       out.ctypes.data_as(ctypes.c_void_p), ctypes.byref(tot), _stream(stream)),
+           "cbw_read_pixel_counts")
+    return out, tot.value
 
 
 def cbw_read_stats(desc, op, ws, stream=None):

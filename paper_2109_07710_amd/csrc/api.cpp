@@ -2,6 +2,8 @@
 // the caller's stream.  See include/convbwd.h for the contract.
 #include <hip/hip_runtime.h>
 
+#include <cstring>
+
 #include "../../include/convbwd.h"
 #include "kernels.hpp"
 #include "plan.hpp"
@@ -189,6 +191,24 @@ size_t cbw_dy_mask_words(const cbw_conv_desc* d)
     return (size_t)(((int64_t)d->N * d->K * d->P * d->Q + 31) / 32);
 }
 
+// Descriptors the per-element data gradient supports.
+static int validate_elementwise(const cbw_conv_desc* d)
+{
+    const int st = validate_desc(d);
+    if (st != CBW_OK) return st;
+    if (d->dtype != CBW_BF16 || d->w_layout != CBW_KRSC) return CBW_ERR_UNSUPPORTED;
+    if (d->C != 64 && d->C != 128 && d->C != 256 && d->C != 512) return CBW_ERR_UNSUPPORTED;
+    if (d->K >= 65536) return CBW_ERR_UNSUPPORTED;   // k is packed in 16 bits
+    if (d->R * d->S > 255) return CBW_ERR_UNSUPPORTED;   // the tap is kept in 8 bits
+    return CBW_OK;
+}
+
+// Workspace of the per-element data gradient: an int32 count per output pixel.
+static size_t elementwise_ws(const cbw_conv_desc* d)
+{
+    return ((size_t)d->N * d->H * d->W * 4 + 255) / 256 * 256;
+}
+
 int cbw_workspace_size(const cbw_conv_desc* desc, int op, size_t* bytes)
 {
     if (!bytes) return CBW_ERR_INVALID_ARG;
@@ -203,6 +223,11 @@ int cbw_workspace_size(const cbw_conv_desc* desc, int op, size_t* bytes)
         WeightPlan p;
         if ((st = plan_weight(desc, &p)) != CBW_OK) return st;
         *bytes = p.total;
+        return CBW_OK;
+    }
+    if (op == CBW_OP_BWD_DATA_ELEMENTWISE) {
+        if ((st = validate_elementwise(desc)) != CBW_OK) return st;
+        *bytes = elementwise_ws(desc);
         return CBW_OK;
     }
     if (op == CBW_OP_FWD) {
@@ -326,6 +351,56 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
                                  desc->w_layout == CBW_KRSC, s);
         if (e != hipSuccess) return hip_status(e);
     }
+    return CBW_OK;
+}
+
+int conv_bwd_data_elementwise(const cbw_conv_desc* desc, const void* dY, const void* W, const uint32_t* x_mask,
+                              void* dX, void* workspace, size_t workspace_bytes, void* stream)
+{
+    int st = validate_elementwise(desc);
+    if (st != CBW_OK) return st;
+    if (!dY || !W || !dX || !x_mask) return CBW_ERR_INVALID_ARG;
+    if (!aligned16(dY) || !aligned16(W) || !aligned16(dX) || !aligned16(x_mask)) return CBW_ERR_UNSUPPORTED;
+    if ((st = check_ws(workspace, workspace_bytes, elementwise_ws(desc))) != CBW_OK) return st;
+    EwParams p{};
+    p.dy = dY;
+    p.w = W;
+    p.mask = x_mask;
+    p.dx = dX;
+    p.counts = static_cast<int32_t*>(workspace);
+    p.N = desc->N; p.H = desc->H; p.W = desc->W; p.C = desc->C; p.K = desc->K; p.R = desc->R; p.S = desc->S;
+    p.P = desc->P; p.Q = desc->Q;
+    p.stride_h = desc->stride_h; p.stride_w = desc->stride_w; p.pad_h = desc->pad_h; p.pad_w = desc->pad_w;
+    p.npix = desc->N * desc->H * desc->W;
+    p.dy_bytes = (uint32_t)((int64_t)desc->N * desc->P * desc->Q * desc->K * 2);
+    p.w_bytes = (uint32_t)((int64_t)desc->K * desc->R * desc->S * desc->C * 2);
+    p.dx_bytes = (uint32_t)((int64_t)p.npix * desc->C * 2);
+    p.div_w = make_fastdiv((uint32_t)desc->W);
+    p.div_h = make_fastdiv((uint32_t)desc->H);
+    return hip_status(launch_elementwise_data(p, static_cast<hipStream_t>(stream)));
+}
+
+int cbw_read_pixel_counts(const cbw_conv_desc* desc, const void* workspace, size_t workspace_bytes,
+                          int32_t* counts, int64_t* total, void* stream)
+{
+    int st = validate_elementwise(desc);
+    if (st != CBW_OK) return st;
+    if (!workspace || !total) return CBW_ERR_INVALID_ARG;
+    if (workspace_bytes < elementwise_ws(desc)) return CBW_ERR_WORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int64_t npix = (int64_t)desc->N * desc->H * desc->W;
+    const int32_t* src = static_cast<const int32_t*>(workspace);
+    int64_t sum = 0;
+    int32_t buf[4096];
+    for (int64_t i0 = 0; i0 < npix; i0 += 4096) {
+        const int64_t n = npix - i0 < 4096 ? npix - i0 : 4096;
+        hipError_t e = hipMemcpyAsync(buf, src + i0, n * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_status(e);
+        for (int64_t i = 0; i < n; ++i) sum += buf[i];
+        if (counts) std::memcpy(counts + i0, buf, n * sizeof(int32_t));
+    }
+    *total = sum;
     return CBW_OK;
 }
 

@@ -79,6 +79,21 @@ struct OccParams {
     int npix_x, C, xct, xctiles, xpb;
 };
 
+// Per-element data gradient on the vector ALUs (bf16, NHWC, KRSC filters).
+struct EwParams {
+    const void* dy;          // [N*P*Q][K]
+    const void* w;           // [K][R][S][C]
+    const uint32_t* mask;    // footprint of X, bit per element of [N*H*W][C]
+    void* dx;                // [N*H*W][C]
+    int32_t* counts;         // [N*H*W] (tap, k) products executed per pixel
+    int N, H, W, C, K, R, S, P, Q;
+    int stride_h, stride_w, pad_h, pad_w;
+    int npix;
+    uint32_t dy_bytes, w_bytes, dx_bytes;
+    FastDiv div_w, div_h;
+};
+hipError_t launch_elementwise_data(const EwParams& p, hipStream_t stream);
+
 int data_tile_channels(int tile);
 int data_tile_pixels(int tile);
 int weight_tile_channels();

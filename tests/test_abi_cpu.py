@@ -128,6 +128,30 @@ def test_forward_descriptor_rules(L):
         cb.CBW_ERR_UNSUPPORTED
 
 
+def test_elementwise_descriptor_rules(L):
+    """The per-element data gradient: bf16, KRSC, C in {64, 128, 256, 512},
+    K < 65536; its workspace is one int32 count per output pixel."""
+    for C in (64, 128, 256, 512):
+        d = cb.ConvDesc.make(2, C, 10, 12, 40, 3, 3, 1, 1)
+        assert cb.cbw_workspace_size(d, cb.CBW_OP_BWD_DATA_ELEMENTWISE) == (2 * 10 * 12 * 4 + 255) // 256 * 256
+    n = ctypes.c_size_t(0)
+    bad = [cb.ConvDesc.make(2, 96, 10, 12, 40, 3, 3, 1, 1), cb.ConvDesc.make(2, 1024, 4, 4, 8, 1, 1),
+           cb.ConvDesc.make(2, 64, 10, 12, 40, 3, 3, 1, 1, dtype="f32"),
+           cb.ConvDesc.make(2, 64, 10, 12, 40, 3, 3, 1, 1, w_layout="kcrs"),
+           cb.ConvDesc.make(1, 64, 2, 2, 65536, 1, 1)]
+    fake = ctypes.c_void_p(1 << 20)
+    for d in bad:
+        assert L.cbw_workspace_size(ctypes.byref(d), cb.CBW_OP_BWD_DATA_ELEMENTWISE, ctypes.byref(n)) == \
+            cb.CBW_ERR_UNSUPPORTED
+        assert L.conv_bwd_data_elementwise(ctypes.byref(d), fake, fake, fake, fake, fake, 1 << 20, None) == \
+            cb.CBW_ERR_UNSUPPORTED
+    good = cb.ConvDesc.make(2, 64, 10, 12, 40, 3, 3, 1, 1)
+    assert L.conv_bwd_data_elementwise(ctypes.byref(good), fake, fake, None, fake, fake, 1 << 20, None) == \
+        cb.CBW_ERR_INVALID_ARG
+    assert L.conv_bwd_data_elementwise(ctypes.byref(good), fake, fake, fake, fake, fake, 16, None) == \
+        cb.CBW_ERR_WORKSPACE
+
+
 def test_null_arguments_rejected_without_gpu(L):
     d = _desc()
     n = ctypes.c_size_t(0)
