@@ -38,7 +38,6 @@ namespace cbw {
 
 namespace {
 
-constexpr int NT = 512;   // 8 waves (two per SIMD) for every tile shape
 constexpr int CH = 8;     // 16-byte chunks of reduction per row per step
 
 // Compile-time shape of data-gradient tile TI (kDataTiles[TI]).
@@ -48,12 +47,13 @@ struct Tile {
     static constexpr int BN = kDataTiles[TI].bn;       // pixels per tile
     static constexpr int WM = kDataTiles[TI].wm;       // waves along channels
     static constexpr int WN = kDataTiles[TI].wn;       // waves along pixels
-    static constexpr int NW = WM * WN;
+    static constexpr int NW = WM * WN;                 // waves: 8 or 16
+    static constexpr int NT = NW * 64;
     static constexpr int TM = BM / WM, TN = BN / WN;   // wave tile
     static constexpr int FM = TM / 16, FN = TN / 16;   // 16x16 MFMA tiles per wave
     static constexpr int IA = (BM / 8 + NW - 1) / NW;  // 1 KB copy instructions per wave per step, A
     static constexpr int IB = (BN / 8 + NW - 1) / NW;  // same for B
-    static_assert(NW * 64 == NT, "eight waves");
+    static_assert(NW == 8 || NW == 16, "two or four waves per SIMD");
     static_assert(BM % 8 == 0 && BN % 8 == 0, "tiles are copied in groups of 8 rows");
     static_assert(TM % 16 == 0 && TN % 16 == 0, "wave tile must be a multiple of 16");
 };
@@ -61,11 +61,12 @@ struct Tile {
 __device__ __forceinline__ int swz8(int row) { return (row >> 1) & 7; }
 
 template <typename T, int MODE, bool UNIT, int TI>
-__global__ __launch_bounds__(NT) void bwd_data_kernel(DataParams p)
+__global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
 {
     using TL = Tile<TI>;
     constexpr int BM = TL::BM, BN = TL::BN, WN = TL::WN, NW = TL::NW;
     constexpr int TM = TL::TM, TN = TL::TN, FM = TL::FM, FN = TL::FN, IA = TL::IA, IB = TL::IB;
+    constexpr int NT = TL::NT;
     constexpr int E = Elem<T>::E;
     constexpr int BK = CH * E;     // reduction elements per step
     constexpr uint32_t ESZ = sizeof(T);
@@ -683,9 +684,11 @@ template <typename T, int MODE, int TI>
 hipError_t launch_shape(const DataParams& p, int nb, hipStream_t stream, const ProfEvents& ev)
 {
     if (p.stride_h == 1 && p.stride_w == 1)
-        hipExtLaunchKernelGGL(bwd_data_kernel<T, MODE, true, TI>, dim3(nb), dim3(NT), 0, stream, ev.start, ev.stop, 0, p);
+        hipExtLaunchKernelGGL(bwd_data_kernel<T, MODE, true, TI>, dim3(nb), dim3(Tile<TI>::NT), 0, stream, ev.start,
+                              ev.stop, 0, p);
     else
-        hipExtLaunchKernelGGL(bwd_data_kernel<T, MODE, false, TI>, dim3(nb), dim3(NT), 0, stream, ev.start, ev.stop, 0, p);
+        hipExtLaunchKernelGGL(bwd_data_kernel<T, MODE, false, TI>, dim3(nb), dim3(Tile<TI>::NT), 0, stream, ev.start,
+                              ev.stop, 0, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     // in gather mode the split is only known on the device

@@ -343,13 +343,14 @@ __device__ __forceinline__ uint2 ds_read_tr16(const void* lds)
     return __builtin_bit_cast(uint2, v);
 }
 
+constexpr int TR_NT = 1024;            // 16 waves (four per SIMD): more waves hide more copy and LDS latency
 constexpr int TR_BK = 64;              // pixels per step
 constexpr int TR_ROW = BM / 8;         // 16-byte chunks per LDS row (one pixel)
-constexpr int TR_IA = TR_BK * BM * 2 / 1024 / (NT / 64);  // 1 KB copies per wave per step, per operand
+constexpr int TR_IA = TR_BK * BM * 2 / 1024 / (TR_NT / 64);  // 1 KB copies per wave per step, per operand
 static_assert(BM == 256 && BN == 256, "the natural-layout kernel assumes 256-wide rows");
 
 // Tiling of the natural-layout kernel for BKT output channels per tile
-// (256, 128 or 64): the 8 waves split the 256 channel columns WM ways and the
+// (256, 128 or 64): the 16 waves split the 256 channel columns WM ways and the
 // BKT output channels WN ways, so every wave holds 64 output channels and
 // 256/WM channel columns.  The channel columns are tpg filter taps of C
 // channels each when taps are packed (C <= 128; columns past tpg*C are
@@ -357,17 +358,17 @@ static_assert(BM == 256 && BN == 256, "the natural-layout kernel assumes 256-wid
 // copied as out-of-range zeros and never read.
 template <int BKT>
 struct WTile {
-    static constexpr int WN = BKT / 64, WM = (NT / 64) / WN;
+    static constexpr int WN = BKT / 64, WM = (TR_NT / 64) / WN;
     static constexpr int TM = BM / WM, TN = BKT / WN;
     static constexpr int FM = TM / 16, FN = TN / 16;
-    static_assert(WM * WN * 64 == NT && TN == 64, "64 output channels per wave");
+    static_assert(WM * WN * 64 == TR_NT && TN == 64, "64 output channels per wave");
 };
 
 template <int BKT>
-__global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
+__global__ __launch_bounds__(TR_NT) void bwd_weight_tr_kernel(WeightParams p)
 {
     constexpr uint32_t ESZ = 2;
-    constexpr int NW = NT / 64;
+    constexpr int NW = TR_NT / 64;
     constexpr int WN = WTile<BKT>::WN;
     constexpr int TM = WTile<BKT>::TM, TN = WTile<BKT>::TN, FM = WTile<BKT>::FM, FN = WTile<BKT>::FN;
     __shared__ uint4 As[2][TR_BK * TR_ROW];
@@ -494,7 +495,7 @@ __global__ __launch_bounds__(NT) void bwd_weight_tr_kernel(WeightParams p)
     __shared__ uint8_t occ_s[OCC_WIN];
     __shared__ uint8_t xlive_s[OCC_WIN];
     if (p.occ) {
-        for (int i = tid; i < OCC_WIN && ch_begin + i < ch_end; i += NT)
+        for (int i = tid; i < OCC_WIN && ch_begin + i < ch_end; i += TR_NT)
             occ_s[i] = p.occ[(int64_t)(ch_begin + i) * p.ktiles + kt];
     }
     __syncthreads();
@@ -567,7 +568,7 @@ int weight_chunk(int dtype) { return CH * (dtype == 1 ? 8 : 4); }
 hipError_t launch_bwd_weight(int dtype, const WeightParams& p, hipStream_t stream, const ProfEvents& ev)
 {
     const int nb = p.tgroups * p.ctiles * p.ktiles * p.nsplit;
-    const dim3 grid(nb), block(NT);
+    const dim3 grid(nb), block(dtype == 1 ? TR_NT : NT);
     if (dtype == 1) {
         if (p.bk == 64) hipExtLaunchKernelGGL(bwd_weight_tr_kernel<64>, grid, block, 0, stream, ev.start, ev.stop, 0, p);
         else if (p.bk == 128) hipExtLaunchKernelGGL(bwd_weight_tr_kernel<128>, grid, block, 0, stream, ev.start, ev.stop, 0, p);

@@ -23,13 +23,14 @@
 #endif
 #define CBW_NUM_CUS 256
 
-// Data-gradient tiles: output channels x pixels, and the waves along each
-// (8 waves, two per SIMD, every wave a 64 x 112 or 64 x 64 block).  The
-// planner picks one per layer from the output channel count, so narrow
-// layers do not pad their channels to 256; the channel width is also the
-// compaction group width.
+// Data-gradient tiles: output channels x pixels, and the waves along each.
+// Every tile runs 16 waves (four per SIMD; wave blocks of 32 x 112, 32 x 112
+// and 32 x 64): more waves hide more of the copy and LDS latency than the
+// larger wave blocks of 8 waves save.  The planner picks one per layer from
+// the output channel count, so narrow layers do not pad their channels to
+// 256; the channel width is also the compaction group width.
 struct DataTile {
     int bm, bn, wm, wn;
 };
 constexpr int kDataTileCount = 3;
-constexpr DataTile kDataTiles[kDataTileCount] = {{256, 224, 4, 2}, {128, 448, 2, 4}, {64, 512, 1, 8}};
+constexpr DataTile kDataTiles[kDataTileCount] = {{256, 224, 8, 2}, {128, 448, 4, 4}, {64, 512, 2, 8}};
