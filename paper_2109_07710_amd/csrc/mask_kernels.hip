@@ -181,10 +181,10 @@ __global__ __launch_bounds__(256) void occupancy_kernel(OccParams p)
 // [nsplit][K][RS][C]; dW is written in KRSC or KCRS.  A block covers 256/G
 // float4 outputs with G threads each: thread g sums the consecutive splits
 // [g*nsplit/G, (g+1)*nsplit/G) in order, then the G group sums are added in
-// group order.  G = 1 when there are enough outputs to fill the machine; a
-// larger G keeps small outputs with many splits from running one long
-// serial sum per thread.  The order depends only on (nsplit, G), so results
-// are reproducible.
+// group order.  G grows (up to 16) until the launch has enough threads to
+// fill the machine, so that few outputs with many splits do not run one
+// long serial sum per thread.  The order depends only on (nsplit, G), so
+// results are reproducible.
 template <int G>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, float* __restrict__ dw,
                                                            int nsplit, int K, int RS, int C, int krsc)
@@ -198,10 +198,18 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     const int z0 = (int)((int64_t)g * nsplit / G), z1 = (int)((int64_t)(g + 1) * nsplit / G);
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
     if (i4 * 4 < total) {
-        for (int z = z0; z < z1; ++z) {
-            const float4 v = p4[(int64_t)z * (total / 4) + i4];
-            if (z == z0) s = v;
-            else { s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w; }
+        // the loads of four splits are issued before they are added, in order
+        for (int zb = z0; zb < z1; zb += 4) {
+            float4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                v[u] = zb + u < z1 ? p4[(int64_t)(zb + u) * (total / 4) + i4] : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (zb + u >= z1) break;
+                if (zb + u == z0) s = v[u];
+                else { s.x += v[u].x; s.y += v[u].y; s.z += v[u].z; s.w += v[u].w; }
+            }
         }
     }
     if (G > 1) {
@@ -269,12 +277,19 @@ hipError_t launch_splitk_reduce(const float* part, float* dw, int nsplit, int K,
                                 hipStream_t stream)
 {
     const int64_t n4 = (int64_t)K * RS * C / 4;
-    // one thread per output while that gives at least two blocks per CU,
-    // else 16 threads per output (each summing a sixteenth of the splits)
-    if (n4 >= 2 * 256 * 256 || nsplit < 32)
-        splitk_reduce_kernel<1><<<(unsigned)((n4 + 255) / 256), 256, 0, stream>>>(part, dw, nsplit, K, RS, C, krsc);
-    else
-        splitk_reduce_kernel<16><<<(unsigned)((n4 + 15) / 16), 256, 0, stream>>>(part, dw, nsplit, K, RS, C, krsc);
+    // G threads per output (each summing a consecutive 1/G of the splits),
+    // G the smallest power of two that gives about 2^19 threads (every CU
+    // full), at most 16 and at most nsplit
+    int G = 1;
+    while (G < 16 && 2 * G <= nsplit && n4 * G < (1 << 19)) G *= 2;
+    const unsigned blocks = (unsigned)((n4 * G + 255) / 256);
+    switch (G) {
+    case 1: splitk_reduce_kernel<1><<<blocks, 256, 0, stream>>>(part, dw, nsplit, K, RS, C, krsc); break;
+    case 2: splitk_reduce_kernel<2><<<blocks, 256, 0, stream>>>(part, dw, nsplit, K, RS, C, krsc); break;
+    case 4: splitk_reduce_kernel<4><<<blocks, 256, 0, stream>>>(part, dw, nsplit, K, RS, C, krsc); break;
+    case 8: splitk_reduce_kernel<8><<<blocks, 256, 0, stream>>>(part, dw, nsplit, K, RS, C, krsc); break;
+    default: splitk_reduce_kernel<16><<<blocks, 256, 0, stream>>>(part, dw, nsplit, K, RS, C, krsc); break;
+    }
     return hipGetLastError();
 }
 
