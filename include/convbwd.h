@@ -209,6 +209,15 @@ int conv_bwd_data_elementwise(const cbw_conv_desc* desc, const void* dY, const v
 int cbw_read_pixel_counts(const cbw_conv_desc* desc, const void* workspace, size_t workspace_bytes,
                           int32_t* counts, int64_t* total, void* stream);
 
+/* After a weight-gradient call on `workspace` (either entry point): the
+ * number of blocks each work item executed, in item order z*ntiles + tile
+ * (split z of tile ((tap group * channel tiles + channel tile) * k tiles +
+ * k tile)).  With skipping, the live blocks of every tile are shared out in
+ * equal ceil(live / nsplit) parts (work redistribution, Sec. IV-F).
+ * `work` (nullable) receives nsplit*ntiles int32; waits for `stream`. */
+int cbw_read_weight_work(const cbw_conv_desc* desc, const void* workspace, size_t workspace_bytes, int32_t* work,
+                         int32_t* nsplit, int32_t* ntiles, void* stream);
+
 /* Copy the statistics of the last `op` call that used `workspace` to the host
  * (waits for `stream`). */
 int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, size_t workspace_bytes,

@@ -28,7 +28,7 @@ CBW_FLAG_NO_SKIP = 1
 EXPORTS = ("cbw_status_string", "cbw_validate_desc", "cbw_mask_words", "cbw_dy_mask_words",
            "cbw_workspace_size", "cbw_relu_mask_pack", "cbw_nonzero_mask_pack", "conv_bwd_data",
            "conv_bwd_data_masked", "conv_fwd_relu_mask", "conv_bwd_weight_sparse", "conv_bwd_weight_sparse_x",
-           "conv_bwd_data_elementwise", "cbw_read_pixel_counts", "cbw_read_stats",
+           "conv_bwd_data_elementwise", "cbw_read_pixel_counts", "cbw_read_weight_work", "cbw_read_stats",
            "cbw_read_live_lists",
            "cbw_read_occupancy", "cbw_set_profile_events")
 
@@ -94,6 +94,7 @@ def lib():
     L.conv_bwd_weight_sparse_x.argtypes = [dp, vp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
     L.conv_bwd_data_elementwise.argtypes = [dp, vp, vp, vp, vp, vp, sz, vp]
     L.cbw_read_pixel_counts.argtypes = [dp, vp, sz, vp, ctypes.POINTER(ctypes.c_int64), vp]
+    L.cbw_read_weight_work.argtypes = [dp, vp, sz, vp, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), vp]
     L.cbw_read_stats.argtypes = [dp, ctypes.c_int, vp, sz, ctypes.POINTER(Stats), vp]
     i32p = ctypes.POINTER(ctypes.c_int32)
     L.cbw_read_live_lists.argtypes = [dp, vp, sz, ctypes.c_int, vp, i32p, i32p, vp]
@@ -218,6 +219,18 @@ def cbw_read_pixel_counts(desc, ws, stream=None):
                                        out.ctypes.data_as(ctypes.c_void_p), ctypes.byref(tot), _stream(stream)),
            "cbw_read_pixel_counts")
     return out, tot.value
+
+
+def cbw_read_weight_work(desc, ws, stream=None):
+    """Blocks executed per weight-gradient work item: numpy int32 [nsplit][ntiles]."""
+    import numpy as np
+    ns, nt = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(lib().cbw_read_weight_work(ctypes.byref(desc), _ptr(ws), _nbytes(ws), None, ctypes.byref(ns),
+                                      ctypes.byref(nt), _stream(stream)), "cbw_read_weight_work")
+    out = np.zeros((ns.value, nt.value), np.int32)
+    _check(lib().cbw_read_weight_work(ctypes.byref(desc), _ptr(ws), _nbytes(ws), out.ctypes.data_as(ctypes.c_void_p),
+                                      ctypes.byref(ns), ctypes.byref(nt), _stream(stream)), "cbw_read_weight_work")
+    return out
 
 
 def cbw_read_stats(desc, op, ws, stream=None):

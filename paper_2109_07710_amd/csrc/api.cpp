@@ -291,6 +291,7 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
         return CBW_ERR_UNSUPPORTED;
     if ((st = check_ws(workspace, workspace_bytes, plan.total)) != CBW_OK) return st;
     if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;
+    if (x_skip && plan.tgroups * plan.ctiles > 1024) return CBW_ERR_UNSUPPORTED;   // liveness flags per chunk
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool skip = !(flags & CBW_FLAG_NO_SKIP);
     hipError_t e;
@@ -308,14 +309,28 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
         op.nchunks = plan.nchunks;
         op.dtype = desc->dtype;
         if (x_skip) {
-            op.x = X;
-            op.xbits = x_mask;
-            op.xocc = at<uint8_t>(workspace, plan.xocc);
-            op.npix_x = desc->N * desc->H * desc->W;
-            op.C = desc->C;
-            op.xct = weight_tile_channels();
-            op.xctiles = plan.ctiles;
-            op.xpb = (op.npix_x + plan.nchunks - 1) / plan.nchunks;
+            // the X-window liveness is read from a packed footprint of X: the
+            // caller's, or one packed here from X's non-zeros
+            const uint32_t* xbits = x_mask;
+            if (!xbits) {
+                uint32_t* packed = at<uint32_t>(workspace, plan.xbits);
+                const int64_t count = (int64_t)desc->N * desc->H * desc->W * desc->C;
+                if ((e = launch_relu_mask_pack(desc->dtype, count, X, packed, 0, s)) != hipSuccess)
+                    return hip_status(e);
+                xbits = packed;
+            }
+            op.xbits = xbits;
+            op.xlive = at<uint8_t>(workspace, plan.xlive);
+            op.N = desc->N; op.H = desc->H; op.W = desc->W; op.C = desc->C; op.P = desc->P; op.Q = desc->Q;
+            op.S = desc->S; op.RS = desc->R * desc->S;
+            op.stride_h = desc->stride_h; op.stride_w = desc->stride_w;
+            op.pad_h = desc->pad_h; op.pad_w = desc->pad_w;
+            op.tpg = plan.tpg;
+            op.tgroups = plan.tgroups;
+            op.ctiles = plan.ctiles;
+            op.ctw = plan.tpg > 1 ? desc->C : weight_tile_channels();
+            op.div_q = make_fastdiv((uint32_t)desc->Q);
+            op.div_p = make_fastdiv((uint32_t)desc->P);
         }
         if ((e = launch_occupancy(op, s)) != hipSuccess) return hip_status(e);
     }
@@ -324,7 +339,8 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
     p.dy = dY;
     p.out = plan.direct ? dW : at<float>(workspace, plan.partials);
     p.occ = skip ? occ : nullptr;
-    p.xocc = skip && x_skip ? at<uint8_t>(workspace, plan.xocc) : nullptr;
+    p.xlive = skip && x_skip ? at<uint8_t>(workspace, plan.xlive) : nullptr;
+    p.work_slots = at<int32_t>(workspace, plan.work_slots);
     p.skip_slots = at<int32_t>(workspace, plan.skip_slots);
     p.header = at<int>(workspace, plan.header);
     p.N = desc->N; p.H = desc->H; p.W = desc->W; p.C = desc->C; p.K = desc->K; p.R = desc->R; p.S = desc->S;
@@ -415,6 +431,24 @@ int conv_bwd_weight_sparse_x(const cbw_conv_desc* desc, const void* X, const voi
                              uint32_t flags, void* stream)
 {
     return run_weight(desc, X, dY, x_mask, dy_mask, true, dW, workspace, workspace_bytes, flags, stream);
+}
+
+int cbw_read_weight_work(const cbw_conv_desc* desc, const void* workspace, size_t workspace_bytes, int32_t* work,
+                         int32_t* nsplit, int32_t* ntiles, void* stream)
+{
+    WeightPlan plan;
+    int st = plan_weight(desc, &plan);
+    if (st != CBW_OK) return st;
+    if (!workspace || !nsplit || !ntiles) return CBW_ERR_INVALID_ARG;
+    if (workspace_bytes < plan.total) return CBW_ERR_WORKSPACE;
+    *nsplit = plan.nsplit;
+    *ntiles = plan.grid / plan.nsplit;
+    if (!work) return CBW_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(work, at<int32_t>(const_cast<void*>(workspace), plan.work_slots),
+                                  (size_t)plan.grid * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    return hip_status(e);
 }
 
 int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, size_t workspace_bytes,

@@ -39,54 +39,179 @@ constexpr int FM = TM / 16, FN = TN / 16;
 constexpr int CH = 8;           // 16-byte chunks per LDS row (128 bytes)
 constexpr int OCC_WIN = 1024;   // occupancy bytes cached per workgroup
 
-// X-operand liveness of chunks [ch_begin, ch_begin + nwin) for a tile over
-// filter taps [tap0, tap0 + ntaps) and channel tile ct: chunk i is live when
-// one of its dY pixels has, at one of those taps, an X pixel inside the image
-// whose channel tile holds a non-zero (xocc).  A chunk that is not live
-// multiplies an all-zero X operand, so skipping it changes no sum.  Every
-// writer stores 1, so concurrent stores to one byte agree.  Called by the
-// whole workgroup.
-__device__ void x_liveness(const WeightParams& p, int ch_begin, int nwin, int chunk_px, int tap0, int ntaps,
-                           int ct, uint8_t* xlive)
+// The chunk range [begin, end) of split z of a weight-gradient tile, with the
+// liveness of its first OCC_WIN chunks cached in live_s.
+//
+// Without skipping the splits are equal ranges of chunks.  With skipping a
+// chunk is live when its dY block holds a non-zero (occ) and, when X blocks
+// are skipped too, its tap-shifted X window does (xlive).  Work
+// redistribution (Sec. IV-F): the tile's live chunks are ranked in chunk
+// order and split z takes the ranks [z*share, (z+1)*share), share =
+// ceil(live / nsplit), so no workgroup executes more than share blocks,
+// however the dead blocks cluster.  The ranges still partition all chunks
+// (a dead chunk goes with the live one after it), so skip counts stay exact;
+// and when every chunk is live they are the unskipped ranges, which keeps
+// the two results bitwise equal.
+//
+// Tiles of up to TILE_LIVE_CAP chunks stage their liveness in LDS in one
+// coalesced pass (four loads in flight per thread) that also decides the
+// all-live case; each thread then counts a contiguous segment of it from LDS
+// (a bit mask for segments of up to 32 chunks).  Larger tiles read their
+// segments from global memory.  The ranks come from a wave-level shuffle
+// scan and one exchange of wave totals.  Called by the whole workgroup before
+// any operand copy; scratch is SPLIT_SCRATCH_BYTES of LDS, free until the
+// function returns.
+constexpr int TILE_LIVE_CAP = 16384;
+constexpr int SPLIT_SCRATCH_BYTES = 256 + TILE_LIVE_CAP;
+
+__device__ void split_range(const WeightParams& p, int kt, int combo, int z, int& begin, int& end,
+                            uint8_t* live_s, uint8_t* scratch)
 {
-    constexpr int U = 4;   // pixels per thread per round, their loads issued together
-    const int tap_end = min(tap0 + ntaps, p.R * p.S);
-    for (int i = threadIdx.x; i < nwin; i += blockDim.x) xlive[i] = 0;
-    __syncthreads();
-    const int total = nwin * chunk_px;
-    for (int base = threadIdx.x; base < total; base += blockDim.x * U) {
-        int ci[U], nn[U], pp[U], qq[U];
-        bool ok[U];
+    const int nch = p.nchunks, T = blockDim.x, tid = threadIdx.x;
+    if (p.occ == nullptr) {
+        begin = min(nch, z * p.chunks_per_split);
+        end = min(nch, begin + p.chunks_per_split);
+        return;
+    }
+    const int ncombo = p.tgroups * p.ctiles;
+    auto live = [&](int c) -> int {
+        int v = p.occ[(int64_t)c * p.ktiles + kt];
+        if (p.xlive) v &= p.xlive[(int64_t)c * ncombo + combo];
+        return v != 0;
+    };
+    int* wsum = reinterpret_cast<int*>(scratch);         // [0, 16): wave totals
+    int* pos = wsum + 32;                                // [32, 34): chunk of ranks r0, r1
+    uint8_t* tl = scratch + 256;                         // tile liveness when staged
+    const bool staged = nch <= TILE_LIVE_CAP;
+    const int per = (nch + T - 1) / T;
+    const int s0 = min(nch, tid * per), s1 = min(nch, s0 + per);
+    int cnt = 0;
+    uint32_t bits = 0;   // bit i: chunk s0 + i is live (segments of up to 32 chunks)
+    bool all = true;
+    if (staged) {
+        for (int cb = tid; cb < nch; cb += 4 * T) {
+            int v[4];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int idx = base + u * (int)blockDim.x;
-            ci[u] = idx / chunk_px;
-            const int pix = (ch_begin + ci[u]) * chunk_px + (idx - ci[u] * chunk_px);
-            ok[u] = idx < total && pix < p.npq;
-            const uint32_t px = ok[u] ? (uint32_t)pix : 0u;
-            const uint32_t nq = fdiv(px, p.div_q);
-            qq[u] = (int)px - (int)nq * p.Q;
-            const uint32_t n = fdiv(nq, p.div_p);
-            pp[u] = (int)nq - (int)n * p.P;
-            nn[u] = (int)n;
-        }
-        uint32_t any = 0;   // bit u: pixel u sees a non-zero X
-        for (int tap = tap0; tap < tap_end; ++tap) {
-            const int r = tap / p.S, s = tap - r * p.S;
+            for (int u = 0; u < 4; ++u) v[u] = cb + u * T < nch ? live(cb + u * T) : 1;
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int h = pp[u] * p.stride_h - p.pad_h + r, w = qq[u] * p.stride_w - p.pad_w + s;
-                const bool in = ok[u] && h >= 0 && h < p.H && w >= 0 && w < p.W;
-                const int64_t a = in ? ((int64_t)(nn[u] * p.H + h) * p.W + w) * p.ctiles + ct : 0;
-                const uint8_t v = in ? p.xocc[a] : (uint8_t)0;
-                any |= (uint32_t)(v != 0) << u;
+            for (int u = 0; u < 4; ++u) {
+                if (cb + u * T < nch) tl[cb + u * T] = (uint8_t)v[u];
+                all &= v[u] != 0;
             }
         }
+    } else {
+        for (int c = s0; c < s1; ++c) {
+            const int v = live(c);
+            cnt += v;
+            bits |= (uint32_t)v << ((c - s0) & 31);
+        }
+        all = cnt == s1 - s0;
+    }
+    // every chunk live (the usual case for element-wise footprints): the
+    // ranges are the unskipped ones and nothing needs ranking
+    if (__syncthreads_and(all)) {
+        begin = min(nch, z * p.chunks_per_split);
+        end = min(nch, begin + p.chunks_per_split);
+        const int n = min(OCC_WIN, max(end - begin, 0));
+        for (int i = tid; i < n; i += T) live_s[i] = 1;
+        __syncthreads();
+        return;
+    }
+    if (staged) {
+        for (int c = s0; c < s1; ++c) {
+            const int v = tl[c];
+            cnt += v;
+            bits |= (uint32_t)v << ((c - s0) & 31);
+        }
+    }
+    // otherwise an inclusive scan of the counts over the threads: within
+    // each wave by shuffles, then across the waves' totals
+    const int lane = tid & 63, wave = tid >> 6, nw = T >> 6;
+    int incl = cnt;
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-            if ((any >> u) & 1u) xlive[ci[u]] = 1;
+    for (int off = 1; off < 64; off <<= 1) {
+        const int v = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += v;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    if (tid == 0) {
+        pos[0] = nch;
+        pos[1] = nch;
     }
     __syncthreads();
+    int total = 0;
+    for (int w = 0; w < nw; ++w) {
+        const int v = wsum[w];
+        if (w < wave) incl += v;
+        total += v;
+    }
+    const int excl = incl - cnt;
+    const int share = (total + p.nsplit - 1) / p.nsplit;
+    const int r0 = min(z * share, total), r1 = min(r0 + share, total);
+    // chunk index of ranks r0 and r1 (nch past the last live chunk), found by
+    // the thread whose segment holds the rank
+    for (int q = 0; q < 2; ++q) {
+        const int r = q == 0 ? r0 : r1;
+        if (r < total && excl <= r && r < incl) {
+            int k = excl;
+            for (int c = s0; c < s1; ++c) {
+                if (!(per <= 32 ? (int)((bits >> (c - s0)) & 1u) : live(c))) continue;
+                if (k == r) {
+                    pos[q] = c;
+                    break;
+                }
+                ++k;
+            }
+        }
+    }
+    __syncthreads();
+    // the bounds are the same for the whole workgroup: keep them scalar so the
+    // chunk loop and its addressing stay on the scalar unit
+    begin = __builtin_amdgcn_readfirstlane(z == 0 ? 0 : pos[0]);
+    end = __builtin_amdgcn_readfirstlane(z == p.nsplit - 1 ? nch : pos[1]);
+    const int n = min(OCC_WIN, max(end - begin, 0));
+    for (int i = tid; i < n; i += T) {
+        const int c = begin + i;
+        live_s[i] = staged ? tl[c] : (uint8_t)live(c);
+    }
+    __syncthreads();
+}
+// The first live chunk in [chunk, end) (end when there is none), counting the
+// dead chunks passed in skipped.  Each lane tests one of 64 consecutive
+// chunks and the wave's ballot names the first live one, so a long run of
+// dead chunks (a balanced range can open with one) costs one probe per 64
+// chunks instead of one per chunk.  Liveness of the first OCC_WIN chunks of
+// the range comes from live_s, later ones from the global bytes.  Called in
+// uniform control flow; every result is the same for the whole workgroup.
+__device__ __forceinline__ int next_live_chunk(const WeightParams& p, const uint8_t* live_s, int begin, int end,
+                                               int kt, int combo, int chunk, int& skipped)
+{
+    if (p.occ == nullptr) return chunk;
+    const int lane = threadIdx.x & 63, ncombo = p.tgroups * p.ctiles;
+    if (chunk < end && chunk - begin < OCC_WIN &&
+        __builtin_amdgcn_readfirstlane((int)live_s[chunk - begin]) != 0)
+        return chunk;   // the common case: the next chunk is live
+    for (; chunk < end; chunk += 64) {
+        const int c = chunk + lane;
+        int v = 0;
+        if (c < end) {
+            const int i = c - begin;
+            if (i < OCC_WIN) {
+                v = live_s[i];
+            } else {
+                v = p.occ[(int64_t)c * p.ktiles + kt];
+                if (p.xlive) v &= p.xlive[(int64_t)c * ncombo + combo];
+            }
+        }
+        const uint64_t m = __ballot(v != 0);
+        if (m != 0) {
+            const int f = __builtin_ctzll(m);
+            skipped += f;
+            return chunk + f;
+        }
+        skipped += min(64, end - chunk);
+    }
+    return end;
 }
 static_assert(BM == BN, "both operands share the staging layout");
 
@@ -160,8 +285,6 @@ __global__ __launch_bounds__(NT) void bwd_weight_kernel(WeightParams p)
 
     if (blockIdx.x == 0 && tid == 0) p.header[0] = p.mode_flags;
 
-    const int ch_begin = z * p.chunks_per_split;
-    const int ch_end = min(p.nchunks, ch_begin + p.chunks_per_split);
 
     floatx4 acc[FM][FN];
 #pragma unroll
@@ -256,30 +379,17 @@ __global__ __launch_bounds__(NT) void bwd_weight_kernel(WeightParams p)
         }
     };
 
-    // The occupancy bytes of this workgroup's chunk range are read once into
-    // LDS (up to OCC_WIN of them); the loop then tests them without a global
-    // read on its critical path.
-    __shared__ uint8_t occ_s[OCC_WIN];
-    __shared__ uint8_t xlive_s[OCC_WIN];
-    if (p.occ) {
-        for (int i = tid; i < OCC_WIN && ch_begin + i < ch_end; i += NT)
-            occ_s[i] = p.occ[(int64_t)(ch_begin + i) * p.ktiles + kt];
-    }
-    __syncthreads();
-    // Blocks whose X operand is entirely zero are skipped as well when the X
-    // occupancy is given (chunks past the cached window count as X-live).
-    const int nwin = min(OCC_WIN, max(ch_end - ch_begin, 0));
-    if (p.xocc) x_liveness(p, ch_begin, nwin, BK, tap, 1, ct, xlive_s);
-    auto live = [&](int chunk) {
-        if (p.occ == nullptr) return true;
-        const int i = chunk - ch_begin;
-        int v = i < OCC_WIN ? occ_s[i] : p.occ[(int64_t)chunk * p.ktiles + kt];
-        if (p.xocc && i < OCC_WIN) v &= xlive_s[i];
-        return __builtin_amdgcn_readfirstlane(v) != 0;  // the same byte for the whole workgroup
-    };
+    // This split's chunk range (balanced over the tile's live chunks when
+    // skipping), with the liveness of its first OCC_WIN chunks read once into
+    // LDS so the loop tests them without a global read on its critical path.
+    // The ranking scratch borrows the second operand buffer, not yet in use.
+    __shared__ uint8_t live_s[OCC_WIN];
+    const int combo = tap * p.ctiles + ct;
+    int ch_begin, ch_end;
+    static_assert(sizeof(As[1]) >= SPLIT_SCRATCH_BYTES, "ranking scratch fits the second operand buffer");
+    split_range(p, kt, combo, z, ch_begin, ch_end, live_s, reinterpret_cast<uint8_t*>(As[1]));
     auto next_live = [&](int chunk) {
-        while (chunk < ch_end && !live(chunk)) { ++chunk; ++skipped; }
-        return chunk;
+        return next_live_chunk(p, live_s, ch_begin, ch_end, kt, combo, chunk, skipped);
     };
 
     int chunk = next_live(ch_begin);
@@ -299,7 +409,10 @@ __global__ __launch_bounds__(NT) void bwd_weight_kernel(WeightParams p)
         chunk = next;
     }
 
-    if (tid == 0) p.skip_slots[blockIdx.x] = skipped;
+    if (tid == 0) {
+        p.skip_slots[blockIdx.x] = skipped;
+        p.work_slots[t] = ch_end - ch_begin - skipped;
+    }
 
     // Epilogue: lane holds channels c0 + wm*TM + i*16 + 4*(lane/16) + v of
     // output channel k0 + wn*TN + j*16 + lane%16; written to [z][k][tap][c].
@@ -393,8 +506,6 @@ __global__ __launch_bounds__(TR_NT) void bwd_weight_tr_kernel(WeightParams p)
 
     if (blockIdx.x == 0 && tid == 0) p.header[0] = p.mode_flags;
 
-    const int ch_begin = z * p.chunks_per_split;
-    const int ch_end = min(p.nchunks, ch_begin + p.chunks_per_split);
 
     const u32x4_t rs_x = make_rsrc_words(p.x, p.x_bytes);
     const u32x4_t rs_dy = make_rsrc_words(p.dy, p.dy_bytes);
@@ -489,31 +600,18 @@ __global__ __launch_bounds__(TR_NT) void bwd_weight_tr_kernel(WeightParams p)
         }
     };
 
-    // The occupancy bytes of this workgroup's chunk range are read once into
-    // LDS (up to OCC_WIN of them); the loop then tests them without a global
-    // read on its critical path.
-    __shared__ uint8_t occ_s[OCC_WIN];
-    __shared__ uint8_t xlive_s[OCC_WIN];
-    if (p.occ) {
-        for (int i = tid; i < OCC_WIN && ch_begin + i < ch_end; i += TR_NT)
-            occ_s[i] = p.occ[(int64_t)(ch_begin + i) * p.ktiles + kt];
-    }
-    __syncthreads();
-    // Blocks whose X operand is entirely zero are skipped as well when the X
-    // occupancy is given (chunks past the cached window count as X-live).
-    const int nwin = min(OCC_WIN, max(ch_end - ch_begin, 0));
-    if (p.xocc) x_liveness(p, ch_begin, nwin, TR_BK, tg * p.tpg, p.tpg, ct, xlive_s);
-    auto live = [&](int chunk) {
-        if (p.occ == nullptr) return true;
-        const int i = chunk - ch_begin;
-        int v = i < OCC_WIN ? occ_s[i] : p.occ[(int64_t)chunk * p.ktiles + kt];
-        if (p.xocc && i < OCC_WIN) v &= xlive_s[i];
-        return __builtin_amdgcn_readfirstlane(v) != 0;  // the same byte for the whole workgroup
-    };
+    // This split's chunk range (balanced over the tile's live chunks when
+    // skipping), with the liveness of its first OCC_WIN chunks read once into
+    // LDS so the loop tests them without a global read on its critical path.
+    // The ranking scratch borrows the second operand buffer, not yet in use.
+    __shared__ uint8_t live_s[OCC_WIN];
+    const int combo = tg * p.ctiles + ct;
+    int ch_begin, ch_end;
+    static_assert(sizeof(As[1]) >= SPLIT_SCRATCH_BYTES, "ranking scratch fits the second operand buffer");
+    split_range(p, kt, combo, z, ch_begin, ch_end, live_s, reinterpret_cast<uint8_t*>(As[1]));
     int skipped = 0;
     auto next_live = [&](int chunk) {
-        while (chunk < ch_end && !live(chunk)) { ++chunk; ++skipped; }
-        return chunk;
+        return next_live_chunk(p, live_s, ch_begin, ch_end, kt, combo, chunk, skipped);
     };
 
     int chunk = next_live(ch_begin);
@@ -537,7 +635,10 @@ __global__ __launch_bounds__(TR_NT) void bwd_weight_tr_kernel(WeightParams p)
         chunk = next;
     }
 
-    if (tid == 0) p.skip_slots[blockIdx.x] = skipped;
+    if (tid == 0) {
+        p.skip_slots[blockIdx.x] = skipped;
+        p.work_slots[t] = ch_end - ch_begin - skipped;
+    }
 
     // Buffer stores over this split's [K][RS][C] region: lanes past K, C or
     // the last tap get offset kOOB and their stores are dropped (no branches).

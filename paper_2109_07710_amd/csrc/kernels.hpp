@@ -48,8 +48,9 @@ struct WeightParams {
     const void* dy;          // [N*P*Q][K]
     float* out;              // [nsplit][K][R*S][C] partials, or dW (KRSC) when nsplit == 1
     const uint8_t* occ;      // [nchunks][ktiles] block occupancy, or null (no skipping)
-    const uint8_t* xocc;     // [N*H*W][ctiles] X pixel occupancy, or null (no X-block skipping)
+    const uint8_t* xlive;    // [nchunks][tgroups*ctiles] X-window liveness, or null (no X-block skipping)
     int32_t* skip_slots;     // [grid] skipped-block count per workgroup
+    int32_t* work_slots;     // [grid] executed blocks per work item (item order)
     int* header;
     int N, H, W, C, K, R, S, P, Q;
     int stride_h, stride_w, pad_h, pad_w;
@@ -70,13 +71,14 @@ struct OccParams {
     const uint32_t* bits;    // packed dY footprint, or null
     uint8_t* occ;            // [nchunks][ktiles]
     int npq, K, chunk, BNk, ktiles, nchunks, dtype;
-    // X pixel occupancy (only when xocc is set): xocc[px][ct] for X pixels
-    // px < npix_x and channel tiles of xct channels; block b covers X pixels
-    // [b*xpb, (b+1)*xpb).
-    const void* x;           // values [npix_x][C] (used when xbits == null)
-    const uint32_t* xbits;   // packed X footprint, or null
-    uint8_t* xocc;
-    int npix_x, C, xct, xctiles, xpb;
+    // X-window liveness (only when xlive is set): xlive[chunk][tg*ctiles+ct]
+    // = 1 iff a pixel of the chunk has, at one of tap group tg's taps, an X
+    // pixel inside the image with a non-zero among channel tile ct's channels.
+    const uint32_t* xbits;   // packed X footprint (a superset of X's non-zeros)
+    uint8_t* xlive;
+    int N, H, W, C, P, Q, S, RS, stride_h, stride_w, pad_h, pad_w;
+    int tpg, tgroups, ctiles, ctw;   // taps per group, groups, channel tiles, channels per tile
+    FastDiv div_q, div_p;
 };
 
 // Per-element data gradient on the vector ALUs (bf16, NHWC, KRSC filters).

@@ -153,27 +153,48 @@ __global__ __launch_bounds__(256) void occupancy_kernel(OccParams p)
     for (int i = threadIdx.x; i < p.ktiles; i += blockDim.x)
         p.occ[(int64_t)chunk * p.ktiles + i] = (uint8_t)(flags[i] != 0);
 
-    // X occupancy: xocc[px][ct] = 1 iff X pixel px has a non-zero among
-    // channels [ct*xct, min(C, ct*xct + xct)) (packed footprint when given).
-    if (p.xocc) {
-        const int pairs = p.xpb * p.xctiles;
-        const int E = p.dtype == 1 ? 8 : 4;
+    // X-window liveness for every (tap group, channel tile) of the weight
+    // gradient's tiling: 1 iff some pixel of this chunk has, at one of the
+    // group's taps, an X pixel inside the image with a non-zero among the
+    // tile's channels (from the packed X footprint).
+    if (p.xlive) {
+        __shared__ int xflags[1024];
+        const int ncombo = p.tgroups * p.ctiles;
+        for (int i = threadIdx.x; i < ncombo; i += blockDim.x) xflags[i] = 0;
+        __syncthreads();
+        const int pairs = ncombo * npx;
         for (int i = threadIdx.x; i < pairs; i += blockDim.x) {
-            const int64_t px = (int64_t)chunk * p.xpb + i / p.xctiles;
-            const int ct = i % p.xctiles;
-            if (px >= p.npix_x) continue;
-            const int lo = ct * p.xct, hi = min(p.C, lo + p.xct);
+            const int combo = i / npx, j = i - combo * npx;
+            const int tg = combo / p.ctiles, ct = combo - tg * p.ctiles;
+            const uint32_t pix = (uint32_t)(px0 + j);
+            const uint32_t nq = fdiv(pix, p.div_q);
+            const int qq = (int)pix - (int)nq * p.Q;
+            const uint32_t nn = fdiv(nq, p.div_p);
+            const int pp = (int)nq - (int)nn * p.P;
+            const int lo = ct * p.ctw, hi = min(p.C, lo + p.ctw);
+            // whole 256-channel tiles on 128-bit boundaries: two vector loads
+            const bool vec = hi - lo == 256 && (p.C & 127) == 0;
             bool any = false;
-            if (p.xbits) {
-                any = any_bits(p.xbits, px * p.C + lo, px * p.C + hi);
-            } else {
-                const uint4* v4 = reinterpret_cast<const uint4*>(static_cast<const char*>(p.x) +
-                                                                 (px * p.C + lo) * (p.dtype == 1 ? 2 : 4));
-                for (int v = 0; v < (hi - lo) / E && !any; ++v)
-                    any = (p.dtype == 1 ? vec_bits<uint16_t>(v4[v], false) : vec_bits<float>(v4[v], false)) != 0;
+            for (int tl = 0; tl < p.tpg && !any; ++tl) {
+                const int tap = tg * p.tpg + tl;
+                if (tap >= p.RS) break;
+                const int r = tap / p.S, s = tap - r * p.S;
+                const int h = pp * p.stride_h - p.pad_h + r, w = qq * p.stride_w - p.pad_w + s;
+                if (h < 0 || h >= p.H || w < 0 || w >= p.W) continue;
+                const int64_t base = (((int64_t)nn * p.H + h) * p.W + w) * p.C;
+                if (vec) {
+                    const uint4* v = reinterpret_cast<const uint4*>(p.xbits + ((base + lo) >> 5));
+                    const uint4 a = v[0], b = v[1];
+                    any = ((a.x | a.y | a.z | a.w) | (b.x | b.y | b.z | b.w)) != 0;
+                } else {
+                    any = any_bits(p.xbits, base + lo, base + hi);
+                }
             }
-            p.xocc[px * p.xctiles + ct] = (uint8_t)any;
+            if (any) xflags[combo] = 1;   // every writer stores 1
         }
+        __syncthreads();
+        for (int i = threadIdx.x; i < ncombo; i += blockDim.x)
+            p.xlive[(int64_t)chunk * ncombo + i] = (uint8_t)(xflags[i] != 0);
     }
 }
 

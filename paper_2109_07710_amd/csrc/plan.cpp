@@ -157,8 +157,10 @@ int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
     size_t cur = 0;
     p.header = take(&cur, 256);
     p.occ = take(&cur, (size_t)p.nchunks * p.ktiles);
-    p.xocc = take(&cur, (size_t)d->N * d->H * d->W * p.ctiles);
+    p.xlive = take(&cur, (size_t)p.nchunks * p.tgroups * p.ctiles);
+    p.xbits = take(&cur, ((size_t)d->N * d->H * d->W * d->C + 31) / 32 * 4);
     p.skip_slots = take(&cur, (size_t)p.grid * 4);
+    p.work_slots = take(&cur, (size_t)p.grid * 4);
     if (!p.direct) p.partials = take(&cur, (size_t)p.nsplit * d->K * d->R * d->S * d->C * 4);
     p.total = cur;
     *out = p;

@@ -63,7 +63,7 @@ struct WeightPlan {
     int cg = 0;                         // channel columns per packed tap (C, or 256 without packing)
     int nchunks = 0, ctiles = 0, ktiles = 0, nsplit = 0, chunks_per_split = 0, grid = 0;
     bool direct = false;  // partial of the single split is dW itself
-    Region header, occ, xocc, skip_slots, partials;
+    Region header, occ, xlive, xbits, skip_slots, work_slots, partials;
     size_t total = 0;
 };
 

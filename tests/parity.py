@@ -93,6 +93,19 @@ def oracle_backward(spec, t, masked=None):
     return res
 
 
+def check_dw_regrouped(a, b, skipped, what):
+    """Two weight gradients of the same inputs: bitwise equal when no block was
+    skipped (same split ranges, same summation order); otherwise the skipping
+    run's splits cover the live blocks in balanced ranges, so its fp32 sums are
+    grouped differently and agree to fp32 reassociation (normwise 1e-5)."""
+    if skipped == 0:
+        assert torch.equal(a, b), what + ": differs without any skipped block"
+        return 0.0
+    err = (a.double() - b.double()).abs().max().item() / max(b.double().abs().max().item(), 1e-30)
+    assert err <= 1e-5, "%s: normwise %.3e" % (what, err)
+    return err
+
+
 def dx_as_nchw(dx):
     return oracle.nhwc_to_nchw(dx.float().cpu().double().numpy())
 

@@ -14,8 +14,8 @@ import torch
 import oracle
 import paper_2109_07710_amd as cb
 import workloads as wl
-from parity import (check_layer, check_values, check_zero_pattern, desc_of, dw_as_kcrs, dx_as_nchw,
-                    dx_bits_nchw, gpu_backward, oracle_backward, oracle_inputs, to_dev, tol_for)
+from parity import (check_dw_regrouped, check_layer, check_values, check_zero_pattern, desc_of, dw_as_kcrs,
+                    dx_as_nchw, dx_bits_nchw, gpu_backward, oracle_backward, oracle_inputs, to_dev, tol_for)
 
 pytestmark = pytest.mark.gpu
 
@@ -146,7 +146,8 @@ def test_masked_equals_dense_times_mask_bitwise():
     assert np.array_equal(bm[mask], bd[mask])
     assert np.array_equal(bm, bs)
     assert np.all(bm[~mask] == 0)
-    assert torch.equal(g_m["dw"], g_s["dw"])
+    sk = cb.cbw_read_stats(g_m["desc"], cb.CBW_OP_BWD_WEIGHT, g_m["ws_dw"]).blocks_skipped
+    check_dw_regrouped(g_m["dw"], g_s["dw"], sk, "dW")
 
 
 def test_run_twice_bitwise_deterministic():
@@ -226,11 +227,65 @@ def test_occupancy_and_block_skip(use_bits):
     st = cb.cbw_read_stats(gpu["desc"], cb.CBW_OP_BWD_WEIGHT, gpu["ws_dw"])
     tiles = spec.R * spec.S          # C = 256: one tap per tile, one channel tile
     assert st.blocks_total == ref.size * tiles and st.blocks_skipped == int((ref == 0).sum()) * tiles > 0
+    # work redistribution: tile t (k tile t % ktiles) executes each live block
+    # once, no split more than ceil(live / nsplit)
+    work = cb.cbw_read_weight_work(gpu["desc"], gpu["ws_dw"])
+    nsplit, ntiles = work.shape
+    live_t = np.array([int(ref[:, t % ref.shape[1]].sum()) for t in range(ntiles)])
+    assert np.array_equal(work.sum(axis=0), live_t)
+    assert np.array_equal(work.max(axis=0), -(-live_t // nsplit))
     ref_full = oracle_backward(spec, t)
     check_values(dw_as_kcrs(gpu["dw"]), ref_full["dw"], ref_full["dw_abs"], ref_full["dw_n"], tol_for("bf16"),
                  False, "dW with skipped blocks")
     g2 = gpu_backward(spec, t, flags=cb.CBW_FLAG_NO_SKIP)
-    assert torch.equal(gpu["dw"], g2["dw"])
+    check_dw_regrouped(gpu["dw"], g2["dw"], st.blocks_skipped, "dW with skipped blocks")
+
+
+@pytest.mark.parametrize("pattern", ["last_image_live", "first_image_live", "odd_images_live"])
+def test_balanced_split_long_dead_runs(pattern):
+    """Configuration 2's layer with dY zero over whole images: runs of dead
+    chunks far longer than one split (and than the cached liveness window of
+    1024 chunks) open or close the balanced ranges.  Each tile's live blocks
+    are executed once, shared so no split runs more than ceil(live / nsplit);
+    dW agrees with the unskipped run and, at sampled entries, the oracle."""
+    spec = wl.config2()[0]
+    _case("balanced split " + pattern)
+    t = wl.draw(spec)
+    dy = t["dy"].clone()
+    keep = {"last_image_live": [spec.N - 1], "first_image_live": [0],
+            "odd_images_live": list(range(1, spec.N, 2))}[pattern]
+    dead = torch.ones(spec.N, dtype=torch.bool)
+    dead[keep] = False
+    dy[dead] = 0
+    t["dy"] = dy
+    gpu = gpu_backward(spec, t, dy_mask=True)
+    desc = gpu["desc"]
+    occ, chunk, kw = cb.cbw_read_occupancy(desc, gpu["ws_dw"])
+    npq = spec.N * spec.P * spec.Q
+    ref = oracle.block_occupancy(dy.view(npq, spec.K).float().numpy(), chunk, kw)
+    assert np.array_equal(occ, ref)
+    work = cb.cbw_read_weight_work(desc, gpu["ws_dw"])
+    nsplit, ntiles = work.shape
+    live_t = np.array([int(ref[:, j % ref.shape[1]].sum()) for j in range(ntiles)])
+    assert np.array_equal(work.sum(axis=0), live_t)
+    assert np.array_equal(work.max(axis=0), -(-live_t // nsplit))
+    if pattern != "odd_images_live":      # a dead run longer than the cached window
+        assert occ.shape[0] - live_t.max() > 1024
+    st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, gpu["ws_dw"])
+    assert st.blocks_skipped == int((ref == 0).sum()) * (ntiles // ref.shape[1])
+    g2 = gpu_backward(spec, t, flags=cb.CBW_FLAG_NO_SKIP)
+    check_dw_regrouped(gpu["dw"], g2["dw"], st.blocks_skipped, "balanced dW against no skipping")
+    # sampled entries against the oracle over the live images only (dead
+    # images contribute exact zeros)
+    sub = {k: t[k][keep] if k != "w" else t[k] for k in ("x", "w", "dy")}
+    x64, _, dy64 = oracle_inputs(sub)
+    rng = np.random.default_rng(5)
+    m = 1500
+    co = np.stack([rng.integers(0, spec.K, m), rng.integers(0, spec.C, m), rng.integers(0, 3, m),
+                   rng.integers(0, 3, m)], 1).astype(np.int32)
+    o, a, nt = oracle.conv_bwd_weight_at(x64, dy64, (3, 3), co, (1, 1), (1, 1))
+    g = gpu["dw"].cpu().numpy()[co[:, 0], co[:, 2], co[:, 3], co[:, 1]].astype(np.float64)
+    check_values(g, o, a, nt, tol_for("bf16"), False, "balanced dW (sampled)")
 
 
 def _x_skip_case(N, C, H, W, K, R, S, stride, pad, dtype, seed):
@@ -279,6 +334,7 @@ def test_x_block_skip(case, use_bits):
     dw = torch.empty((K, R, S, C), dtype=torch.float32, device="cuda")
     cb.conv_bwd_weight_sparse_x(desc, d["x"], d["dy"], xm, dym, dw, ws)
     st_x = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws)
+    work_x = cb.cbw_read_weight_work(desc, ws)
     occ, chunk, kw = cb.cbw_read_occupancy(desc, ws)
     dw_y = torch.empty_like(dw)
     cb.conv_bwd_weight_sparse(desc, d["x"], d["dy"], dym, dw_y, ws)
@@ -296,13 +352,20 @@ def test_x_block_skip(case, use_bits):
     live_y = oracle.weight_block_liveness(np.ones_like(x64, bool), dy64 != 0, (R, S), (st, st), (pd, pd),
                                           chunk, kw, ctile, tpg)
     assert st_x.blocks_total == live.size == st_y.blocks_total
+    # work redistribution: every tile's live blocks are executed exactly once,
+    # shared so that no split runs more than ceil(live / nsplit) of them
+    nsplit, ntiles = work_x.shape
+    per_tile = live.reshape(ntiles, -1).sum(axis=1)          # tiles in (group, channel tile, k tile) order
+    assert np.array_equal(work_x.sum(axis=0), per_tile)
+    assert np.array_equal(work_x.max(axis=0), -(-per_tile // nsplit))
     assert st_x.blocks_skipped == int((~live).sum())
     assert st_y.blocks_skipped == int((~live_y).sum()) > 0
     if (C, st) in ((256, 1), (64, 1), (32, 1)):   # cases where the zero band empties whole X windows
         assert st_x.blocks_skipped > st_y.blocks_skipped
     ref_dw, ref_abs, ref_n = oracle.conv_bwd_weight(x64, dy64, (R, S), (st, st), (pd, pd), with_bound=True)
     check_values(dw_as_kcrs(dw), ref_dw, ref_abs, ref_n, tol_for(dt), False, "dW with X-block skipping")
-    assert torch.equal(dw, dw_n) and torch.equal(dw, dw_y)
+    check_dw_regrouped(dw, dw_n, st_x.blocks_skipped, "X-skipping dW against no skipping")
+    check_dw_regrouped(dw_y, dw_n, st_y.blocks_skipped, "dY-skipping dW against no skipping")
 
 
 def test_guard_bands_untouched():
