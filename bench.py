@@ -317,8 +317,10 @@ def layer_timing(cb, torch, spec, steps, warmup):
         ms_d = min(ms_d, tm(dense))
     sparse_x()
     st_x = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws_w)
+    work_x = cb.cbw_read_weight_work(desc, ws_w)
     sparse()
     torch.cuda.synchronize()
+    work = cb.cbw_read_weight_work(desc, ws_w)
     rec = {"layer": spec.name, "N": spec.N, "C": spec.C, "K": spec.K, "H": spec.H, "W": spec.W, "R": spec.R,
            "masked_dx": bool(spec.need_dx and spec.masked), "need_dx": bool(spec.need_dx),
            "x_density": round(float((x > 0).float().mean().item()), 4),
@@ -336,11 +338,21 @@ def layer_timing(cb, torch, spec, steps, warmup):
         rec["dx_rows_executed"] = round(st.rows_live / st.rows_total, 4)
     st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws_w)
     rec["dw_blocks_executed"] = round(1.0 - st.blocks_skipped / max(st.blocks_total, 1), 4)
+    rec["dw_split_balance"] = split_balance(work)
     # the variant whose weight gradient also skips all-zero X blocks
     rec["sparse_x_ms"] = round(ms_x, 4)
     rec["speedup_x_vs_dense"] = round(ms_d / ms_x, 4)
     rec["dw_blocks_executed_x"] = round(1.0 - st_x.blocks_skipped / max(st_x.blocks_total, 1), 4)
+    rec["dw_split_balance_x"] = split_balance(work_x)
     return rec
+
+
+def split_balance(work):
+    """Executed weight-gradient blocks over what the busiest split of each
+    tile bounds (nsplit x its maximum), summed over the tiles: 1.0 when every
+    split of a tile executes the same number of blocks."""
+    cap = int(work.max(axis=0).sum()) * work.shape[0]
+    return round(int(work.sum()) / cap, 4) if cap else 1.0
 
 
 def elementwise_sweep(args):
