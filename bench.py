@@ -205,6 +205,68 @@ def main():
     ms_fwd, _ = timed(fwd, args.steps)
     del y_fwd, ym_fwd, ws_f
 
+    # Per-step distribution, hot (operands left in the caches by the step
+    # before) and cold (the 256 MB last-level cache flushed by writing 512 MB
+    # before every step), each step bracketed by its own events.
+    log("per-step distribution, hot and cold")
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+
+    def distribution(cold, n=max(10, min(args.steps, 40))):
+        per = []
+        for i in range(n):
+            if cold:
+                flush.fill_(i & 0xFF)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            sparse_step()
+            b.record(stream)
+            torch.cuda.synchronize()
+            per.append(a.elapsed_time(b))
+        q = np.percentile(per, [10, 50, 90])
+        return {"p10_ms": round(float(q[0]), 4), "median_ms": round(float(q[1]), 4),
+                "p90_ms": round(float(q[2]), 4), "steps": n}
+
+    dist = {"hot": distribution(False), "cold": distribution(True)}
+    del flush
+
+    # The semantic equivalent without output sparsity: the dense step followed
+    # by a separate multiply of dX with the 0/1 ReLU derivative.
+    relu_d = (x > 0).to(x.dtype)
+
+    def dense_mask_step():
+        dense_dx()
+        dx.mul_(relu_d)
+        dense_dw()
+
+    for _ in range(10):
+        dense_mask_step()
+    ms_dense_mask, _ = timed(dense_mask_step, args.steps)
+    del relu_d
+
+    # NCHW callers: the same step through the library's boundary transposes
+    # (activations and footprints in NCHW order), timed apart from the path.
+    log("timing %d sparse steps with NCHW tensors" % args.steps)
+    desc_n = cb.ConvDesc.make(spec.N, spec.C, spec.H, spec.W, spec.K, spec.R, spec.S, spec.stride, spec.pad,
+                              act_layout="nchw")
+    x_n = x.permute(0, 3, 1, 2).contiguous()
+    dy_n = dy.permute(0, 3, 1, 2).contiguous()
+    dx_n = torch.empty_like(x_n)
+    xm_n = torch.empty(cb.cbw_mask_words(desc_n), dtype=torch.int32, device=dev)
+    dym_n = torch.empty(cb.cbw_dy_mask_words(desc_n), dtype=torch.int32, device=dev)
+    cb.cbw_relu_mask_pack(desc_n, x_n, xm_n)
+    cb.cbw_nonzero_mask_pack(desc_n.dtype, dy_n.numel(), dy_n, dym_n)
+    ws_mn = cb.workspace(desc_n, cb.CBW_OP_BWD_DATA_MASKED, dev)
+    ws_wn = cb.workspace(desc_n, cb.CBW_OP_BWD_WEIGHT, dev)
+
+    def sparse_step_nchw():
+        cb.conv_bwd_data_masked(desc_n, dy_n, w, xm_n, dx_n, ws_mn, 0)
+        cb.conv_bwd_weight_sparse(desc_n, x_n, dy_n, dym_n, dw, ws_wn, 0)
+
+    for _ in range(20):
+        sparse_step_nchw()
+    ms_nchw, _ = timed(sparse_step_nchw, args.steps)
+    del x_n, dy_n, dx_n, xm_n, dym_n, ws_mn, ws_wn
+
     if args.copy_calibration:
         a = torch.ones(64 << 20, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
@@ -242,6 +304,11 @@ def main():
         "executed_tflops": round(f_exec / (ms_sparse * 1e-3) / 1e12, 2),
         "kernels_ms": {"dx_gemm": round(ms_dx_gemm, 4), "dw_gemm": round(ms_dw_gemm, 4),
                        "step_with_events": round(ms_sparse_k, 4)},
+        "step_distribution": dist,
+        "dense_plus_mask_multiply_ms": round(ms_dense_mask, 4),
+        "speedup_vs_dense_plus_mask_multiply": round(ms_dense_mask / ms_sparse, 4),
+        "nchw_boundary": {"sparse_step_ms": round(ms_nchw, 4), "added_ms": round(ms_nchw - ms_sparse, 4),
+                          "note": "NCHW activations through the boundary transposes; NHWC is native"},
         "mask_pack_ms": round(ms_pack, 4),
         "forward_relu_mask": {"ms": round(ms_fwd, 4), "tflops": round(f_conv / (ms_fwd * 1e-3) / 1e12, 2)},
         "flops": {"dx_dense": f_conv, "dw_dense": f_conv, "dx_useful": f_useful_dx, "dw_useful": f_useful_dw},
@@ -501,8 +568,22 @@ def cpu_baseline(spec, t, budget_s):
         done += 1
     flops = 2 * spec.dense_flops() * done / spec.N
     return {"value": round(flops / el / 1e12, 6), "unit": "TFLOP/s (dense-equivalent)",
-            "cores": oracle.num_threads(), "kind": "oracle",
+            "cores": oracle.num_threads(), "kind": "oracle", "cpu": cpu_model(),
+            "gmac_per_s": round(flops / 2 / el / 1e9, 3),
             "sample": "%d of %d images of the same layer (masked dX + dW, fp64), %.1f s" % (done, spec.N, el)}
+
+
+def cpu_model():
+    """The host CPU's model name (Linux), or the platform's processor string."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 if __name__ == "__main__":

@@ -62,7 +62,14 @@ typedef enum {
 
 /* Activation layout of X, dX, Y, dY.  Channel-innermost (NHWC) is the native
  * one: the paper stores neurons "channel first" and indexes non-zeros through
- * the channel dimension 32 at a time (Sec. IV-B). */
+ * the channel dimension 32 at a time (Sec. IV-B).  NCHW is accepted by
+ * conv_bwd_data, conv_bwd_data_masked, conv_bwd_weight_sparse and
+ * conv_bwd_weight_sparse_x: the library transposes the activations (and
+ * reorders footprint bits) into NHWC copies in the workspace, runs the NHWC
+ * path there and transposes dX back, so an NCHW call adds HBM-bound copies
+ * and a larger workspace.  The forward and the per-element data gradient
+ * return CBW_ERR_UNSUPPORTED for NCHW.  Footprint bitmaps are always in the
+ * caller's layout (bit i = element i of the tensor as the caller stores it). */
 typedef enum { CBW_NCHW = 0, CBW_NHWC = 1 } cbw_act_layout;
 /* Filter layout of W and dW. */
 typedef enum { CBW_KCRS = 0, CBW_KRSC = 1 } cbw_w_layout;
@@ -74,7 +81,7 @@ typedef struct {
     int32_t K, R, S;         /* output channels (the paper's M), filter size   */
     int32_t P, Q;            /* output height, width; must equal the formula   */
     int32_t stride_h, stride_w, pad_h, pad_w;
-    int32_t act_layout;      /* cbw_act_layout; only CBW_NHWC is implemented   */
+    int32_t act_layout;      /* cbw_act_layout; NCHW for the backward calls    */
     int32_t w_layout;        /* cbw_w_layout; both implemented                 */
     int32_t dtype;           /* cbw_dtype                                      */
 } cbw_conv_desc;
@@ -115,7 +122,7 @@ int cbw_workspace_size(const cbw_conv_desc* desc, int op, size_t* bytes);
 /* ReLU footprint bitmap of X (Sec. III-B boxed derivative, read as the ReLU
  * output footprint: live iff X > 0; Sec. IV-B: the output bitmap the forward
  * pass leaves in memory for the backward pass).  Bit i of word i/32 (LSB
- * first) is element i of X in X's own linear (NHWC) order; trailing bits of
+ * first) is element i of X in X's own linear order; trailing bits of
  * the last word are 0.  x_mask: cbw_mask_words(desc) words. */
 int cbw_relu_mask_pack(const cbw_conv_desc* desc, const void* X, uint32_t* x_mask, void* stream);
 
@@ -126,7 +133,8 @@ int cbw_nonzero_mask_pack(int32_t dtype, int64_t count, const void* t, uint32_t*
 
 /* Dense data gradient (Sec. IV-B, the backward pass as the forward operation
  * with M and C interchanged): dX[N,H,W,C] from dY[N,P,Q,K] and W (KRSC or
- * KCRS).  Workspace: cbw_workspace_size(desc, CBW_OP_BWD_DATA). */
+ * KCRS); dX[N,C,H,W] from dY[N,K,P,Q] for NCHW.
+ * Workspace: cbw_workspace_size(desc, CBW_OP_BWD_DATA). */
 int conv_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, void* dX,
                   void* workspace, size_t workspace_bytes, void* stream);
 
@@ -158,7 +166,7 @@ int conv_fwd_relu_mask(const cbw_conv_desc* desc, const void* X, const void* W, 
 
 /* Weight gradient with input sparsity (Sec. III-B; weight-gradient phase of
  * Sec. IV-B): dW (float32, layout desc->w_layout) from X[N,H,W,C] and
- * dY[N,P,Q,K].  Blocks of (pixel chunk x output-channel tile) in which dY is
+ * dY[N,P,Q,K] (NCHW: X[N,C,H,W], dY[N,K,P,Q]).  Blocks of (pixel chunk x output-channel tile) in which dY is
  * entirely zero are skipped; the skipped products are exactly zero.  dy_mask
  * (nullable) is a packed dY footprint (cbw_nonzero_mask_pack or the next
  * layer's ReLU bitmap, any superset of dY's non-zeros; 16-byte aligned);

@@ -16,7 +16,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libconvbwd.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["api.cpp", "plan.cpp", "bwd_data.hip", "bwd_weight.hip", "mask_kernels.hip", "elementwise.hip"]
+SOURCES = ["api.cpp", "plan.cpp", "bwd_data.hip", "bwd_weight.hip", "mask_kernels.hip", "elementwise.hip", "layout.hip"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result"]
 DEVICE = ["-x", "hip", "--offload-arch=gfx950",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

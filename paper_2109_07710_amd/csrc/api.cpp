@@ -91,6 +91,23 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
 
     const bool gather = masked && !(flags & CBW_FLAG_NO_SKIP);
     const int mode = !masked ? MODE_DENSE : (gather ? MODE_GATHER : MODE_SELECT);
+    hipError_t e;
+    void* dX_out = dX;
+    if (desc->act_layout == CBW_NCHW) {
+        // the kernels read an NHWC copy of dY (and an NHWC-order footprint)
+        // and write an NHWC dX, transposed into the caller's dX at the end
+        void* tdy = at<void>(ws, plan.t_dy);
+        if ((e = launch_transpose(desc->dtype, dY, tdy, desc->N, desc->K, desc->P * desc->Q, s)) != hipSuccess)
+            return hip_status(e);
+        dY = tdy;
+        dX = at<void>(ws, plan.t_dx);
+        if (masked) {
+            uint32_t* t = at<uint32_t>(ws, plan.t_mask);
+            if ((e = launch_bits_nchw_to_nhwc(x_mask, t, desc->N, desc->C, desc->H * desc->W, s)) != hipSuccess)
+                return hip_status(e);
+            x_mask = t;
+        }
+    }
     int* header = at<int>(ws, plan.header);
     void* wt = at<void>(ws, plan.wt);
     DataParams p = data_params(desc, dY, wt, dX, plan.npix, plan.groups);
@@ -117,11 +134,14 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
         p.lists = cp.lists;
         p.counts = cp.counts;
     }
-    hipError_t e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S,
-                                    desc->w_layout == CBW_KRSC, header, mode, gather ? &cp : nullptr, s);
+    e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S, desc->w_layout == CBW_KRSC,
+                         header, mode, gather ? &cp : nullptr, s);
     if (e != hipSuccess) return hip_status(e);
     if (gather && (e = launch_compact_scatter(cp, s)) != hipSuccess) return hip_status(e);
-    return hip_status(launch_bwd_data(desc->dtype, mode, p, s, prof_events(0)));
+    if ((e = launch_bwd_data(desc->dtype, mode, p, s, prof_events(0))) != hipSuccess) return hip_status(e);
+    if (dX != dX_out)
+        e = launch_transpose(desc->dtype, dX, dX_out, desc->N, desc->H * desc->W, desc->C, s);
+    return hip_status(e);
 }
 
 int run_fwd(const cbw_conv_desc* desc, const void* X, const void* W, void* Y, uint32_t* y_mask, void* ws,
@@ -194,7 +214,7 @@ size_t cbw_dy_mask_words(const cbw_conv_desc* d)
 // Descriptors the per-element data gradient supports.
 static int validate_elementwise(const cbw_conv_desc* d)
 {
-    const int st = validate_desc(d);
+    const int st = require_nhwc(d);
     if (st != CBW_OK) return st;
     if (d->dtype != CBW_BF16 || d->w_layout != CBW_KRSC) return CBW_ERR_UNSUPPORTED;
     if (d->C != 64 && d->C != 128 && d->C != 256 && d->C != 512) return CBW_ERR_UNSUPPORTED;
@@ -295,6 +315,28 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool skip = !(flags & CBW_FLAG_NO_SKIP);
     hipError_t e;
+    if (desc->act_layout == CBW_NCHW) {
+        // the kernels read NHWC copies of X and dY (and NHWC-order footprints)
+        void* tx = at<void>(workspace, plan.t_x);
+        void* tdy = at<void>(workspace, plan.t_dy);
+        if ((e = launch_transpose(desc->dtype, X, tx, desc->N, desc->C, desc->H * desc->W, s)) != hipSuccess ||
+            (e = launch_transpose(desc->dtype, dY, tdy, desc->N, desc->K, desc->P * desc->Q, s)) != hipSuccess)
+            return hip_status(e);
+        X = tx;
+        dY = tdy;
+        if (skip && dy_mask) {
+            uint32_t* t = at<uint32_t>(workspace, plan.t_dymask);
+            if ((e = launch_bits_nchw_to_nhwc(dy_mask, t, desc->N, desc->K, desc->P * desc->Q, s)) != hipSuccess)
+                return hip_status(e);
+            dy_mask = t;
+        }
+        if (skip && x_skip && x_mask) {
+            uint32_t* t = at<uint32_t>(workspace, plan.xbits);
+            if ((e = launch_bits_nchw_to_nhwc(x_mask, t, desc->N, desc->C, desc->H * desc->W, s)) != hipSuccess)
+                return hip_status(e);
+            x_mask = t;
+        }
+    }
     uint8_t* occ = at<uint8_t>(workspace, plan.occ);
     if (skip) {
         OccParams op{};

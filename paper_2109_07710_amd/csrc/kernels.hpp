@@ -118,6 +118,11 @@ hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t
 hipError_t launch_fwd_prep(int dtype, const void* w, void* wt, int K, int C, int R, int S, int krsc, int* header,
                            uint32_t* zero, int64_t zero_words, hipStream_t stream);
 hipError_t launch_compact_scatter(const CompactParams& p, hipStream_t stream);
+// Boundary layout conversion (NCHW callers): dst[b][c][r] = src[b][r][c] for
+// `batch` matrices of rows x cols elements, and footprint bits in NCHW
+// element order reordered to NHWC element order.
+hipError_t launch_transpose(int dtype, const void* src, void* dst, int batch, int rows, int cols, hipStream_t s);
+hipError_t launch_bits_nchw_to_nhwc(const uint32_t* src, uint32_t* dst, int N, int C, int HW, hipStream_t s);
 hipError_t launch_relu_mask_pack(int dtype, int64_t count, const void* x, uint32_t* bits, int relu,
                                  hipStream_t stream);
 hipError_t launch_occupancy(const OccParams& p, hipStream_t stream);

@@ -33,7 +33,6 @@ int validate_desc(const cbw_conv_desc* d)
     if (d->dtype != CBW_F32 && d->dtype != CBW_BF16) return CBW_ERR_INVALID_ARG;
     if (d->act_layout != CBW_NHWC && d->act_layout != CBW_NCHW) return CBW_ERR_INVALID_ARG;
     if (d->w_layout != CBW_KRSC && d->w_layout != CBW_KCRS) return CBW_ERR_INVALID_ARG;
-    if (d->act_layout != CBW_NHWC) return CBW_ERR_UNSUPPORTED;
     const int E = d->dtype == CBW_BF16 ? 8 : 4;
     if (d->C % E != 0 || d->K % E != 0) return CBW_ERR_UNSUPPORTED;
     const int64_t npix = (int64_t)d->N * d->H * d->W, npq = (int64_t)d->N * d->P * d->Q;
@@ -45,6 +44,13 @@ int validate_desc(const cbw_conv_desc* d)
     if ((int64_t)d->K * d->C * d->R * d->S * 4 >= kMaxElems) return CBW_ERR_UNSUPPORTED;
     if (d->K > 1024 * kWeightTileK) return CBW_ERR_UNSUPPORTED;  // occupancy flags per chunk
     return CBW_OK;
+}
+
+int require_nhwc(const cbw_conv_desc* d)
+{
+    const int st = validate_desc(d);
+    if (st != CBW_OK) return st;
+    return d->act_layout == CBW_NHWC ? CBW_OK : CBW_ERR_UNSUPPORTED;
 }
 
 int data_tile_index(int C)
@@ -91,6 +97,11 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out)
     const size_t tile_bytes = (size_t)p.bn * p.bm * 4;
     if (masked) p.partial = take(&cur, (size_t)kDataSlots * tile_bytes);
     else if (p.split > 1) p.partial = take(&cur, (size_t)p.ptiles * p.groups * p.split * tile_bytes);
+    if (d->act_layout == CBW_NCHW) {
+        p.t_dy = take(&cur, (size_t)d->N * d->P * d->Q * d->K * elem_bytes(d->dtype));
+        p.t_dx = take(&cur, (size_t)p.npix * d->C * elem_bytes(d->dtype));
+        if (masked) p.t_mask = take(&cur, ((size_t)p.npix * d->C + 31) / 32 * 4);
+    }
     p.total = cur;
     *out = p;
     return CBW_OK;
@@ -98,7 +109,7 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out)
 
 int fwd_as_data_desc(const cbw_conv_desc* d, cbw_conv_desc* out)
 {
-    int st = validate_desc(d);
+    int st = require_nhwc(d);
     if (st != CBW_OK) return st;
     if (d->stride_h != 1 || d->stride_w != 1) return CBW_ERR_UNSUPPORTED;
     if (d->pad_h > d->R - 1 || d->pad_w > d->S - 1) return CBW_ERR_UNSUPPORTED;
@@ -162,6 +173,11 @@ int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
     p.skip_slots = take(&cur, (size_t)p.grid * 4);
     p.work_slots = take(&cur, (size_t)p.grid * 4);
     if (!p.direct) p.partials = take(&cur, (size_t)p.nsplit * d->K * d->R * d->S * d->C * 4);
+    if (d->act_layout == CBW_NCHW) {
+        p.t_x = take(&cur, (size_t)d->N * d->H * d->W * d->C * elem_bytes(d->dtype));
+        p.t_dy = take(&cur, (size_t)p.npq * d->K * elem_bytes(d->dtype));
+        p.t_dymask = take(&cur, ((size_t)p.npq * d->K + 31) / 32 * 4);
+    }
     p.total = cur;
     *out = p;
     return CBW_OK;

@@ -34,6 +34,9 @@ struct DataPlan {
     int ptiles = 0, nsteps = 0;
     int split = 1;          // dense / select: host-chosen reduction split
     Region header, wt, blk_counts, counts, lists, partial;
+    // NCHW callers: NHWC copies of dY and dX and the NHWC-order footprint,
+    // after every other region (the other offsets do not depend on layout)
+    Region t_dy, t_dx, t_mask;
     size_t total = 0;
 };
 
@@ -64,10 +67,17 @@ struct WeightPlan {
     int nchunks = 0, ctiles = 0, ktiles = 0, nsplit = 0, chunks_per_split = 0, grid = 0;
     bool direct = false;  // partial of the single split is dW itself
     Region header, occ, xlive, xbits, skip_slots, work_slots, partials;
+    // NCHW callers: NHWC copies of X and dY and the NHWC-order dY footprint
+    // (a caller's X footprint is reordered into xbits), after every other region
+    Region t_x, t_dy, t_dymask;
     size_t total = 0;
 };
 
+// Accepts NHWC and NCHW activations (NCHW is served through the boundary
+// transposes of the three backward operations); require_nhwc() is for the
+// operations that run on NHWC only.
 int validate_desc(const cbw_conv_desc* d);
+int require_nhwc(const cbw_conv_desc* d);
 int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out);
 int plan_weight(const cbw_conv_desc* d, WeightPlan* out);
 // The forward convolution as a data-gradient GEMM: for stride 1, Y = conv(X, W)

@@ -67,7 +67,7 @@ def test_validation_codes(L):
     assert cb.cbw_validate_desc(d) == cb.CBW_ERR_INVALID_ARG
     assert cb.cbw_validate_desc(_desc(C=12)) == cb.CBW_ERR_UNSUPPORTED           # not a multiple of 8 (bf16)
     assert cb.cbw_validate_desc(_desc(C=12, K=8, dtype="f32")) == cb.CBW_OK     # multiple of 4 (fp32)
-    assert cb.cbw_validate_desc(_desc(act_layout="nchw")) == cb.CBW_ERR_UNSUPPORTED
+    assert cb.cbw_validate_desc(_desc(act_layout="nchw")) == cb.CBW_OK
     assert cb.cbw_validate_desc(_desc(w_layout="kcrs")) == cb.CBW_OK
     assert cb.cbw_validate_desc(_desc(N=4096, H=1024, W=1024, C=8)) == cb.CBW_ERR_UNSUPPORTED  # >= 2^31 elems
     # the fp32 weight gradient must stay below 2^31 bytes: 7680^2*9*4 fits, 8192^2*9*4 does not
@@ -176,3 +176,33 @@ def test_null_arguments_rejected_without_gpu(L):
         cb.CBW_ERR_WORKSPACE
     misaligned = ctypes.c_void_p((1 << 20) + 2)
     assert L.conv_bwd_data(ctypes.byref(d), misaligned, fake, fake, None, 0, None) == cb.CBW_ERR_UNSUPPORTED
+
+
+def _ws(d, op):
+    n = ctypes.c_size_t(0)
+    st = cb.lib().cbw_workspace_size(ctypes.byref(d), op, ctypes.byref(n))
+    return st, n.value
+
+
+def test_nchw_workspace_and_scope(L):
+    """NCHW callers of the three backward operations get NHWC copies of their
+    activations (and NHWC-order footprints) after every NHWC region: the
+    workspace grows by exactly those buffers, 256-byte aligned; the forward
+    and the per-element data gradient refuse NCHW."""
+    al = lambda b: (b + 255) // 256 * 256
+    a = cb.ConvDesc.make(4, 64, 10, 12, 32, 3, 3, 1, 1)
+    b = cb.ConvDesc.make(4, 64, 10, 12, 32, 3, 3, 1, 1, act_layout="nchw")
+    act_x, act_y = 4 * 10 * 12 * 64 * 2, 4 * 10 * 12 * 32 * 2
+    bits_x, bits_y = (4 * 10 * 12 * 64 + 31) // 32 * 4, (4 * 10 * 12 * 32 + 31) // 32 * 4
+    st, nh = _ws(a, cb.CBW_OP_BWD_DATA)
+    st2, nc = _ws(b, cb.CBW_OP_BWD_DATA)
+    assert st == st2 == cb.CBW_OK and nc == nh + al(act_y) + al(act_x)
+    st, nh = _ws(a, cb.CBW_OP_BWD_DATA_MASKED)
+    st2, nc = _ws(b, cb.CBW_OP_BWD_DATA_MASKED)
+    assert st == st2 == cb.CBW_OK and nc == nh + al(act_y) + al(act_x) + al(bits_x)
+    st, nh = _ws(a, cb.CBW_OP_BWD_WEIGHT)
+    st2, nc = _ws(b, cb.CBW_OP_BWD_WEIGHT)
+    assert st == st2 == cb.CBW_OK and nc == nh + al(act_x) + al(act_y) + al(bits_y)
+    assert _ws(b, cb.CBW_OP_FWD)[0] == cb.CBW_ERR_UNSUPPORTED
+    e = cb.ConvDesc.make(4, 64, 10, 12, 64, 3, 3, 1, 1, act_layout="nchw")
+    assert _ws(e, cb.CBW_OP_BWD_DATA_ELEMENTWISE)[0] == cb.CBW_ERR_UNSUPPORTED
