@@ -41,6 +41,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--no-miopen", action="store_true", help="skip the torch (MIOpen) context timing")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU baseline time budget")
     ap.add_argument("--sweep", choices=["config4", "config3", "config5", "config5_pooled", "elementwise"], default=None,
                     help="instead of the main line, time the sparse and dense steps over a workload set "
@@ -267,6 +268,26 @@ def main():
     ms_nchw, _ = timed(sparse_step_nchw, args.steps)
     del x_n, dy_n, dx_n, xm_n, dym_n, ws_mn, ws_wn
 
+    # Context only: the same dense backward through torch's convolution
+    # backward (MIOpen), on the same tensors viewed as channels-last NCHW.
+    miopen = None
+    if not args.no_miopen:
+        log("timing the dense backward through torch (MIOpen), context only")
+        try:
+            xv, wv, dyv = x.permute(0, 3, 1, 2), w.permute(0, 3, 1, 2), dy.permute(0, 3, 1, 2)
+
+            def miopen_bwd():
+                torch.ops.aten.convolution_backward(dyv, xv, wv, None, [spec.stride] * 2, [spec.pad] * 2, [1, 1],
+                                                    False, [0, 0], 1, [True, True, False])
+
+            for _ in range(10):
+                miopen_bwd()
+            ms_mi, _ = timed(miopen_bwd, max(10, args.steps // 2))
+            miopen = {"dense_dx_dw_ms": round(ms_mi, 4), "our_dense_step_speedup": round(ms_mi / ms_dense, 3),
+                      "layout": "channels-last bf16", "call": "torch.ops.aten.convolution_backward"}
+        except Exception as exc:  # context only: a failure there does not void the measurement
+            miopen = {"error": str(exc)[:200]}
+
     if args.copy_calibration:
         a = torch.ones(64 << 20, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
@@ -309,6 +330,7 @@ def main():
         "speedup_vs_dense_plus_mask_multiply": round(ms_dense_mask / ms_sparse, 4),
         "nchw_boundary": {"sparse_step_ms": round(ms_nchw, 4), "added_ms": round(ms_nchw - ms_sparse, 4),
                           "note": "NCHW activations through the boundary transposes; NHWC is native"},
+        "miopen_context": miopen,
         "mask_pack_ms": round(ms_pack, 4),
         "forward_relu_mask": {"ms": round(ms_fwd, 4), "tflops": round(f_conv / (ms_fwd * 1e-3) / 1e12, 2)},
         "flops": {"dx_dense": f_conv, "dw_dense": f_conv, "dx_useful": f_useful_dx, "dw_useful": f_useful_dw},
