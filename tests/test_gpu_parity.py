@@ -288,6 +288,50 @@ def test_balanced_split_long_dead_runs(pattern):
     check_values(g, o, a, nt, tol_for("bf16"), False, "balanced dW (sampled)")
 
 
+@pytest.mark.parametrize("pattern", ["last_image_live", "odd_images_live"])
+def test_balanced_split_past_staged_tile(pattern):
+    """Configuration 2's layer at N = 336: 16464 chunks, more than a tile
+    stages in LDS (16384), so the ranking reads its segments from global
+    memory.  dY is zero over whole images; the occupancy, the per-tile work
+    and dW (against the unskipped run) are checked as for the smaller
+    batch.  A chunk is live exactly when it holds a pixel of a live image
+    (a live image's 64 x 256 dY blocks are never all zero at density 0.4)."""
+    spec = wl.config2(N=336)[0]
+    _case("balanced split past the staged tile, " + pattern)
+    d = wl.draw_on_device(spec)
+    keep = [spec.N - 1] if pattern == "last_image_live" else list(range(1, spec.N, 2))
+    dead = torch.ones(spec.N, dtype=torch.bool, device="cuda")
+    dead[keep] = False
+    d["dy"][dead] = 0
+    desc = desc_of(spec)
+    dym = torch.zeros(cb.cbw_dy_mask_words(desc), dtype=torch.int32, device="cuda")
+    cb.cbw_nonzero_mask_pack(desc.dtype, d["dy"].numel(), d["dy"], dym)
+    ws = cb.workspace(desc, cb.CBW_OP_BWD_WEIGHT)
+    dw = torch.empty((spec.K, spec.R, spec.S, spec.C), dtype=torch.float32, device="cuda")
+    cb.conv_bwd_weight_sparse(desc, d["x"], d["dy"], dym, dw, ws)
+    occ, chunk, kw = cb.cbw_read_occupancy(desc, ws)
+    work = cb.cbw_read_weight_work(desc, ws)
+    st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws)
+    dw_n = torch.empty_like(dw)
+    cb.conv_bwd_weight_sparse(desc, d["x"], d["dy"], dym, dw_n, ws, cb.CBW_FLAG_NO_SKIP)
+    torch.cuda.synchronize()
+    nch = occ.shape[0]
+    assert nch > 16384
+    ppi = spec.P * spec.Q
+    live_img = np.zeros(spec.N, bool)
+    live_img[keep] = True
+    first = np.arange(nch) * chunk // ppi
+    last = np.minimum(np.arange(nch) * chunk + chunk, spec.N * ppi) - 1
+    expect = np.array([live_img[a:b + 1].any() for a, b in zip(first, last // ppi)])
+    assert np.array_equal(occ.astype(bool), np.repeat(expect[:, None], occ.shape[1], axis=1))
+    nsplit, ntiles = work.shape
+    live_t = np.full(ntiles, int(expect.sum()))
+    assert np.array_equal(work.sum(axis=0), live_t)
+    assert np.array_equal(work.max(axis=0), -(-live_t // nsplit))
+    assert st.blocks_skipped == int((~expect).sum()) * ntiles
+    check_dw_regrouped(dw, dw_n, st.blocks_skipped, "balanced dW past the staged tile against no skipping")
+
+
 def _x_skip_case(N, C, H, W, K, R, S, stride, pad, dtype, seed):
     """Inputs with whole zero regions in both operands: X dead over a band of
     rows of every image and over the upper channel tile of a few pixels, dY
