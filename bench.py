@@ -41,7 +41,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
-    ap.add_argument("--no-miopen", action="store_true", help="skip the torch (MIOpen) context timing")
+    ap.add_argument("--no-context", action="store_true",
+                    help="skip the context timings through torch (MIOpen convolution, hipBLASLt GEMMs)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU baseline time budget")
     ap.add_argument("--sweep", choices=["config4", "config3", "config5", "config5_pooled", "elementwise"], default=None,
                     help="instead of the main line, time the sparse and dense steps over a workload set "
@@ -270,8 +271,8 @@ def main():
 
     # Context only: the same dense backward through torch's convolution
     # backward (MIOpen), on the same tensors viewed as channels-last NCHW.
-    miopen = None
-    if not args.no_miopen:
+    miopen = gemm_ctx = None
+    if not args.no_context:
         log("timing the dense backward through torch (MIOpen), context only")
         try:
             xv, wv, dyv = x.permute(0, 3, 1, 2), w.permute(0, 3, 1, 2), dy.permute(0, 3, 1, 2)
@@ -287,6 +288,30 @@ def main():
                       "layout": "channels-last bf16", "call": "torch.ops.aten.convolution_backward"}
         except Exception as exc:  # context only: a failure there does not void the measurement
             miopen = {"error": str(exc)[:200]}
+        # Context only: plain library GEMMs (hipBLASLt through torch.matmul) of
+        # the two gradients' GEMM shapes with the same FLOP count (no im2col,
+        # no footprint), and a large square one, the practical matrix-core
+        # rate of the library on this GPU.
+        log("timing plain library GEMMs, context only")
+        try:
+            gemm_ctx = {}
+            npq, crs = spec.N * desc.P * desc.Q, spec.C * spec.R * spec.S
+            for name, (m, k, n) in (("dx_shape", (npq, spec.K * spec.R * spec.S, spec.C)),
+                                    ("dw_shape", (spec.K, npq, crs)), ("square_8192", (8192, 8192, 8192))):
+                a_m = torch.randn(m, k, device=dev).to(torch.bfloat16)
+                b_m = torch.randn(k, n, device=dev).to(torch.bfloat16)
+
+                def mm():
+                    torch.matmul(a_m, b_m)
+
+                for _ in range(10):
+                    mm()
+                ms_mm, _ = timed(mm, 20)
+                gemm_ctx[name] = {"mnk": [m, n, k], "ms": round(ms_mm, 4),
+                                  "tflops": round(2 * m * n * k / (ms_mm * 1e-3) / 1e12, 1)}
+                del a_m, b_m
+        except Exception as exc:
+            gemm_ctx = {"error": str(exc)[:200]}
 
     if args.copy_calibration:
         a = torch.ones(64 << 20, dtype=torch.float32, device=dev)
@@ -331,6 +356,7 @@ def main():
         "nchw_boundary": {"sparse_step_ms": round(ms_nchw, 4), "added_ms": round(ms_nchw - ms_sparse, 4),
                           "note": "NCHW activations through the boundary transposes; NHWC is native"},
         "miopen_context": miopen,
+        "library_gemm_context": gemm_ctx,
         "mask_pack_ms": round(ms_pack, 4),
         "forward_relu_mask": {"ms": round(ms_fwd, 4), "tflops": round(f_conv / (ms_fwd * 1e-3) / 1e12, 2)},
         "flops": {"dx_dense": f_conv, "dw_dense": f_conv, "dx_useful": f_useful_dx, "dw_useful": f_useful_dw},
