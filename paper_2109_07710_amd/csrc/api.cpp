@@ -2,6 +2,7 @@
 // the caller's stream.  See include/convbwd.h for the contract.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstring>
 
 #include "../../include/convbwd.h"
@@ -349,6 +350,11 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
         op.BNk = plan.bk;
         op.ktiles = plan.ktiles;
         op.nchunks = plan.nchunks;
+        // chunks per workgroup: about one (pixel, k tile) pair per thread,
+        // within the per-chunk flag arrays (1024 entries each)
+        const int ncombo = x_skip ? plan.tgroups * plan.ctiles : 1;
+        const int per_chunk = weight_chunk_px(desc->dtype) * plan.ktiles;
+        op.cpw = std::max(1, std::min(256 / per_chunk, 1024 / std::max(plan.ktiles, ncombo)));
         op.dtype = desc->dtype;
         if (x_skip) {
             // the X-window liveness is read from a packed footprint of X: the

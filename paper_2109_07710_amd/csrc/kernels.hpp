@@ -71,6 +71,7 @@ struct OccParams {
     const uint32_t* bits;    // packed dY footprint, or null
     uint8_t* occ;            // [nchunks][ktiles]
     int npq, K, chunk, BNk, ktiles, nchunks, dtype;
+    int cpw;                 // chunks per workgroup (cpw * ktiles, and cpw * combos, at most 1024)
     // X-window liveness (only when xlive is set): xlive[chunk][tg*ctiles+ct]
     // = 1 iff a pixel of the chunk has, at one of tap group tg's taps, an X
     // pixel inside the image with a non-zero among channel tile ct's channels.

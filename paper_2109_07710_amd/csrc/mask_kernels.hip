@@ -110,22 +110,26 @@ __global__ __launch_bounds__(CNT) void compact_scatter_kernel(CompactParams p)
 }
 
 // occ[chunk][kt] = 1 iff dY has a non-zero in pixels of the chunk and
-// channels of k-tile kt (from the packed footprint when given: one pixel per
-// thread, the tile's words read as vectors when K is a multiple of 256).
+// channels of k-tile kt (from the packed footprint when given: one (pixel,
+// k-tile) pair per thread, the tile's words read as vectors when the k-tile
+// is 256 wide and K a multiple of 256).  A workgroup covers p.cpw
+// consecutive chunks, enough pairs for its 256 threads, so narrow layers do
+// not launch one nearly idle workgroup per 64-pixel chunk.
 __global__ __launch_bounds__(256) void occupancy_kernel(OccParams p)
 {
-    __shared__ int flags[1024];
-    const int chunk = blockIdx.x;
-    for (int i = threadIdx.x; i < p.ktiles; i += blockDim.x) flags[i] = 0;
+    __shared__ int flags[1024];                  // [chunk of the group][k tile]
+    const int chunk0 = blockIdx.x * p.cpw;
+    const int nloc = min(p.cpw, p.nchunks - chunk0);
+    const int px0 = chunk0 * p.chunk;
+    const int npx = min(nloc * p.chunk, p.npq - px0);   // pixels of the group
+    for (int i = threadIdx.x; i < nloc * p.ktiles; i += blockDim.x) flags[i] = 0;
     __syncthreads();
-    const int px0 = chunk * p.chunk;
-    const int npx = min(p.chunk, p.npq - px0);
     if (p.bits) {
         const bool vec = p.BNk == 256 && (p.K & 255) == 0;
         const int pairs = npx * p.ktiles;
         for (int i = threadIdx.x; i < pairs; i += blockDim.x) {
-            const int px = px0 + i / p.ktiles, kt = i % p.ktiles;
-            const int64_t base = (int64_t)px * p.K;
+            const int j = i / p.ktiles, kt = i - j * p.ktiles;   // pixel of the group, k tile
+            const int64_t base = (int64_t)(px0 + j) * p.K;
             const int lo = kt * p.BNk, hi = min(p.K, lo + p.BNk);
             bool any;
             if (vec) {
@@ -135,7 +139,7 @@ __global__ __launch_bounds__(256) void occupancy_kernel(OccParams p)
             } else {
                 any = any_bits(p.bits, base + lo, base + hi);
             }
-            if (any) atomicOr(&flags[kt], 1);
+            if (any) flags[(j / p.chunk) * p.ktiles + kt] = 1;   // every writer stores 1
         }
     } else {
         const int E = p.dtype == 1 ? 8 : 4;
@@ -146,21 +150,22 @@ __global__ __launch_bounds__(256) void occupancy_kernel(OccParams p)
         for (int i = threadIdx.x; i < nv; i += blockDim.x) {
             const uint4 v = v4[i];
             const uint32_t b = p.dtype == 1 ? vec_bits<uint16_t>(v, false) : vec_bits<float>(v, false);
-            if (b) atomicOr(&flags[((i % vpp) * E) / p.BNk], 1);
+            const int j = i / vpp;
+            if (b) flags[(j / p.chunk) * p.ktiles + ((i - j * vpp) * E) / p.BNk] = 1;
         }
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < p.ktiles; i += blockDim.x)
-        p.occ[(int64_t)chunk * p.ktiles + i] = (uint8_t)(flags[i] != 0);
+    for (int i = threadIdx.x; i < nloc * p.ktiles; i += blockDim.x)
+        p.occ[(int64_t)chunk0 * p.ktiles + i] = (uint8_t)(flags[i] != 0);
 
     // X-window liveness for every (tap group, channel tile) of the weight
-    // gradient's tiling: 1 iff some pixel of this chunk has, at one of the
+    // gradient's tiling: 1 iff some pixel of the chunk has, at one of the
     // group's taps, an X pixel inside the image with a non-zero among the
     // tile's channels (from the packed X footprint).
     if (p.xlive) {
-        __shared__ int xflags[1024];
+        __shared__ int xflags[1024];             // [chunk of the group][combo]
         const int ncombo = p.tgroups * p.ctiles;
-        for (int i = threadIdx.x; i < ncombo; i += blockDim.x) xflags[i] = 0;
+        for (int i = threadIdx.x; i < nloc * ncombo; i += blockDim.x) xflags[i] = 0;
         __syncthreads();
         const int pairs = ncombo * npx;
         for (int i = threadIdx.x; i < pairs; i += blockDim.x) {
@@ -190,11 +195,11 @@ __global__ __launch_bounds__(256) void occupancy_kernel(OccParams p)
                     any = any_bits(p.xbits, base + lo, base + hi);
                 }
             }
-            if (any) xflags[combo] = 1;   // every writer stores 1
+            if (any) xflags[(j / p.chunk) * ncombo + combo] = 1;   // every writer stores 1
         }
         __syncthreads();
-        for (int i = threadIdx.x; i < ncombo; i += blockDim.x)
-            p.xlive[(int64_t)chunk * ncombo + i] = (uint8_t)(xflags[i] != 0);
+        for (int i = threadIdx.x; i < nloc * ncombo; i += blockDim.x)
+            p.xlive[(int64_t)chunk0 * ncombo + i] = (uint8_t)(xflags[i] != 0);
     }
 }
 
@@ -290,7 +295,9 @@ hipError_t launch_compact_scatter(const CompactParams& p, hipStream_t stream)
 
 hipError_t launch_occupancy(const OccParams& p, hipStream_t stream)
 {
-    occupancy_kernel<<<p.nchunks, 256, 0, stream>>>(p);
+    if (p.cpw < 1 || p.cpw * p.ktiles > 1024 || (p.xlive && p.cpw * p.tgroups * p.ctiles > 1024))
+        return hipErrorInvalidValue;
+    occupancy_kernel<<<(p.nchunks + p.cpw - 1) / p.cpw, 256, 0, stream>>>(p);
     return hipGetLastError();
 }
 
