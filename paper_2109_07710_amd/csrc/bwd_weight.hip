@@ -503,6 +503,11 @@ __global__ __launch_bounds__(TR_NT) void bwd_weight_tr_kernel(WeightParams p)
     const int tg = rem / p.ctiles;          // tap group: taps tg*tpg .. tg*tpg + tpg - 1
     const int cg = p.cg;                    // channel columns per packed tap (a multiple of 8)
     const int c0 = ct * BM, k0 = kt * BKT;
+    // Columns of this tile that hold data: the group's taps (fewer in a last,
+    // short group) or the channels left in a last channel tile.  A wave whose
+    // columns all lie past them has only zero operands, so it skips its
+    // fragment reads and matrix instructions (it still copies and waits).
+    const int used_cols = p.tpg > 1 ? min(p.tpg, RS - tg * p.tpg) * cg : min(BM, p.C - c0);
 
     if (blockIdx.x == 0 && tid == 0) p.header[0] = p.mode_flags;
 
@@ -572,7 +577,9 @@ __global__ __launch_bounds__(TR_NT) void bwd_weight_tr_kernel(WeightParams p)
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+    const bool wave_busy = __builtin_amdgcn_readfirstlane(wm * TM) < used_cols;
     auto compute = [&](int buf) {
+        if (!wave_busy) return;
         const char* Ab = reinterpret_cast<const char*>(As[buf]);
         const char* Bb = reinterpret_cast<const char*>(Bs[buf]);
 #pragma unroll

@@ -136,8 +136,11 @@ int weight_taps_per_group(const cbw_conv_desc* d)
 {
     const int rs = d->R * d->S;
     if (d->dtype != CBW_BF16 || rs == 1 || 2 * d->C > kWeightTileC) return 1;
+    // as few groups as the tile allows, the taps spread evenly over them
+    // (9 taps of 64 channels: 3 + 3 + 3 rather than 4 + 4 + 1)
     const int t = kWeightTileC / d->C;
-    return t < rs ? t : rs;
+    const int groups = (rs + t - 1) / t;
+    return (rs + groups - 1) / groups;
 }
 
 int plan_weight(const cbw_conv_desc* d, WeightPlan* out)

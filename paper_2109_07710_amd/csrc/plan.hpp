@@ -54,9 +54,10 @@ inline int host_data_split(int T, int nsteps)
 }
 
 // Weight-gradient tiling (bf16): output channels per tile (64, 128 or 256,
-// from K) and, when C <= 128, floor(256/C) filter taps (at most R*S) packed
-// side by side in one 256-column channel tile, C columns each, so narrow
-// layers fill the tile.
+// from K) and, when C <= 128, up to floor(256/C) filter taps packed side by
+// side in one 256-column channel tile, C columns each, so narrow layers fill
+// the tile; the R*S taps go into as few groups as that allows, spread
+// evenly over them.
 int weight_tile_k_for(const cbw_conv_desc* d);
 int weight_taps_per_group(const cbw_conv_desc* d);
 

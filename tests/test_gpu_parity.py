@@ -353,7 +353,7 @@ def _x_skip_case(N, C, H, W, K, R, S, stride, pad, dtype, seed):
 
 @pytest.mark.parametrize("case", [
     (2, 256, 16, 16, 256, 3, 3, 1, 1, "bf16"),     # one tap per tile
-    (2, 64, 12, 14, 64, 3, 3, 1, 1, "bf16"),       # four taps packed per tile
+    (2, 64, 12, 14, 64, 3, 3, 1, 1, "bf16"),       # three taps packed per tile (3 + 3 + 3)
     (2, 48, 13, 11, 40, 3, 3, 2, 1, "bf16"),       # stride 2, five taps packed, ragged tiles
     (2, 320, 9, 9, 72, 1, 1, 1, 0, "bf16"),        # 1x1, two channel tiles
     (2, 32, 10, 10, 24, 3, 3, 1, 1, "f32"),        # float32 kernel
@@ -387,9 +387,11 @@ def test_x_block_skip(case, use_bits):
     cb.conv_bwd_weight_sparse_x(desc, d["x"], d["dy"], xm, dym, dw_n, ws, cb.CBW_FLAG_NO_SKIP)
     torch.cuda.synchronize()
     # the tiling: filter taps packed side by side for bf16 when two or more
-    # channel tiles fit in 256 columns, else one tap per 256-channel tile
+    # channel tiles fit in 256 columns (as few groups as fit, the taps spread
+    # evenly over them), else one tap per 256-channel tile
     packed = dt == "bf16" and R * S > 1 and 2 * C <= 256
-    tpg = min(256 // C, R * S) if packed else 1
+    groups = -(-(R * S) // (256 // C)) if packed else R * S
+    tpg = -(-(R * S) // groups) if packed else 1
     ctile = C if packed else 256
     x64, _, dy64 = oracle_inputs(t)
     live = oracle.weight_block_liveness(x64 != 0, dy64 != 0, (R, S), (st, st), (pd, pd), chunk, kw, ctile, tpg)
