@@ -457,9 +457,11 @@ __device__ __forceinline__ uint2 ds_read_tr16(const void* lds)
 }
 
 constexpr int TR_NT = 1024;            // 16 waves (four per SIMD): more waves hide more copy and LDS latency
+#ifndef CBW_DW_TR64_NT
+#define CBW_DW_TR64_NT 1024
+#endif
 constexpr int TR_BK = 64;              // pixels per step
 constexpr int TR_ROW = BM / 8;         // 16-byte chunks per LDS row (one pixel)
-constexpr int TR_IA = TR_BK * BM * 2 / 1024 / (TR_NT / 64);  // 1 KB copies per wave per step, per operand
 static_assert(BM == 256 && BN == 256, "the natural-layout kernel assumes 256-wide rows");
 
 // Tiling of the natural-layout kernel for BKT output channels per tile
@@ -471,17 +473,20 @@ static_assert(BM == 256 && BN == 256, "the natural-layout kernel assumes 256-wid
 // copied as out-of-range zeros and never read.
 template <int BKT>
 struct WTile {
-    static constexpr int WN = BKT / 64, WM = (TR_NT / 64) / WN;
+    static constexpr int NT = BKT == 64 ? CBW_DW_TR64_NT : TR_NT;   // threads per workgroup
+    static constexpr int WN = BKT / 64, WM = (NT / 64) / WN;
     static constexpr int TM = BM / WM, TN = BKT / WN;
     static constexpr int FM = TM / 16, FN = TN / 16;
-    static_assert(WM * WN * 64 == TR_NT && TN == 64, "64 output channels per wave");
+    static constexpr int IA = TR_BK * BM * 2 / 1024 / (NT / 64);  // 1 KB copies per wave per step, per operand
+    static_assert(WM * WN * 64 == NT && TN == 64, "64 output channels per wave");
 };
 
 template <int BKT>
-__global__ __launch_bounds__(TR_NT) void bwd_weight_tr_kernel(WeightParams p)
+__global__ __launch_bounds__(WTile<BKT>::NT) void bwd_weight_tr_kernel(WeightParams p)
 {
     constexpr uint32_t ESZ = 2;
-    constexpr int NW = TR_NT / 64;
+    constexpr int NW = WTile<BKT>::NT / 64;
+    constexpr int TR_IA = WTile<BKT>::IA;
     constexpr int WN = WTile<BKT>::WN;
     constexpr int TM = WTile<BKT>::TM, TN = WTile<BKT>::TN, FM = WTile<BKT>::FM, FN = WTile<BKT>::FN;
     __shared__ uint4 As[2][TR_BK * TR_ROW];
@@ -676,7 +681,7 @@ int weight_chunk(int dtype) { return CH * (dtype == 1 ? 8 : 4); }
 hipError_t launch_bwd_weight(int dtype, const WeightParams& p, hipStream_t stream, const ProfEvents& ev)
 {
     const int nb = p.tgroups * p.ctiles * p.ktiles * p.nsplit;
-    const dim3 grid(nb), block(dtype == 1 ? TR_NT : NT);
+    const dim3 grid(nb), block(dtype != 1 ? NT : p.bk == 64 ? WTile<64>::NT : WTile<256>::NT);
     if (dtype == 1) {
         if (p.bk == 64) hipExtLaunchKernelGGL(bwd_weight_tr_kernel<64>, grid, block, 0, stream, ev.start, ev.stop, 0, p);
         else if (p.bk == 128) hipExtLaunchKernelGGL(bwd_weight_tr_kernel<128>, grid, block, 0, stream, ev.start, ev.stop, 0, p);
