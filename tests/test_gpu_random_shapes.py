@@ -10,7 +10,9 @@ zero over the first image (its upper half for a batch of one) so that the
 weight gradient skips blocks where a whole chunk of pixels falls inside.
 Checks: masked and dense dX (values, and the +0.0 pattern of killed
 outputs), dW with dY skipping, with X skipping and without skipping (values;
-the skipping runs agree with the unskipped one to fp32 reassociation).
+the skipping runs agree with the unskipped one to fp32 reassociation), and
+that a second call of the masked dX and of both skipping dW calls gives the
+same bits.
 """
 import numpy as np
 import pytest
@@ -106,6 +108,17 @@ def test_random_shape(c):
         torch.cuda.synchronize()
         dws[name] = (o, cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, wsw).blocks_skipped)
     torch.cuda.synchronize()
+    # a second run of every call gives the same bits (fixed reduction orders)
+    again = torch.full_like(x, float("nan"))
+    cb.conv_bwd_data_masked(desc, dy, w, xm, again, cb.workspace(desc, cb.CBW_OP_BWD_DATA_MASKED))
+    assert torch.equal(again.view(torch.int16 if c["dtype"] == "bf16" else torch.int32),
+                       dxm.view(torch.int16 if c["dtype"] == "bf16" else torch.int32)), "masked dX not reproducible"
+    for name, fn in (("dy_skip", lambda o: cb.conv_bwd_weight_sparse(desc, x, dy, dym, o, wsw)),
+                     ("x_skip", lambda o: cb.conv_bwd_weight_sparse_x(desc, x, dy, xm, dym, o, wsw))):
+        o = torch.full(w.shape, float("nan"), dtype=torch.float32, device="cuda")
+        fn(o)
+        torch.cuda.synchronize()
+        assert torch.equal(o.view(torch.int32), dws[name][0].view(torch.int32)), "dW %s not reproducible" % name
 
     x64 = oracle.nhwc_to_nchw(t["x"].double().numpy())
     w64 = oracle.krsc_to_kcrs(t["w"].double().numpy())
