@@ -182,13 +182,15 @@ def main():
     f_exec = f_conv * exec_frac_dx + f_conv * exec_frac_dw
 
     # dominant kernel: the longer of the two GEMMs
+    tiling = cb.cbw_data_tiling(desc)   # all pixels are live here, so the gather mode tiles alike
     kern = {"dx_gemm": ms_dx_gemm, "dw_gemm": ms_dw_gemm}
     dom = max(kern, key=kern.get)
     dom_flops = f_conv * (exec_frac_dx if dom == "dx_gemm" else exec_frac_dw)
     achieved = dom_flops / (kern[dom] * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_for(dom),
-                "kernel": {"dx_gemm": "bwd_data_kernel<unsigned short, 2, true, 0> (bf16, gather, 256x224 tile)",
+                "kernel": {"dx_gemm": "bwd_data_kernel<unsigned short, 2, true, 0> (bf16, gather, %d-channel x %d-pixel "
+                                      "tiles of %d-row capacity)" % (tiling[0], tiling[2], tiling[1]),
                            "dw_gemm": "bwd_weight_tr_kernel<256> (bf16, 256-wide output-channel tile)"}[dom],
                 "kernel_ms": round(kern[dom], 4), "flops_per_launch": dom_flops}
 
@@ -589,10 +591,13 @@ def traffic_for(kernel):
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    src = {"dx_gemm": "bwd_data.hip", "dw_gemm": "bwd_weight.hip"}[kernel]
-    h = hashlib.sha256(open(os.path.join(ROOT, "paper_2109_07710_amd", "csrc", src), "rb").read()).hexdigest()
     entry = rec.get(kernel)
-    if not entry or entry.get("source_sha256") != h:
+    if not entry or not entry.get("sources"):
+        return None
+    h = hashlib.sha256()
+    for src in entry["sources"]:
+        h.update(open(os.path.join(ROOT, src), "rb").read())
+    if entry.get("sources_sha256") != h.hexdigest():
         return None
     return entry.get("hbm_bytes_per_launch")
 

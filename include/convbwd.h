@@ -103,6 +103,18 @@ typedef struct {
     int64_t blocks_skipped;  /* dW blocks skipped (dY, or with the _x variant X, all zero)     */
 } cbw_stats;
 
+/* Host-only inspection of the data-gradient tiling that conv_bwd_data and
+ * the CBW_FLAG_NO_SKIP masked call use for this descriptor (tests and tools):
+ * *channels output channels per tile, *capacity pixel rows a tile can hold,
+ * and *rows pixel rows each tile covers -- the capacity, or 16 or 32 rows
+ * less, whichever lets the busiest CU finish its tiles first given one
+ * resident tile per CU (tiles / CUs rounded up, times the rows); the full
+ * capacity whenever the tiles are few enough for the reduction to be split.
+ * The skipping masked call makes the same choice on the device from the live
+ * pixel counts.  Any output pointer may be NULL.  Returns CBW_OK or the
+ * descriptor's validation status. */
+int cbw_data_tiling(const cbw_conv_desc* desc, int32_t* channels, int32_t* capacity, int32_t* rows);
+
 /* Human-readable name of a cbw_status value (static storage). */
 const char* cbw_status_string(int status);
 

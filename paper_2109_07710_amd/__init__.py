@@ -26,7 +26,7 @@ CBW_OP_BWD_DATA, CBW_OP_BWD_DATA_MASKED, CBW_OP_BWD_WEIGHT, CBW_OP_FWD, CBW_OP_B
 CBW_FLAG_NO_SKIP = 1
 
 EXPORTS = ("cbw_status_string", "cbw_validate_desc", "cbw_mask_words", "cbw_dy_mask_words",
-           "cbw_workspace_size", "cbw_relu_mask_pack", "cbw_nonzero_mask_pack", "conv_bwd_data",
+           "cbw_workspace_size", "cbw_data_tiling", "cbw_relu_mask_pack", "cbw_nonzero_mask_pack", "conv_bwd_data",
            "conv_bwd_data_masked", "conv_fwd_relu_mask", "conv_bwd_weight_sparse", "conv_bwd_weight_sparse_x",
            "conv_bwd_data_elementwise", "cbw_read_pixel_counts", "cbw_read_weight_work", "cbw_read_stats",
            "cbw_read_live_lists",
@@ -85,6 +85,8 @@ def lib():
     L.cbw_dy_mask_words.argtypes = [dp]
     L.cbw_dy_mask_words.restype = sz
     L.cbw_workspace_size.argtypes = [dp, ctypes.c_int, ctypes.POINTER(sz)]
+    i32p_ = ctypes.POINTER(ctypes.c_int32)
+    L.cbw_data_tiling.argtypes = [dp, i32p_, i32p_, i32p_]
     L.cbw_relu_mask_pack.argtypes = [dp, vp, vp, vp]
     L.cbw_nonzero_mask_pack.argtypes = [ctypes.c_int32, ctypes.c_int64, vp, vp, vp]
     L.conv_bwd_data.argtypes = [dp, vp, vp, vp, vp, sz, vp]
@@ -156,6 +158,15 @@ def cbw_workspace_size(desc, op):
     n = ctypes.c_size_t(0)
     _check(lib().cbw_workspace_size(ctypes.byref(desc), op, ctypes.byref(n)), "cbw_workspace_size")
     return n.value
+
+
+def cbw_data_tiling(desc):
+    """(channels per tile, pixel-row capacity, pixel rows per tile) of the
+    data-gradient GEMM in its dense and non-skipping modes (host only)."""
+    a, b, c = ctypes.c_int32(0), ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(lib().cbw_data_tiling(ctypes.byref(desc), ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)),
+           "cbw_data_tiling")
+    return a.value, b.value, c.value
 
 
 def workspace(desc, op, device="cuda"):

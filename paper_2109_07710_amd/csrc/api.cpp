@@ -115,6 +115,8 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
     p.tile = plan.tile;
     p.mask = x_mask;
     p.ptiles = plan.ptiles;
+    p.brows = plan.brows;
+    p.maxtiles = plan.maxtiles;
     p.nslots = kDataSlots;
     p.smax = kDataMaxSplit;
     p.split = gather ? 1 : plan.split;
@@ -165,6 +167,8 @@ int run_fwd(const cbw_conv_desc* desc, const void* X, const void* W, void* Y, ui
     DataParams p = data_params(&vd, X, wt, Y, plan.npix, plan.groups);
     p.tile = plan.tile;
     p.ptiles = plan.ptiles;
+    p.brows = plan.brows;
+    p.maxtiles = plan.maxtiles;
     p.nslots = kDataSlots;
     p.smax = kDataMaxSplit;
     p.split = plan.split;
@@ -228,6 +232,17 @@ static int validate_elementwise(const cbw_conv_desc* d)
 static size_t elementwise_ws(const cbw_conv_desc* d)
 {
     return ((size_t)d->N * d->H * d->W * 4 + 255) / 256 * 256;
+}
+
+int cbw_data_tiling(const cbw_conv_desc* desc, int32_t* channels, int32_t* capacity, int32_t* rows)
+{
+    DataPlan p;
+    const int st = plan_data(desc, false, &p);
+    if (st != CBW_OK) return st;
+    if (channels) *channels = p.bm;
+    if (capacity) *capacity = p.bn;
+    if (rows) *rows = p.brows;
+    return CBW_OK;
 }
 
 int cbw_workspace_size(const cbw_conv_desc* desc, int op, size_t* bytes)

@@ -53,19 +53,59 @@ struct Tile {
     static constexpr int FM = TM / 16, FN = TN / 16;   // 16x16 MFMA tiles per wave
     static constexpr int IA = (BM / 8 + NW - 1) / NW;  // 1 KB copy instructions per wave per step, A
     static constexpr int IB = (BN / 8 + NW - 1) / NW;  // same for B
-    static_assert(NW == 8 || NW == 16, "two or four waves per SIMD");
+    static_assert(NW == 16, "four waves per SIMD");
     static_assert(BM % 8 == 0 && BN % 8 == 0, "tiles are copied in groups of 8 rows");
     static_assert(TM % 16 == 0 && TN % 16 == 0, "wave tile must be a multiple of 16");
 };
 
 __device__ __forceinline__ int swz8(int row) { return (row >> 1) & 7; }
 
+// Wave coordinates (wm along channels, wn along pixels) of wave w.  The
+// waves w, w + 4, w + 8 and w + 12 of a workgroup share one SIMD (measured:
+// which SIMD varies between workgroups, the grouping does not), and the
+// coordinates are spread so that those four waves sit in different pixel
+// columns where WN allows: when a tile's pixel blocks do not divide evenly
+// among the WN columns, the columns with one block more fall on different
+// SIMDs and every SIMD gets the same matrix work.
+template <int WN>
+__device__ __forceinline__ void wave_coords(int w, int& wm, int& wn)
+{
+    static_assert(WN == 2 || WN == 4 || WN == 8, "16-wave tiles only");
+    const int s = w & 3, q = w >> 2;
+    if (WN == 2) {
+        wm = s + 4 * (q >> 1);
+        wn = q & 1;
+    } else if (WN == 4) {
+        wm = s;
+        wn = q;
+    } else {
+        wm = s >> 1;
+        wn = 2 * q + (s & 1);
+    }
+}
+
+// Rows per tile in gather mode, from the live counts of every channel group
+// (the host makes the same choice for the other modes from the pixel count).
+template <int BN>
+__device__ __forceinline__ int gather_rows(const int32_t* counts, int groups, int slots)
+{
+    int tiles[kDataRowChoices];
+#pragma unroll
+    for (int c = 0; c < kDataRowChoices; ++c) {
+        const int rows = BN - 16 * c;
+        int t = 0;
+        for (int g = 0; g < groups; ++g) t += (counts[g] + rows - 1) / rows;
+        tiles[c] = t;
+    }
+    return data_rows_pick(tiles, BN, slots);
+}
+
 template <typename T, int MODE, bool UNIT, int TI>
 __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
 {
     using TL = Tile<TI>;
     constexpr int BM = TL::BM, BN = TL::BN, WN = TL::WN, NW = TL::NW;
-    constexpr int TM = TL::TM, TN = TL::TN, FM = TL::FM, FN = TL::FN, IA = TL::IA, IB = TL::IB;
+    constexpr int TM = TL::TM, FM = TL::FM, FN = TL::FN, IA = TL::IA, IB = TL::IB;
     constexpr int NT = TL::NT;
     constexpr int E = Elem<T>::E;
     constexpr int BK = CH * E;     // reduction elements per step
@@ -79,7 +119,8 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave / WN, wn = wave % WN;
+    int wm, wn;
+    wave_coords<WN>(wave, wm, wn);
 
     // Work items are (tile, reduction split).  In gather mode the number of
     // live tiles T follows from the compaction counts; when T is small
@@ -88,23 +129,29 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     // (splitk_data_reduce_kernel) -- every workgroup derives the same S.
     const int kchunks = (p.K + (CH * Elem<T>::E) - 1) / (CH * Elem<T>::E);
     const int nsteps = p.R * p.S * kchunks;
-    int ntiles, nsplit;
+    int ntiles, nsplit, brows;
     if (MODE == MODE_GATHER) {
+        brows = gather_rows<BN>(p.counts, p.ctiles, p.nslots);
         ntiles = 0;
-        for (int g = 0; g < p.ctiles; ++g) ntiles += (p.counts[g] + BN - 1) / BN;
+        for (int g = 0; g < p.ctiles; ++g) ntiles += (p.counts[g] + brows - 1) / brows;
         nsplit = data_split(ntiles, nsteps, p.nslots, p.smax);
     } else {
+        brows = p.brows;
         ntiles = p.ptiles * p.ctiles;
         nsplit = p.split;
     }
-    const int item = xcd_remap(blockIdx.x, gridDim.x);
-    if (item >= ntiles * nsplit) return;  // uniform across the workgroup
+    // The grid may hold more workgroups than items (gather mode sizes it for
+    // the most tiles any row choice gives); the surplus exits, and the XCD
+    // remap runs over the items alone so that every XCD gets its share.
+    const int nitems = ntiles * nsplit;
+    if ((int)blockIdx.x >= nitems) return;  // uniform across the workgroup
+    const int item = xcd_remap(blockIdx.x, nitems);
     const int tile = item / nsplit, z = item - tile * nsplit;
     int ctile, ptile;
     if (MODE == MODE_GATHER) {
         int g = 0, cum = 0;
         while (true) {
-            const int tg = (p.counts[g] + BN - 1) / BN;
+            const int tg = (p.counts[g] + brows - 1) / brows;
             if (tile < cum + tg) break;
             cum += tg;
             ++g;
@@ -116,7 +163,14 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
         ctile = tile - ptile * p.ctiles;
     }
     const int c0 = ctile * BM;
-    const int row0 = ptile * BN;
+    const int row0 = ptile * brows;
+    // The tile's brows / 16 pixel blocks are shared out among the WN pixel
+    // columns of waves as evenly as possible: this wave's column covers fnw
+    // blocks (FN or FN - 1) from row wrow0.
+    const int nblk16 = brows >> 4;
+    const int fn_base = nblk16 / WN, fn_rem = nblk16 - fn_base * WN;
+    const int fnw = __builtin_amdgcn_readfirstlane(fn_base + (wn < fn_rem ? 1 : 0));
+    const int wrow0 = 16 * (wn * fn_base + (wn < fn_rem ? wn : fn_rem));
     const int nrows = MODE == MODE_GATHER ? p.counts[ctile] : p.npix;
     const int st_begin = (int)((int64_t)z * nsteps / nsplit);
     const int st_end = (int)((int64_t)(z + 1) * nsteps / nsplit);
@@ -161,7 +215,7 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     for (int i = tid; i < BN; i += NT) {
         const int r = row0 + i;
         int pix = -1;
-        if (r < nrows) pix = (MODE == MODE_GATHER) ? p.lists[(int64_t)ctile * p.npix + r] : r;
+        if (i < brows && r < nrows) pix = (MODE == MODE_GATHER) ? p.lists[(int64_t)ctile * p.npix + r] : r;
         pix_s[i] = pix;
     }
     __syncthreads();
@@ -221,8 +275,8 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
         const uint32_t b_step = (uint32_t)k0 * ESZ;
 #pragma unroll
         for (int j = 0; j < IB; ++j) {
-            const int g = wave + NW * j;
-            if (IB * NW * 8 == BN || g * 8 < BN) {
+            const int g = wave_u + NW * j;
+            if (g * 8 < brows) {
                 const bool kin = kfull || (k0 + b_lc[j] * E < p.K);
                 buf_load16_lds(rs_dy, kin ? b_off[j] + b_step : kOOB,
                                lds_addr(&Bs[buf][(wave_u + NW * j) * 8 * CH]));
@@ -237,25 +291,28 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
         if (++ld_kc == kchunks) { ld_kc = 0; ++ld_tap; }
     };
 
-    auto compute = [&](int buf) {
+    // NB: the wave's pixel blocks (fnw, a compile-time FN or FN - 1)
+    auto compute = [&](int buf, auto nb_tag) {
+        constexpr int NB = decltype(nb_tag)::value;
 #pragma unroll
         for (int kc = 0; kc < CH / 4; ++kc) {
             const int chl = kc * 4 + (lane >> 4);
-            uint4 fa[FM], fb[FN];
+            uint4 fa[FM], fb[NB];
 #pragma unroll
             for (int i = 0; i < FM; ++i) {
                 const int row = wm * TM + i * 16 + (lane & 15);
                 fa[i] = As[buf][row * CH + (chl ^ swz8(row))];
             }
 #pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                const int row = wn * TN + j * 16 + (lane & 15);
+            for (int j = 0; j < NB; ++j) {
+                const int row = wrow0 + j * 16 + (lane & 15);
                 fb[j] = Bs[buf][row * CH + (chl ^ swz8(row))];
             }
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int j = 0; j < FN; ++j) acc[i][j] = mfma_chunk(acc[i][j], fa[i], fb[j], T{});
+                for (int j = 0; j < NB; ++j) acc[i][j] = mfma_chunk(acc[i][j], fa[i], fb[j], T{});
+
         }
     };
 
@@ -289,14 +346,19 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     const int mask_step = nloc > 1 ? 1 : 0;
     wait_vmem();
     __syncthreads();
-    for (int step = 0; step < nloc; ++step) {
-        const int buf = step & 1;
-        if (step + 1 < nloc) load(buf ^ 1);
-        if (mask_lds && step == mask_step) fetch_mask();
-        compute(buf);
-        wait_vmem();
-        __syncthreads();
-    }
+    auto main_loop = [&](auto nb_tag) {
+        for (int step = 0; step < nloc; ++step) {
+            const int buf = step & 1;
+            if (step + 1 < nloc) load(buf ^ 1);
+            if (mask_lds && step == mask_step) fetch_mask();
+            compute(buf, nb_tag);
+            wait_vmem();
+            __syncthreads();
+        }
+    };
+    static_assert(FN >= 2, "a wave column holds at least two pixel blocks");
+    if (fnw == FN) main_loop(std::integral_constant<int, FN>{});
+    else main_loop(std::integral_constant<int, FN - 1>{});
 
     if (mask_lds) {
         // msk_s is not an operand buffer: no barrier is needed before writing it
@@ -309,13 +371,14 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     }
 
     // Epilogue: lane holds channels c0 + wm*TM + i*16 + 4*(lane/16) + v of
-    // pixel row wn*TN + j*16 + lane%16.
+    // pixel row wrow0 + j*16 + lane%16, j < fnw.
     if (nsplit > 1) {
         // partial tile [item][row][channel] in fp32, reduced afterwards
         float* __restrict__ part = p.partial + (int64_t)item * BN * BM;
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-            const int pr = wn * TN + j * 16 + (lane & 15);
+            if (j >= fnw) break;   // uniform: the wave's column has fnw blocks
+            const int pr = wrow0 + j * 16 + (lane & 15);
 #pragma unroll
             for (int i = 0; i < FM; ++i) {
                 const int cl = wm * TM + i * 16 + 4 * (lane >> 4);
@@ -336,7 +399,8 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
         static_assert(TM % 32 == 0, "wave tile must cover whole footprint words");
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-            const int pr = wn * TN + j * 16 + (lane & 15);
+            if (j >= fnw) break;   // uniform: the wave's column has fnw blocks
+            const int pr = wrow0 + j * 16 + (lane & 15);
 #pragma unroll
             for (int w = 0; w < MWJ; ++w) ew[j][w] = msk_s[pr * (BM / 32) + (wm * TM) / 32 + w];
         }
@@ -356,7 +420,8 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
         const int q = lane >> 4;
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-            const int pr = wn * TN + j * 16 + (lane & 15);
+            if (j >= fnw) break;   // uniform: the wave's column has fnw blocks
+            const int pr = wrow0 + j * 16 + (lane & 15);
             const int pix = pix_s[pr];
             const int clane = wm * TM + 4 * q;
             const uint32_t base = (uint32_t)(pix * p.C + c0 + clane) * ESZ;
@@ -410,7 +475,8 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
         constexpr bool LDSW = decltype(lds_tag)::value;
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-            const int pr = wn * TN + j * 16 + (lane & 15);
+            if (j >= fnw) break;   // uniform: the wave's column has fnw blocks
+            const int pr = wrow0 + j * 16 + (lane & 15);
             const int pix = pix_s[pr];
             const int clane = wm * TM + 4 * (lane >> 4);   // first channel of the lane's block, i = 0
             const uint32_t base = (uint32_t)(pix * p.C + c0 + clane) * ESZ;
@@ -557,6 +623,8 @@ __global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
         ntiles = p.ptiles * p.ctiles;
         nsplit = p.split;
     }
+    // A split reduction only happens with full BN-row tiles (data_rows_pick
+    // keeps BN whenever 2 * tiles <= slots), so tiles are counted at BN here.
     if (nsplit <= 1) return;
     const int64_t nvec = (int64_t)ntiles * BN * (BM / 4);
     T* __restrict__ dx = reinterpret_cast<T*>(p.dx);
@@ -720,8 +788,9 @@ hipError_t launch_type(int mode, const DataParams& p, int nb, hipStream_t stream
 
 hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream, const ProfEvents& ev)
 {
-    // enough workgroups for every tile unsplit, or for nslots split items
-    const int nb = max(p.ptiles * p.ctiles, p.nslots);
+    // enough workgroups for every tile unsplit (gather mode: at the smallest
+    // row choice), or for nslots split items
+    const int nb = max(mode == MODE_GATHER ? p.maxtiles : p.ptiles * p.ctiles, p.nslots);
     if (nb <= 0) return hipSuccess;
     if (p.tile < 0 || p.tile >= kDataTileCount) return hipErrorInvalidValue;
     return dtype == 1 ? launch_type<uint16_t>(mode, p, nb, stream, ev)

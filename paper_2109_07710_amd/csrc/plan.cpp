@@ -80,7 +80,14 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out)
     p.groups = (d->C + p.bm - 1) / p.bm;
     p.nblk = (int)((p.npix + kCompactBlock - 1) / kCompactBlock);
     size_t cur = 0;
-    p.ptiles = (int)((p.npix + p.bn - 1) / p.bn);
+    int cand[kDataRowChoices];
+    for (int c = 0; c < kDataRowChoices; ++c) {
+        const int rows = p.bn - 16 * c;
+        cand[c] = p.groups * (int)((p.npix + rows - 1) / rows);
+    }
+    p.brows = data_rows_pick(cand, p.bn, kDataSlots);
+    p.ptiles = (int)((p.npix + p.brows - 1) / p.brows);
+    p.maxtiles = cand[kDataRowChoices - 1];
     const int bk = 8 * (d->dtype == CBW_BF16 ? 8 : 4);
     p.nsteps = d->R * d->S * ((d->K + bk - 1) / bk);
     p.split = host_data_split(p.ptiles * p.groups, p.nsteps);

@@ -32,6 +32,8 @@ struct DataPlan {
     int64_t npix = 0;
     int groups = 0, nblk = 0;
     int ptiles = 0, nsteps = 0;
+    int brows = 0;          // dense / select: pixel rows per tile (data_rows_pick)
+    int maxtiles = 0;       // most tiles any row choice can give (the gather mode's grid)
     int split = 1;          // dense / select: host-chosen reduction split
     Region header, wt, blk_counts, counts, lists, partial;
     // NCHW callers: NHWC copies of dY and dX and the NHWC-order footprint,

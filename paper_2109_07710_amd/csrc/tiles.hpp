@@ -34,3 +34,32 @@ struct DataTile {
 };
 constexpr int kDataTileCount = 3;
 constexpr DataTile kDataTiles[kDataTileCount] = {{256, 224, 8, 2}, {128, 448, 4, 4}, {64, 512, 2, 8}};
+
+// Pixel rows a data-gradient tile actually covers: its capacity BN, or 16 or
+// 32 rows less.  With `slots` resident workgroups the busiest CU runs
+// ceil(tiles / slots) tiles one after another, so the rows that make
+// ceil(tiles / slots) * rows smallest finish first (ties go to the larger
+// tile).  Example: 32 images of 56 x 56 (100352 pixels) on 256 CUs take 448
+// tiles of 224 rows (two rounds of 14 pixel blocks) or 483 tiles of 208 rows (two
+// rounds of 13).  When so few tiles exist that the reduction is split
+// (2 * tiles <= slots) the full tile is kept.  tiles[d] is the tile count at
+// BN - 16 d rows.  constexpr, so host planner and kernels share this one rule.
+#ifndef CBW_DX_ROW_CHOICES
+#define CBW_DX_ROW_CHOICES 3
+#endif
+constexpr int kDataRowChoices = CBW_DX_ROW_CHOICES;
+constexpr int data_rows_pick(const int* tiles, int bn, int slots)
+{
+    if (2 * tiles[0] <= slots) return bn;
+    int best = bn;
+    long long best_cost = (long long)((tiles[0] + slots - 1) / slots) * bn;
+    for (int d = 1; d < kDataRowChoices; ++d) {
+        const int rows = bn - 16 * d;
+        const long long cost = (long long)((tiles[d] + slots - 1) / slots) * rows;
+        if (cost < best_cost) {
+            best = rows;
+            best_cost = cost;
+        }
+    }
+    return best;
+}

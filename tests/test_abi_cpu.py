@@ -206,3 +206,43 @@ def test_nchw_workspace_and_scope(L):
     assert _ws(b, cb.CBW_OP_FWD)[0] == cb.CBW_ERR_UNSUPPORTED
     e = cb.ConvDesc.make(4, 64, 10, 12, 64, 3, 3, 1, 1, act_layout="nchw")
     assert _ws(e, cb.CBW_OP_BWD_DATA_ELEMENTWISE)[0] == cb.CBW_ERR_UNSUPPORTED
+
+
+# (N, C, H, W) -> expected (channels, capacity, rows).  The rows follow from
+# counting rounds by hand: with 256 resident tiles, T tiles take ceil(T / 256)
+# rounds, and the pick minimises rounds x rows among capacity, capacity - 16
+# and capacity - 32 (full capacity when T <= 128, where the reduction splits).
+TILING_CASES = [
+    # 100352 pixels, 256 channels: 448 / 483 / 523 tiles -> 2, 2, 3 rounds -> 208
+    ((32, 256, 56, 56), (256, 224, 208)),
+    # 49152 pixels: 220 / 237 / 256 tiles, one round each -> the smallest, 192
+    ((12, 256, 64, 64), (256, 224, 192)),
+    # 114688 pixels: 512 / 552 / 598 tiles -> 2, 3, 3 rounds -> 224
+    ((28, 256, 64, 64), (256, 224, 224)),
+    # 128 channels, 100352 pixels: 224 / 233 / 242 tiles, one round -> 416
+    ((32, 128, 56, 56), (128, 448, 416)),
+    # 110592 pixels: 247 / 256 / 266 tiles -> 1, 1, 2 rounds -> 432
+    ((27, 128, 64, 64), (128, 448, 432)),
+    # 64 channels, 100352 pixels: 196 / 203 / 210 tiles, one round -> 480
+    ((2, 64, 224, 224), (64, 512, 480)),
+    # 126976 pixels: 248 / 256 / 265 tiles -> 1, 1, 2 rounds -> 496
+    ((31, 64, 64, 64), (64, 512, 496)),
+    # 512 pixels: one tile, split reduction -> full capacity
+    ((2, 16, 16, 16), (64, 512, 512)),
+    # 28672 pixels: 128 tiles of 224 -> split regime -> 224
+    ((8, 256, 56, 64), (256, 224, 224)),
+]
+
+
+@pytest.mark.parametrize("shape,expect", TILING_CASES, ids=lambda v: "x".join(map(str, v)))
+def test_data_tile_rows(L, shape, expect):
+    N, C, H, W = shape
+    d = cb.ConvDesc.make(N, C, H, W, C, 3, 3, 1, 1)
+    assert cb.cbw_data_tiling(d) == expect
+
+
+def test_data_tiling_rejects_bad_descriptors(L):
+    d = _desc()
+    d.P += 1
+    z = ctypes.c_int32(0)
+    assert L.cbw_data_tiling(ctypes.byref(d), ctypes.byref(z), None, None) == cb.CBW_ERR_INVALID_ARG
