@@ -100,6 +100,45 @@ __device__ __forceinline__ int gather_rows(const int32_t* counts, int groups, in
     return data_rows_pick(tiles, BN, slots);
 }
 
+// Channel group and pixel tile of gather-mode tile `tile`.  Tiles are taken
+// round by round: round r holds the r-th pixel tile of every group that has
+// more than r tiles, groups in order.  The groups of one pixel range thus sit
+// next to each other in the order, as in the dense mode (tile = ptile *
+// groups + group), and the XCD that runs them reads their shared dY rows
+// into one L2 instead of every group's XCD reading them again.  Rounds in
+// which every group still has a tile are resolved in closed form.
+__device__ __forceinline__ void gather_tile(const int32_t* counts, int groups, int rows, int tile, int& g,
+                                            int& ptile)
+{
+    int tmin = 0x7fffffff, tmax = 0;
+    for (int k = 0; k < groups; ++k) {
+        const int t = (counts[k] + rows - 1) / rows;
+        tmin = min(tmin, t);
+        tmax = max(tmax, t);
+    }
+    if (tile < tmin * groups) {
+        ptile = tile / groups;
+        g = tile - ptile * groups;
+        return;
+    }
+    int before = tmin * groups;
+    for (int r = tmin; r < tmax; ++r) {
+        for (int k = 0; k < groups; ++k) {
+            if ((counts[k] + rows - 1) / rows <= r) continue;
+            if (before == tile) {
+                g = k;
+                ptile = r;
+                return;
+            }
+            ++before;
+        }
+    }
+    // not reached for tile < the total tile count; past it, a tile beyond
+    // every group's rows (no pixel is read or written)
+    g = 0;
+    ptile = tmax;
+}
+
 template <typename T, int MODE, bool UNIT, int TI>
 __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
 {
@@ -149,15 +188,7 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     const int tile = item / nsplit, z = item - tile * nsplit;
     int ctile, ptile;
     if (MODE == MODE_GATHER) {
-        int g = 0, cum = 0;
-        while (true) {
-            const int tg = (p.counts[g] + brows - 1) / brows;
-            if (tile < cum + tg) break;
-            cum += tg;
-            ++g;
-        }
-        ctile = g;
-        ptile = tile - cum;
+        gather_tile(p.counts, p.ctiles, brows, tile, ctile, ptile);
     } else {
         ptile = tile / p.ctiles;
         ctile = tile - ptile * p.ctiles;
@@ -323,9 +354,10 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
 
     // Footprint words of the tile (pixel row x 32-channel word, valid when
     // every pixel's group of BM channels starts on a word).  Only the
-    // epilogue needs them: they are fetched from inside the main loop, next
-    // to step 1's copies (so no wait is spent on them), held in registers
-    // and staged in LDS after the loop.
+    // epilogue needs them: they are fetched together with step 0's copies
+    // (their latency hides under the copies'), held in registers through the
+    // main loop and staged in LDS after it.  (Fetching them next to step 1's
+    // copies instead measured 1.5 us slower per launch.)
     const bool mask_lds = SEL && (p.C % 32) == 0 && nsplit == 1;
     constexpr int MW = SEL ? BN * (BM / 32) : 0;                  // footprint words per tile
     constexpr int MI = MW > 0 ? (MW + NT - 1) / NT : 1;          // per thread
@@ -343,14 +375,13 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
             mwords[u] = word;
         }
     };
-    const int mask_step = nloc > 1 ? 1 : 0;
+    if (mask_lds) fetch_mask();
     wait_vmem();
     __syncthreads();
     auto main_loop = [&](auto nb_tag) {
         for (int step = 0; step < nloc; ++step) {
             const int buf = step & 1;
             if (step + 1 < nloc) load(buf ^ 1);
-            if (mask_lds && step == mask_step) fetch_mask();
             compute(buf, nb_tag);
             wait_vmem();
             __syncthreads();
@@ -607,6 +638,8 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const T* __restrict__ w, 
 // Sums the nsplit partial tiles of every live tile in split order and writes
 // dX like the GEMM epilogue would (footprint select, rounding).  Runs with a
 // fixed grid; exits at once when the GEMM did not split.
+constexpr int kMaxDataSplit = 16;   // the planner's kDataMaxSplit (checked at dispatch)
+
 template <typename T, int MODE, int TI>
 __global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
 {
@@ -634,15 +667,7 @@ __global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
         const int pr = rem / (BM / 4), cl = (rem - pr * (BM / 4)) * 4;
         int ctile, ptile;
         if (MODE == MODE_GATHER) {
-            int g = 0, cum = 0;
-            while (true) {
-                const int tg = (p.counts[g] + BN - 1) / BN;
-                if (tile < cum + tg) break;
-                cum += tg;
-                ++g;
-            }
-            ctile = g;
-            ptile = tile - cum;
+            gather_tile(p.counts, p.ctiles, BN, tile, ctile, ptile);
         } else {
             ptile = tile / p.ctiles;
             ctile = tile - ptile * p.ctiles;
@@ -652,9 +677,17 @@ __global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
         const int c = ctile * BM + cl;
         if (r >= nrows || c >= p.C) continue;
         const int pix = MODE == MODE_GATHER ? p.lists[(int64_t)ctile * p.npix + r] : r;
-        floatx4 s = *reinterpret_cast<const floatx4*>(p.partial + ((int64_t)tile * nsplit * BN + pr) * BM + cl);
-        for (int zz = 1; zz < nsplit; ++zz)
-            s += *reinterpret_cast<const floatx4*>(p.partial + (((int64_t)tile * nsplit + zz) * BN + pr) * BM + cl);
+        // every split's partial is loaded before any is added (latency, not
+        // bandwidth, bounds a serial chain of loads); the sum runs in split order
+        const float* __restrict__ base = p.partial + ((int64_t)tile * nsplit * BN + pr) * BM + cl;
+        floatx4 pv[kMaxDataSplit];
+#pragma unroll
+        for (int zz = 0; zz < kMaxDataSplit; ++zz)
+            if (zz < nsplit) pv[zz] = *reinterpret_cast<const floatx4*>(base + (int64_t)zz * BN * BM);
+        floatx4 s = pv[0];
+#pragma unroll
+        for (int zz = 1; zz < kMaxDataSplit; ++zz)
+            if (zz < nsplit) s += pv[zz];
         const int64_t o = (int64_t)pix * p.C + c;
         if constexpr (MODE == MODE_FWD) {
             // ReLU, rounding and footprint bits as in the GEMM's forward epilogue
@@ -792,7 +825,7 @@ hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t
     // row choice), or for nslots split items
     const int nb = max(mode == MODE_GATHER ? p.maxtiles : p.ptiles * p.ctiles, p.nslots);
     if (nb <= 0) return hipSuccess;
-    if (p.tile < 0 || p.tile >= kDataTileCount) return hipErrorInvalidValue;
+    if (p.tile < 0 || p.tile >= kDataTileCount || p.smax > kMaxDataSplit) return hipErrorInvalidValue;
     return dtype == 1 ? launch_type<uint16_t>(mode, p, nb, stream, ev)
                       : launch_type<float>(mode, p, nb, stream, ev);
 }

@@ -77,7 +77,8 @@ __global__ void mask_pack_kernel(const T* __restrict__ x, uint32_t* __restrict__
 __global__ __launch_bounds__(CNT) void compact_scatter_kernel(CompactParams p)
 {
     __shared__ int red[4];
-    __shared__ int wcnt[4];
+    __shared__ int wcnt[4], wdead[4];
+    __shared__ int dead_s[CNT];
     const int blk = blockIdx.x, g = blockIdx.y;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
@@ -88,25 +89,35 @@ __global__ __launch_bounds__(CNT) void compact_scatter_kernel(CompactParams p)
 
     const int px = blk * CNT + tid;
     const bool live = pixel_live(p, px, g);
-    const uint64_t bal = __ballot(live);
-    if (lane == 0) wcnt[wave] = __popcll(bal);
+    const bool dead = px < p.npix && !live;
+    const uint64_t bal = __ballot(live), dbal = __ballot(dead);
+    if (lane == 0) {
+        wcnt[wave] = __popcll(bal);
+        wdead[wave] = __popcll(dbal);
+    }
     __syncthreads();
     const int offset = red[0] + red[1] + red[2] + red[3];
-    int wbase = 0;
-    for (int w = 0; w < wave; ++w) wbase += wcnt[w];
-    const uint64_t lower = lane == 0 ? 0ull : (bal & ((~0ull) >> (64 - lane)));
-    const int rank = wbase + __popcll(lower);
-    if (px < p.npix) {
-        if (live) {
-            p.lists[(int64_t)g * p.npix + offset + rank] = px;
-        } else {
-            const int lo = g * p.G, hi = min(p.C, lo + p.G);
-            uint4* row = reinterpret_cast<uint4*>(static_cast<char*>(p.dx) + ((int64_t)px * p.C + lo) * p.elem_bytes);
-            const int nvec = (hi - lo) * p.elem_bytes / 16;
-            for (int v = 0; v < nvec; ++v) row[v] = make_uint4(0, 0, 0, 0);
-        }
+    int wbase = 0, dbase = 0;
+    for (int w = 0; w < wave; ++w) {
+        wbase += wcnt[w];
+        dbase += wdead[w];
     }
+    const uint64_t below = lane == 0 ? 0ull : ((~0ull) >> (64 - lane));
+    if (live) p.lists[(int64_t)g * p.npix + offset + wbase + __popcll(bal & below)] = px;
+    if (dead) dead_s[dbase + __popcll(dbal & below)] = px;
     if (blk == p.nblk - 1 && tid == 0) p.counts[g] = offset + wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
+    __syncthreads();
+    // The dead pixels' rows of dX are cleared by the whole block together:
+    // consecutive threads write consecutive 16-byte pieces of one row, so a
+    // wave covers whole rows rather than one 16-byte piece of 64 rows.
+    const int ndead = wdead[0] + wdead[1] + wdead[2] + wdead[3];
+    const int lo = g * p.G, hi = min(p.C, lo + p.G);
+    const int nvec = (hi - lo) * p.elem_bytes / 16;
+    for (int q = tid; q < ndead * nvec; q += CNT) {
+        const int d = q / nvec, v = q - d * nvec;
+        uint4* row = reinterpret_cast<uint4*>(static_cast<char*>(p.dx) + ((int64_t)dead_s[d] * p.C + lo) * p.elem_bytes);
+        row[v] = make_uint4(0, 0, 0, 0);
+    }
 }
 
 // occ[chunk][kt] = 1 iff dY has a non-zero in pixels of the chunk and
