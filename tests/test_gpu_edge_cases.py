@@ -176,3 +176,56 @@ def test_largest_addressable_tensors():
     o, a, nt = oracle.conv_bwd_weight_at(x64, dy64, (3, 3), co, (1, 1), (1, 1))
     g = part.cpu().numpy()[co[:, 0], co[:, 2], co[:, 3], co[:, 1]].astype(np.float64)
     check_values(g, o, a, nt, tol_for("bf16"), False, "dW of 16 images (sampled)")
+
+
+# Live-row counts that differ between channel groups, so the skipping call's
+# tile order (round by round across groups) runs past the rounds every group
+# fills: one group all live and one all dead; one group all live and one with
+# a third of its pixels live; three groups with 100%, 60% and 5% of their
+# pixels live.  With 8 images the few tiles split their reduction; with 32
+# images (112 tiles per full group) the last two cases run unsplit.
+UNEVEN = [("live_dead", 512, (1.0, 0.0)), ("live_third", 512, (1.0, 0.33)), ("three_groups", 768, (1.0, 0.6, 0.05))]
+
+
+@pytest.mark.parametrize("N", [8, 32])
+@pytest.mark.parametrize("name,C,fracs", UNEVEN, ids=[u[0] for u in UNEVEN])
+def test_uneven_group_counts(name, C, fracs, N):
+    _case("uneven group counts %s C=%d %s N=%d" % (name, C, fracs, N))
+    H, W, K = 28, 28, 64
+    rng = np.random.default_rng(41)
+    desc = cb.ConvDesc.make(N, C, H, W, K, 3, 3, 1, 1)
+    x = torch.from_numpy(np.abs(rng.standard_normal((N, H, W, C), dtype=np.float32))).to(torch.bfloat16)
+    # per group, a pixel is either live on every channel of the group or dead
+    # on all of them (each group is 256 channels wide)
+    live_px = np.stack([rng.random((N, H, W)) < f for f in fracs], -1)
+    keep = np.repeat(live_px, 256, axis=-1)
+    x = x * torch.from_numpy(keep)
+    w = torch.from_numpy(rng.standard_normal((K, 3, 3, C), dtype=np.float32) * 0.05).to(torch.bfloat16)
+    dy = torch.from_numpy(rng.standard_normal((N, H, W, K), dtype=np.float32)).to(torch.bfloat16)
+    xd, wd, dyd = x.cuda(), w.cuda(), dy.cuda()
+    xm = torch.zeros(cb.cbw_mask_words(desc), dtype=torch.int32, device="cuda")
+    cb.cbw_relu_mask_pack(desc, xd, xm)
+    dense, gat = torch.empty_like(xd), torch.full_like(xd, float("nan"))
+    cb.conv_bwd_data(desc, dyd, wd, dense, cb.workspace(desc, cb.CBW_OP_BWD_DATA))
+    ws = cb.workspace(desc, cb.CBW_OP_BWD_DATA_MASKED)
+    cb.conv_bwd_data_masked(desc, dyd, wd, xm, gat, ws, 0)
+    torch.cuda.synchronize()
+    st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_DATA_MASKED, ws)
+    assert st.rows_live == int(live_px.sum()), "live rows counted by the compaction"
+    live = xd > 0
+    gb, db = gat.view(torch.int16), dense.view(torch.int16)
+    assert not (gb[~live] != 0).any(), "killed outputs must be +0.0"
+    # values against the oracle at sampled live outputs (a split reduction sums
+    # in another order than the dense call, so only tolerance applies there)
+    lv = np.argwhere(live.cpu().numpy())
+    pick = lv[rng.choice(len(lv), size=min(3000, len(lv)), replace=False)]
+    coords = pick[:, [0, 3, 1, 2]].astype(np.int32)          # (n, c, h, w)
+    dy64 = oracle.nhwc_to_nchw(dy.double().numpy())
+    w64 = oracle.krsc_to_kcrs(w.double().numpy())
+    o, absd, nt = oracle.conv_bwd_data_at(dy64, w64, (H, W), coords, (1, 1), (1, 1))
+    g = gat.float().cpu().numpy()[pick[:, 0], pick[:, 1], pick[:, 2], pick[:, 3]].astype(np.float64)
+    check_values(g, o, absd, nt, tol_for("bf16"), True, name + " skipping dX (sampled live outputs)")
+    if N == 32 and name != "live_dead":
+        # neither call splits its reduction here (more than 128 tiles each):
+        # the same per-output summation order, so the same bits
+        assert torch.equal(gb[live], db[live]), "skipping call differs from the dense call at live outputs"
