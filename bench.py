@@ -233,6 +233,25 @@ def main():
     dist = {"hot": distribution(False), "cold": distribution(True)}
     del flush
 
+    # A caller's per-layer dispatch: from one earlier call's statistics, the
+    # data gradient compacts only when at most 90% of its pixel rows were
+    # live (else the same kernel applies the footprint in its epilogue,
+    # CBW_FLAG_NO_SKIP, with no compaction pass), and the weight gradient
+    # skips only when at least 5% of its blocks were skippable (else no
+    # occupancy pass).  Outputs are the same either way.
+    dx_skip, dw_skip = adaptive_choice(st_dx, st_dw)
+
+    def adaptive_step():
+        cb.conv_bwd_data_masked(desc, dy, w, xm, dx, ws_m, 0 if dx_skip else cb.CBW_FLAG_NO_SKIP)
+        if dw_skip:
+            cb.conv_bwd_weight_sparse(desc, x, dy, dym, dw, ws_w, 0)
+        else:
+            cb.conv_bwd_weight_sparse(desc, x, dy, None, dw, ws_w, cb.CBW_FLAG_NO_SKIP)
+
+    for _ in range(10):
+        adaptive_step()
+    ms_adaptive, _ = timed(adaptive_step, args.steps)
+
     # The semantic equivalent without output sparsity: the dense step followed
     # by a separate multiply of dX with the 0/1 ReLU derivative.
     relu_d = (x > 0).to(x.dtype)
@@ -353,6 +372,11 @@ def main():
         "kernels_ms": {"dx_gemm": round(ms_dx_gemm, 4), "dw_gemm": round(ms_dw_gemm, 4),
                        "step_with_events": round(ms_sparse_k, 4)},
         "step_distribution": dist,
+        "adaptive_dispatch": {"ms_per_step": round(ms_adaptive, 4), "speedup_vs_dense": round(ms_dense / ms_adaptive, 4),
+                              "dx_call": "compacting" if dx_skip else "non-skipping (footprint in the epilogue)",
+                              "dw_call": "skipping" if dw_skip else "non-skipping",
+                              "rule": "compact dX if <= 90% of rows were live, skip dW blocks if >= 5% were "
+                                      "skippable, from an earlier call's statistics"},
         "dense_plus_mask_multiply_ms": round(ms_dense_mask, 4),
         "speedup_vs_dense_plus_mask_multiply": round(ms_dense_mask / ms_sparse, 4),
         "nchw_boundary": {"sparse_step_ms": round(ms_nchw, 4), "added_ms": round(ms_nchw - ms_sparse, 4),
@@ -461,7 +485,39 @@ def layer_timing(cb, torch, spec, steps, warmup):
     rec["speedup_x_vs_dense"] = round(ms_d / ms_x, 4)
     rec["dw_blocks_executed_x"] = round(1.0 - st_x.blocks_skipped / max(st_x.blocks_total, 1), 4)
     rec["dw_split_balance_x"] = split_balance(work_x)
+    # the per-layer dispatch of the main line, decided from the stats above
+    st_dx = (cb.cbw_read_stats(desc, cb.CBW_OP_BWD_DATA_MASKED, ws_m)
+             if spec.need_dx and spec.masked else None)
+    dx_skip, dw_skip = adaptive_choice(st_dx, st)
+
+    def adaptive():
+        if spec.need_dx:
+            if spec.masked:
+                cb.conv_bwd_data_masked(desc, dy, w, xm, dx, ws_m, 0 if dx_skip else cb.CBW_FLAG_NO_SKIP)
+            else:
+                cb.conv_bwd_data(desc, dy, w, dx, ws_d)
+        if dw_skip:
+            cb.conv_bwd_weight_sparse(desc, x, dy, dym, dw, ws_w, 0)
+        else:
+            cb.conv_bwd_weight_sparse(desc, x, dy, None, dw, ws_w, cb.CBW_FLAG_NO_SKIP)
+
+    for _ in range(max(warmup // 4, 2)):
+        adaptive()
+    ms_a = min(tm(adaptive), tm(adaptive))
+    rec["adaptive_ms"] = round(ms_a, 4)
+    rec["speedup_adaptive_vs_dense"] = round(ms_d / ms_a, 4)
+    rec["adaptive_calls"] = "dX %s, dW %s" % ("compacting" if dx_skip else "non-skipping",
+                                              "skipping" if dw_skip else "non-skipping")
     return rec
+
+
+def adaptive_choice(st_dx, st_dw):
+    """Per-layer dispatch from an earlier call's statistics (None: no data
+    gradient): compact the data gradient when at most 90% of its pixel rows
+    were live, skip weight-gradient blocks when at least 5% were skippable."""
+    dx_skip = st_dx is not None and st_dx.rows_live <= 0.9 * st_dx.rows_total
+    dw_skip = st_dw.blocks_skipped >= 0.05 * max(st_dw.blocks_total, 1)
+    return dx_skip, dw_skip
 
 
 def split_balance(work):
