@@ -33,6 +33,8 @@ CASES = [
     ("c128_rows432", 27, 128, 64, 64, (128, 448, 432)),
     ("c64_rows480", 2, 64, 224, 224, (64, 512, 480)),
     ("c64_rows496", 31, 64, 64, 64, (64, 512, 496)),
+    ("c256_rows192_f32", 12, 256, 64, 64, (256, 224, 192)),
+    ("c256_rows208_f32", 32, 256, 56, 56, (256, 224, 208)),
 ]
 
 
@@ -57,10 +59,11 @@ def _coords(N, C, H, W, rng):
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_tile_rows_parity(case):
     name, N, C, H, W, expect = case
-    print("\n[case] tile rows %s N=%d C=K=%d %dx%d" % (name, N, C, H, W), flush=True)
-    spec = wl.LayerSpec(name, 2, 200 + CASES.index(case), N=N, C=C, H=H, W=W, K=C, R=3, S=3,
+    dtype = "f32" if name.endswith("_f32") else "bf16"
+    print("\n[case] tile rows %s N=%d C=K=%d %dx%d %s" % (name, N, C, H, W, dtype), flush=True)
+    spec = wl.LayerSpec(name, 2, 200 + CASES.index(case), N=N, C=C, H=H, W=W, K=C, R=3, S=3, dtype=dtype,
                         x_kind="shifted_gauss", x_param=0.25, dy_kind="bernoulli", dy_param=0.4)
-    desc = cb.ConvDesc.make(N, C, H, W, C, 3, 3, 1, 1)
+    desc = cb.ConvDesc.make(N, C, H, W, C, 3, 3, 1, 1, dtype=dtype)
     assert cb.cbw_data_tiling(desc) == expect
     t = wl.draw(spec)
     x, w, dy = (t[k].cuda() for k in ("x", "w", "dy"))
@@ -77,7 +80,8 @@ def test_tile_rows_parity(case):
     torch.cuda.synchronize()
 
     live = (x > 0)
-    db, sb, gb = (a.view(torch.int16) for a in (dense, sel, gat))
+    ity = torch.int16 if dtype == "bf16" else torch.int32
+    db, sb, gb = (a.view(ity) for a in (dense, sel, gat))
     for what, m in (("non-skipping", sb), ("skipping", gb)):
         assert not (m[~live] != 0).any(), "%s masked call: killed outputs must be +0.0" % what
         assert torch.equal(m[live], db[live]), "%s masked call differs from the dense call at live outputs" % what
@@ -87,11 +91,11 @@ def test_tile_rows_parity(case):
     x64 = oracle.nhwc_to_nchw(t["x"].double().numpy())
     w64 = oracle.krsc_to_kcrs(t["w"].double().numpy())
     dy64 = oracle.nhwc_to_nchw(t["dy"].double().numpy())
-    tol = tol_for("bf16")
+    tol = tol_for(dtype)
     o, absd, nt = oracle.conv_bwd_data_at(dy64, w64, (H, W), cx, (1, 1), (1, 1))
     g = dense.float().cpu().numpy()[cx[:, 0], cx[:, 2], cx[:, 3], cx[:, 1]].astype(np.float64)
-    e1 = check_values(g, o, absd, nt, tol, True, name + " dense dX (sampled)")
+    e1 = check_values(g, o, absd, nt, tol, dtype == "bf16", name + " dense dX (sampled)")
     z, a, n = oracle.conv_fwd_at(x64, w64, cx, (1, 1), (1, 1))
     gy = y.float().cpu().numpy()[cx[:, 0], cx[:, 2], cx[:, 3], cx[:, 1]].astype(np.float64)
-    e2 = check_values(gy, np.maximum(z, 0.0), a, n, tol, True, name + " forward (sampled)")
+    e2 = check_values(gy, np.maximum(z, 0.0), a, n, tol, dtype == "bf16", name + " forward (sampled)")
     print("  dX normwise %.3e, forward normwise %.3e" % (e1, e2), flush=True)
