@@ -17,10 +17,18 @@ The dense comparison step runs the same kernels with skipping off:
 Footprint packing (cbw_relu_mask_pack, cbw_nonzero_mask_pack) belongs to the
 forward pass and is timed separately.
 
+Timing: after the warm-up, sparse and dense steps are timed in --rounds
+alternating rounds (the order flips every round) of exactly --steps steps,
+each round between synchronizations; step times are the medians over rounds.
+
 Prints one JSON line.  value = dense-equivalent TFLOP/s of the sparse step,
 (F_conv(dX) + F_conv(dW)) / t, with F_conv = 2 N K P Q C R S per gradient;
 useful TFLOP/s counts only live outputs of dX (2 nnz(mask) K R S) and non-zero
-entries of dY for dW (2 nnz(dY) C R S).
+entries of dY for dW (2 nnz(dY) C R S).  roofline.frac is the dominant GEMM
+kernel's useful FLOPs over its duration against the 2.5 PFLOP/s bf16 peak
+(also against the measured peak, and the executed-FLOP rate beside it).  The
+same run checks the timed step's outputs against the oracle on sampled
+coordinates (exit status 1 on a mismatch) and times the VGG-16 stack.
 """
 import argparse
 import json
@@ -47,6 +55,10 @@ def parse():
     ap.add_argument("--sweep", choices=["config4", "config3", "config5", "config5_pooled", "elementwise"], default=None,
                     help="instead of the main line, time the sparse and dense steps over a workload set "
                          "(one JSON line per layer or density point)")
+    ap.add_argument("--rounds", type=int, default=5,
+                    help="alternating sparse/dense timing rounds of --steps steps each (medians reported)")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the measured-peak microbenchmarks")
+    ap.add_argument("--no-stack", action="store_true", help="skip the VGG-16 stack timing")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 256 MiB device copy three times (reference for HBM byte counters)")
     return ap.parse_args()
@@ -118,8 +130,9 @@ def main():
 
     def timed(fn, steps, per_kernel=False):
         """Mean ms per call of fn over `steps` back-to-back calls, HIP events
-        on the launch stream; optionally the mean duration of the data- and
-        weight-gradient GEMM kernels from events recorded around them."""
+        on the launch stream, synchronized on both sides; optionally the mean
+        duration of the data- and weight-gradient GEMM kernels from events the
+        library records around their dispatch."""
         evs = []
         if per_kernel:
             for _ in range(steps):
@@ -158,17 +171,25 @@ def main():
         dense_step()
     torch.cuda.synchronize()
 
-    log("timing %d sparse steps" % args.steps)
-    ms_sparse, _ = timed(sparse_step, args.steps)
-    log("timing %d dense steps" % args.steps)
-    ms_dense, _ = timed(dense_step, args.steps)
+    # Sparse and dense steps timed in alternating rounds (the order flips
+    # every round), each round exactly `steps` steps between synchronizations;
+    # the medians over rounds are the step times, so clock ramp-up after a
+    # short warm-up biases neither side.
+    log("timing %d rounds of %d sparse and %d dense steps" % (args.rounds, args.steps, args.steps))
+    per_round = alternate({"sparse": sparse_step, "dense": dense_step}, lambda fn: timed(fn, args.steps)[0],
+                          args.rounds)
+    ms_sparse = float(np.median(per_round["sparse"]))
+    ms_dense = float(np.median(per_round["dense"]))
     log("timing %d sparse steps with per-kernel events" % args.steps)
     ms_sparse_k, (ms_dx_gemm, ms_dw_gemm) = timed(sparse_step, args.steps, per_kernel=True)
+    _, (ms_dx_gemm_dense, ms_dw_gemm_dense) = timed(dense_step, args.steps, per_kernel=True)
 
     sparse_step()
     torch.cuda.synchronize()
     st_dx = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_DATA_MASKED, ws_m)
     st_dw = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws_w)
+    log("parity of the timed step's outputs against the oracle (sampled)")
+    parity = check_against_oracle(spec, t_cpu, dx, dw, x)
 
     nnz_mask = int(torch.count_nonzero(x > 0).item())
     nnz_dy = int(torch.count_nonzero(dy).item())
@@ -181,18 +202,40 @@ def main():
     exec_frac_dw = 1.0 - st_dw.blocks_skipped / max(st_dw.blocks_total, 1)
     f_exec = f_conv * exec_frac_dx + f_conv * exec_frac_dw
 
-    # dominant kernel: the longer of the two GEMMs
+    peaks = None
+    if not args.no_peaks:
+        log("measured peaks (matrix-core loop, HBM streams)")
+        peaks = measure_peaks(torch, stream)
+
+    # Dominant kernel: the longer of the two GEMMs.  `achieved` counts the
+    # useful FLOPs of its gradient (live dX outputs, or non-zero dY entries
+    # for dW), the figure the target is stated in; the executed
+    # (dense-equivalent over the rows and blocks actually run) rate is
+    # reported beside it.
     tiling = cb.cbw_data_tiling(desc)   # all pixels are live here, so the gather mode tiles alike
     kern = {"dx_gemm": ms_dx_gemm, "dw_gemm": ms_dw_gemm}
     dom = max(kern, key=kern.get)
-    dom_flops = f_conv * (exec_frac_dx if dom == "dx_gemm" else exec_frac_dw)
-    achieved = dom_flops / (kern[dom] * 1e-3) / 1e12
+    dom_useful = f_useful_dx if dom == "dx_gemm" else f_useful_dw
+    dom_exec = f_conv * (exec_frac_dx if dom == "dx_gemm" else exec_frac_dw)
+    achieved = dom_useful / (kern[dom] * 1e-3) / 1e12
+    achieved_exec = dom_exec / (kern[dom] * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_for(dom),
+                "flops": "useful: %s" % ("2 nnz(mask) K R S (live dX outputs)" if dom == "dx_gemm"
+                                         else "2 nnz(dY) C R S (non-zero dY entries)"),
                 "kernel": {"dx_gemm": "bwd_data_kernel<unsigned short, 2, true, 0> (bf16, gather, %d-channel x %d-pixel "
                                       "tiles of %d-row capacity)" % (tiling[0], tiling[2], tiling[1]),
                            "dw_gemm": "bwd_weight_tr_kernel<256> (bf16, 256-wide output-channel tile)"}[dom],
-                "kernel_ms": round(kern[dom], 4), "flops_per_launch": dom_flops}
+                "kernel_ms": round(kern[dom], 4), "flops_per_launch": dom_useful,
+                "executed": {"achieved": round(achieved_exec, 2),
+                             "frac": round(achieved_exec / PEAK_BF16_TFLOPS, 4), "flops_per_launch": dom_exec},
+                "step_useful_frac": round(useful / PEAK_BF16_TFLOPS, 4),
+                "step_dense_equiv_frac": round(dense_eq / PEAK_BF16_TFLOPS, 4)}
+    if peaks and "mfma_bf16_tflops" in peaks:
+        pk = peaks["mfma_bf16_tflops"]
+        roofline["measured_peak"] = {"tflops": pk, "frac": round(achieved / pk, 4),
+                                     "frac_executed": round(achieved_exec / pk, 4),
+                                     "step_useful_frac": round(useful / pk, 4)}
 
     # The forward convolution with the ReLU and the footprint fused (the
     # producer of this layer's footprint), timed as a whole call on the same layer.
@@ -209,26 +252,33 @@ def main():
     ms_fwd, _ = timed(fwd, args.steps)
     del y_fwd, ym_fwd, ws_f
 
-    # Per-step distribution, hot (operands left in the caches by the step
-    # before) and cold (the 256 MB last-level cache flushed by writing 512 MB
-    # before every step), each step bracketed by its own events.
+    # Per-step distribution of both steps, hot (operands left in the caches by
+    # the step before) and cold (the 256 MB last-level cache flushed by
+    # writing 512 MB before every step), each step bracketed by its own
+    # events; sparse and dense steps interleaved.
     log("per-step distribution, hot and cold")
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
 
     def distribution(cold, n=max(10, min(args.steps, 40))):
-        per = []
+        per = {"sparse": [], "dense": []}
         for i in range(n):
-            if cold:
-                flush.fill_(i & 0xFF)
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            sparse_step()
-            b.record(stream)
-            torch.cuda.synchronize()
-            per.append(a.elapsed_time(b))
-        q = np.percentile(per, [10, 50, 90])
-        return {"p10_ms": round(float(q[0]), 4), "median_ms": round(float(q[1]), 4),
-                "p90_ms": round(float(q[2]), 4), "steps": n}
+            for name, fn in (("sparse", sparse_step), ("dense", dense_step))[::(1 if i % 2 == 0 else -1)]:
+                if cold:
+                    flush.fill_(i & 0xFF)
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                fn()
+                b.record(stream)
+                torch.cuda.synchronize()
+                per[name].append(a.elapsed_time(b))
+        out = {}
+        for name, v in per.items():
+            q = np.percentile(v, [10, 50, 90])
+            out[name] = {"p10_ms": round(float(q[0]), 4), "median_ms": round(float(q[1]), 4),
+                         "p90_ms": round(float(q[2]), 4)}
+        out["speedup_median"] = round(out["dense"]["median_ms"] / out["sparse"]["median_ms"], 4)
+        out["steps"] = n
+        return out
 
     dist = {"hot": distribution(False), "cold": distribution(True)}
     del flush
@@ -248,10 +298,6 @@ def main():
         else:
             cb.conv_bwd_weight_sparse(desc, x, dy, None, dw, ws_w, cb.CBW_FLAG_NO_SKIP)
 
-    for _ in range(10):
-        adaptive_step()
-    ms_adaptive, _ = timed(adaptive_step, args.steps)
-
     # The semantic equivalent without output sparsity: the dense step followed
     # by a separate multiply of dX with the 0/1 ReLU derivative.
     relu_d = (x > 0).to(x.dtype)
@@ -262,8 +308,13 @@ def main():
         dense_dw()
 
     for _ in range(10):
+        adaptive_step()
         dense_mask_step()
-    ms_dense_mask, _ = timed(dense_mask_step, args.steps)
+    extra = alternate({"adaptive": adaptive_step, "dense_mask": dense_mask_step, "dense": dense_step},
+                      lambda fn: timed(fn, args.steps)[0], 3)
+    ms_adaptive = float(np.median(extra["adaptive"]))
+    ms_dense_mask = float(np.median(extra["dense_mask"]))
+    ms_dense_here = float(np.median(extra["dense"]))
     del relu_d
 
     # NCHW callers: the same step through the library's boundary transposes
@@ -289,6 +340,13 @@ def main():
         sparse_step_nchw()
     ms_nchw, _ = timed(sparse_step_nchw, args.steps)
     del x_n, dy_n, dx_n, xm_n, dym_n, ws_mn, ws_wn
+
+    # The largest configuration: the whole VGG-16 conv stack (13 layers,
+    # N = 32 at 224 x 224), inputs drawn on the device with the same recipe.
+    stack = None
+    if not args.no_stack:
+        log("VGG-16 stack (13 layers), inputs drawn on the device")
+        stack = vgg16_stack(cb, torch, max(3, args.steps // 4), args.rounds)
 
     # Context only: the same dense backward through torch's convolution
     # backward (MIOpen), on the same tensors viewed as channels-last NCHW.
@@ -366,13 +424,21 @@ def main():
         "useful_tflops": round(useful, 2),
         "speedup_vs_dense": round(ms_dense / ms_sparse, 4),
         "dense_ms_per_step": round(ms_dense, 4),
+        "timing": {"rounds": args.rounds, "steps_per_round": args.steps,
+                   "sparse_ms_per_round": [round(v, 4) for v in per_round["sparse"]],
+                   "dense_ms_per_round": [round(v, 4) for v in per_round["dense"]],
+                   "rule": "median over rounds; sparse and dense alternate, the order flipping every round"},
         "dense_equiv_tflops_dense_path": round(2 * f_conv / (ms_dense * 1e-3) / 1e12, 2),
         "executed_fraction": {"dx_rows": round(exec_frac_dx, 6), "dw_blocks": round(exec_frac_dw, 6)},
         "executed_tflops": round(f_exec / (ms_sparse * 1e-3) / 1e12, 2),
         "kernels_ms": {"dx_gemm": round(ms_dx_gemm, 4), "dw_gemm": round(ms_dw_gemm, 4),
+                       "dx_gemm_dense": round(ms_dx_gemm_dense, 4), "dw_gemm_dense": round(ms_dw_gemm_dense, 4),
                        "step_with_events": round(ms_sparse_k, 4)},
         "step_distribution": dist,
-        "adaptive_dispatch": {"ms_per_step": round(ms_adaptive, 4), "speedup_vs_dense": round(ms_dense / ms_adaptive, 4),
+        "parity": parity,
+        "adaptive_dispatch": {"ms_per_step": round(ms_adaptive, 4),
+                              "speedup_vs_dense": round(ms_dense_here / ms_adaptive, 4),
+                              "dense_ms_same_rounds": round(ms_dense_here, 4),
                               "dx_call": "compacting" if dx_skip else "non-skipping (footprint in the epilogue)",
                               "dw_call": "skipping" if dw_skip else "non-skipping",
                               "rule": "compact dX if <= 90% of rows were live, skip dW blocks if >= 5% were "
@@ -381,6 +447,8 @@ def main():
         "speedup_vs_dense_plus_mask_multiply": round(ms_dense_mask / ms_sparse, 4),
         "nchw_boundary": {"sparse_step_ms": round(ms_nchw, 4), "added_ms": round(ms_nchw - ms_sparse, 4),
                           "note": "NCHW activations through the boundary transposes; NHWC is native"},
+        "vgg16_stack": stack,
+        "measured_peaks": peaks,
         "miopen_context": miopen,
         "library_gemm_context": gemm_ctx,
         "mask_pack_ms": round(ms_pack, 4),
@@ -392,6 +460,211 @@ def main():
                          "simulated 32nm FP16 ASIC (not comparable hardware)",
     }
     print(json.dumps(out), flush=True)
+    if not parity["ok"]:
+        log("PARITY FAILURE: %s" % parity)
+        sys.exit(1)
+
+
+def alternate(fns, time_fn, rounds):
+    """Time each callable of `fns` once per round with time_fn, rotating the
+    order every round (round r starts at entry r mod len, so with two
+    entries the order flips).  Returns name -> list of per-round results."""
+    names = list(fns)
+    out = {n: [] for n in names}
+    for r in range(rounds):
+        k = r % len(names)
+        for n in names[k:] + names[:k]:
+            out[n].append(time_fn(fns[n]))
+    return out
+
+
+def check_against_oracle(spec, t, dx, dw, x, nsample=400):
+    """Sampled parity of the timed step's dX and dW against the oracle (the
+    same normwise bound the tests use), plus the exact zero pattern of dX
+    over the whole tensor: every output whose footprint bit is clear must be
+    the +0.0 pattern."""
+    import numpy as np
+    import torch
+    import oracle
+    rng = np.random.default_rng(771)
+    st, pd = (spec.stride,) * 2, (spec.pad,) * 2
+    tol = 2e-2 if spec.dtype == "bf16" else 1e-5
+    killed_nonzero = int(((dx.view(torch.int16) != 0) & ~(x > 0)).sum().item())
+    x64 = oracle.nhwc_to_nchw(t["x"].double().numpy())
+    dy64 = oracle.nhwc_to_nchw(t["dy"].double().numpy())
+    w64 = oracle.krsc_to_kcrs(t["w"].double().numpy())
+    cx = np.stack([rng.integers(0, m, nsample) for m in (spec.N, spec.C, spec.H, spec.W)], 1).astype(np.int32)
+    o, _, _ = oracle.conv_bwd_data_at(dy64, w64, (spec.H, spec.W), cx, st, pd)
+    live = x64[cx[:, 0], cx[:, 1], cx[:, 2], cx[:, 3]] > 0
+    o = np.where(live, o, 0.0)
+    g = dx.float().cpu().numpy()[cx[:, 0], cx[:, 2], cx[:, 3], cx[:, 1]].astype(np.float64)
+    e_dx = float(np.max(np.abs(g - o)) / max(np.max(np.abs(o)), 1e-300))
+    cw = np.stack([rng.integers(0, m, nsample) for m in (spec.K, spec.C, spec.R, spec.S)], 1).astype(np.int32)
+    o, _, _ = oracle.conv_bwd_weight_at(x64, dy64, (spec.R, spec.S), cw, st, pd)
+    g = dw.cpu().numpy()[cw[:, 0], cw[:, 2], cw[:, 3], cw[:, 1]].astype(np.float64)
+    e_dw = float(np.max(np.abs(g - o)) / max(np.max(np.abs(o)), 1e-300))
+    ok = killed_nonzero == 0 and e_dx <= tol and e_dw <= tol
+    return {"ok": bool(ok), "dx_normwise_err": e_dx, "dw_normwise_err": e_dw, "tol": tol,
+            "killed_outputs_not_plus_zero": killed_nonzero, "samples": nsample}
+
+
+def measure_peaks(torch, stream):
+    """Measured ceilings on this GPU: a bf16 matrix-core loop (16x16x32 and
+    32x32x16 instructions, four waves per SIMD, no memory traffic) and two
+    HBM streams over 1 GiB buffers (4x the last-level cache): read only, and
+    copy (bytes read + written).  Best of five launches each."""
+    import paper_2109_07710_amd.peaks as pk
+    dev = torch.device("cuda:0")
+    seed = torch.randn(pk.seed_bytes() // 2, device=dev).to(torch.bfloat16)
+    blocks = 256 * 4
+    sink = torch.zeros(pk.sink_words(blocks), dtype=torch.int32, device=dev)
+    res = {}
+
+    def best(launch, n=5):
+        for _ in range(2):
+            launch()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(n):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            launch()
+            b.record(stream)
+            torch.cuda.synchronize()
+            ms.append(a.elapsed_time(b))
+        return min(ms)
+
+    try:
+        iters = 8192
+        for shape, name in ((pk.MFMA_16X16X32, "16x16x32"), (pk.MFMA_32X32X16, "32x32x16")):
+            ms = best(lambda: pk.mfma(shape, blocks, iters, seed, sink, stream))
+            res["mfma_bf16_%s_tflops" % name] = round(pk.mfma_flops(shape, blocks, iters) / (ms * 1e-3) / 1e12, 1)
+        res["mfma_bf16_tflops"] = max(res["mfma_bf16_16x16x32_tflops"], res["mfma_bf16_32x32x16_tflops"])
+        nbytes = 1 << 30
+        src = torch.ones(nbytes // 4, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        ms = best(lambda: pk.hbm_read(src, sink, stream))
+        res["hbm_read_gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
+        ms = best(lambda: pk.hbm_copy(src, dst, stream))
+        res["hbm_copy_gbs"] = round(2 * nbytes / (ms * 1e-3) / 1e9, 1)
+        del src, dst
+        res["spec"] = {"mfma_bf16_tflops": PEAK_BF16_TFLOPS, "hbm_gbs": PEAK_HBM_GBS}
+        res["method"] = ("bf16 matrix loop: %d workgroups of 4 waves, %d rounds of 8 (16x16x32) or 4 (32x32x16) "
+                         "independent instructions per wave; HBM: 1 GiB streams; best of 5" % (blocks, iters))
+    except Exception as exc:  # the measurement is context: a failure leaves the spec peaks
+        res["error"] = str(exc)[:200]
+    return res
+
+
+def vgg16_stack(cb, torch, steps, rounds):
+    """The VGG-16 conv stack (13 layers, N = 32, 224 x 224 input) as one
+    step: every layer's sparse backward (masked dX where the footprint
+    applies, dense dX after a pool, no dX for conv1_1; skipping dW), against
+    the same layers' dense step and the per-layer dispatch.  Inputs drawn on
+    the device (workloads.draw_on_device, same recipe as the tests)."""
+    import numpy as np
+    import workloads as wl
+    dev = torch.device("cuda:0")
+    layers = []
+    for spec in wl.config5():
+        t = wl.draw_on_device(spec, dev)
+        x, w, dy = t["x"], t["w"], t["dy"]
+        desc = cb.ConvDesc.make(spec.N, spec.C, spec.H, spec.W, spec.K, spec.R, spec.S, spec.stride, spec.pad)
+        L = {"spec": spec, "desc": desc, "x": x, "w": w, "dy": dy,
+             "xm": torch.empty(cb.cbw_mask_words(desc), dtype=torch.int32, device=dev),
+             "dym": torch.empty(cb.cbw_dy_mask_words(desc), dtype=torch.int32, device=dev),
+             "dx": torch.empty_like(x) if spec.need_dx else None,
+             "dw": torch.empty((spec.K, spec.R, spec.S, spec.C), dtype=torch.float32, device=dev),
+             "ws_m": cb.workspace(desc, cb.CBW_OP_BWD_DATA_MASKED, dev) if spec.need_dx and spec.masked else None,
+             "ws_d": cb.workspace(desc, cb.CBW_OP_BWD_DATA, dev) if spec.need_dx else None,
+             "ws_w": cb.workspace(desc, cb.CBW_OP_BWD_WEIGHT, dev)}
+        cb.cbw_relu_mask_pack(desc, x, L["xm"])
+        cb.cbw_nonzero_mask_pack(desc.dtype, dy.numel(), dy, L["dym"])
+        true_c = spec.extra.get("true_c", spec.C)
+        L["useful"] = 2 * int(torch.count_nonzero(dy).item()) * true_c * spec.R * spec.S
+        L["dense_flops"] = spec.dense_flops() * (2 if spec.need_dx else 1)
+        if spec.need_dx:
+            L["useful"] += (2 * int(torch.count_nonzero(x > 0).item()) * spec.K * spec.R * spec.S
+                            if spec.masked else spec.dense_flops())
+        layers.append(L)
+
+    def sparse(L):
+        d, s = L["desc"], L["spec"]
+        if s.need_dx:
+            if s.masked:
+                cb.conv_bwd_data_masked(d, L["dy"], L["w"], L["xm"], L["dx"], L["ws_m"], 0)
+            else:
+                cb.conv_bwd_data(d, L["dy"], L["w"], L["dx"], L["ws_d"])
+        cb.conv_bwd_weight_sparse(d, L["x"], L["dy"], L["dym"], L["dw"], L["ws_w"], 0)
+
+    def dense(L):
+        d, s = L["desc"], L["spec"]
+        if s.need_dx:
+            cb.conv_bwd_data(d, L["dy"], L["w"], L["dx"], L["ws_d"])
+        cb.conv_bwd_weight_sparse(d, L["x"], L["dy"], None, L["dw"], L["ws_w"], cb.CBW_FLAG_NO_SKIP)
+
+    for L in layers:
+        sparse(L)
+    torch.cuda.synchronize()
+    for L in layers:
+        s = L["spec"]
+        st_dx = (cb.cbw_read_stats(L["desc"], cb.CBW_OP_BWD_DATA_MASKED, L["ws_m"])
+                 if s.need_dx and s.masked else None)
+        L["choice"] = adaptive_choice(st_dx, cb.cbw_read_stats(L["desc"], cb.CBW_OP_BWD_WEIGHT, L["ws_w"]))
+
+    def adaptive(L):
+        d, s = L["desc"], L["spec"]
+        dx_skip, dw_skip = L["choice"]
+        if s.need_dx:
+            if s.masked:
+                cb.conv_bwd_data_masked(d, L["dy"], L["w"], L["xm"], L["dx"], L["ws_m"],
+                                        0 if dx_skip else cb.CBW_FLAG_NO_SKIP)
+            else:
+                cb.conv_bwd_data(d, L["dy"], L["w"], L["dx"], L["ws_d"])
+        if dw_skip:
+            cb.conv_bwd_weight_sparse(d, L["x"], L["dy"], L["dym"], L["dw"], L["ws_w"], 0)
+        else:
+            cb.conv_bwd_weight_sparse(d, L["x"], L["dy"], None, L["dw"], L["ws_w"], cb.CBW_FLAG_NO_SKIP)
+
+    def tm(fn):
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps
+
+    kinds = {"sparse": sparse, "dense": dense, "adaptive": adaptive}
+    for _ in range(3):
+        for fn in kinds.values():
+            for L in layers:
+                fn(L)
+    whole = alternate({k: (lambda f=f: [f(L) for L in layers]) for k, f in kinds.items()}, tm, rounds)
+    res = {k: float(np.median(v)) for k, v in whole.items()}
+    per_layer = []
+    for L in layers:
+        r = alternate({k: (lambda f=f, L=L: f(L)) for k, f in kinds.items()}, tm, 3)
+        s = L["spec"]
+        per_layer.append({"layer": s.name, "C": s.extra.get("true_c", s.C), "K": s.K, "HW": s.H,
+                          "dx": "masked" if s.need_dx and s.masked else ("dense" if s.need_dx else "none"),
+                          **{k + "_ms": round(float(np.median(v)), 4) for k, v in r.items()}})
+    useful = sum(L["useful"] for L in layers)
+    dense_flops = sum(L["dense_flops"] for L in layers)
+    out = {"sparse_ms": round(res["sparse"], 4), "dense_ms": round(res["dense"], 4),
+           "adaptive_ms": round(res["adaptive"], 4),
+           "speedup_vs_dense": round(res["dense"] / res["sparse"], 4),
+           "adaptive_speedup_vs_dense": round(res["dense"] / res["adaptive"], 4),
+           "dense_equiv_tflops": round(dense_flops / (res["sparse"] * 1e-3) / 1e12, 2),
+           "useful_tflops": round(useful / (res["sparse"] * 1e-3) / 1e12, 2),
+           "useful_tflops_adaptive": round(useful / (res["adaptive"] * 1e-3) / 1e12, 2),
+           "dense_gflop": round(dense_flops / 1e9, 1), "useful_gflop": round(useful / 1e9, 1),
+           "steps_per_round": steps, "rounds": rounds, "layers": per_layer,
+           "inputs": "drawn on the device (workloads.draw_on_device), N=32, 224x224"}
+    del layers
+    torch.cuda.empty_cache()
+    return out
 
 
 def layer_timing(cb, torch, spec, steps, warmup):
@@ -445,17 +718,15 @@ def layer_timing(cb, torch, spec, steps, warmup):
         torch.cuda.synchronize()
         return a.elapsed_time(b) / steps
 
-    # Both steps are warmed up together (the clocks ramp up after the host-side
-    # input generation), then timed alternately; the faster of two rounds counts.
+    # The steps are warmed up together (the clocks ramp up after the host-side
+    # input generation), then timed in alternating rounds; medians count.
     for _ in range(warmup):
         sparse()
         sparse_x()
         dense()
-    ms_s, ms_x, ms_d = float("inf"), float("inf"), float("inf")
-    for _ in range(2):
-        ms_s = min(ms_s, tm(sparse))
-        ms_x = min(ms_x, tm(sparse_x))
-        ms_d = min(ms_d, tm(dense))
+    import numpy as np
+    rr = alternate({"s": sparse, "x": sparse_x, "d": dense}, tm, 3)
+    ms_s, ms_x, ms_d = (float(np.median(rr[k])) for k in ("s", "x", "d"))
     sparse_x()
     st_x = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws_w)
     work_x = cb.cbw_read_weight_work(desc, ws_w)
@@ -470,6 +741,16 @@ def layer_timing(cb, torch, spec, steps, warmup):
     f = spec.dense_flops()
     nflops = f * (2 if spec.need_dx else 1)
     rec["dense_equiv_tflops"] = round(nflops / (ms_s * 1e-3) / 1e12, 2)
+    # HBM roofline: the algorithmic bytes of the step against 8 TB/s (the
+    # bound for the 1x1 layers, whose arithmetic intensity is far below the
+    # ridge) next to the matrix-core floor of its dense-equivalent FLOPs
+    nbytes = step_bytes(spec)
+    rec["algorithmic_mb"] = round(nbytes / 1e6, 2)
+    rec["hbm_floor_ms"] = round(nbytes / (PEAK_HBM_GBS * 1e9) * 1e3, 4)
+    rec["mfma_floor_ms"] = round(nflops / (PEAK_BF16_TFLOPS * 1e12) * 1e3, 4)
+    rec["bound"] = "hbm" if rec["hbm_floor_ms"] > rec["mfma_floor_ms"] else "mfma"
+    rec["hbm_frac"] = round(rec["hbm_floor_ms"] / ms_s, 4)
+    rec["mfma_frac_dense_equiv"] = round(rec["mfma_floor_ms"] / ms_s, 4)
     useful = 2 * int(torch.count_nonzero(dy).item()) * spec.extra.get("true_c", spec.C) * spec.R * spec.S
     if spec.need_dx:
         useful += (2 * int(torch.count_nonzero(x > 0).item()) * spec.K * spec.R * spec.S if spec.masked else f)
@@ -503,12 +784,27 @@ def layer_timing(cb, torch, spec, steps, warmup):
 
     for _ in range(max(warmup // 4, 2)):
         adaptive()
-    ms_a = min(tm(adaptive), tm(adaptive))
+    ra = alternate({"a": adaptive, "d": dense}, tm, 3)
+    ms_a = float(np.median(ra["a"]))
     rec["adaptive_ms"] = round(ms_a, 4)
     rec["speedup_adaptive_vs_dense"] = round(ms_d / ms_a, 4)
     rec["adaptive_calls"] = "dX %s, dW %s" % ("compacting" if dx_skip else "non-skipping",
                                               "skipping" if dw_skip else "non-skipping")
     return rec
+
+
+def step_bytes(spec):
+    """Algorithmic HBM bytes of one backward step of a layer: every operand
+    read once and every result written once (dX: dY, W, the footprint bits
+    when masked, dX; dW: X, dY, dW in fp32)."""
+    e = 2 if spec.dtype == "bf16" else 4
+    npix, npq = spec.N * spec.H * spec.W, spec.N * spec.P * spec.Q
+    b = npix * spec.C * e + npq * spec.K * e + spec.K * spec.R * spec.S * spec.C * 4
+    if spec.need_dx:
+        b += npq * spec.K * e + spec.K * spec.R * spec.S * spec.C * e + npix * spec.C * e
+        if spec.masked:
+            b += (npix * spec.C + 7) // 8
+    return b
 
 
 def adaptive_choice(st_dx, st_dw):

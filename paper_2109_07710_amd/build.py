@@ -3,7 +3,8 @@
     python -m paper_2109_07710_amd.build
 
 Every source is compiled by hipcc for gfx950 only, with packed fp32
-instructions disabled, and linked into paper_2109_07710_amd/libconvbwd.so.
+instructions disabled, and linked into paper_2109_07710_amd/libconvbwd.so;
+the benchmark's peak-measurement kernels go into libcbwpeaks.so.
 """
 import concurrent.futures
 import os
@@ -14,6 +15,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libconvbwd.so")
+# measured machine ceilings for the benchmark's roofline (include/cbw_peaks.h)
+PEAKS_LIB = os.path.join(HERE, "libcbwpeaks.so")
+PEAKS_SOURCES = ["peaks.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["api.cpp", "plan.cpp", "bwd_data.hip", "bwd_weight.hip", "mask_kernels.hip", "elementwise.hip", "layout.hip"]
@@ -39,11 +43,8 @@ def _compile(src, verbose):
     return obj
 
 
-def build(verbose=False):
-    os.makedirs(BUILD, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, lib, verbose):
+    tmp = lib + ".tmp"
     # -z defs: a symbol missing from the objects fails the link here rather
     # than the library's load on the device host
     cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-Wl,-z,defs", "-o", tmp] + objs
@@ -51,8 +52,17 @@ def build(verbose=False):
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
-        raise RuntimeError("link failed\n" + r.stderr)
-    os.replace(tmp, LIB)
+        raise RuntimeError("link failed (%s)\n%s" % (os.path.basename(lib), r.stderr))
+    os.replace(tmp, lib)
+
+
+def build(verbose=False):
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = SOURCES + PEAKS_SOURCES
+    with concurrent.futures.ThreadPoolExecutor(max_workers=len(srcs)) as ex:
+        objs = dict(zip(srcs, ex.map(lambda s: _compile(s, verbose), srcs)))
+    _link([objs[s] for s in SOURCES], LIB, verbose)
+    _link([objs[s] for s in PEAKS_SOURCES], PEAKS_LIB, verbose)
     return LIB
 
 

@@ -246,3 +246,22 @@ def test_data_tiling_rejects_bad_descriptors(L):
     d.P += 1
     z = ctypes.c_int32(0)
     assert L.cbw_data_tiling(ctypes.byref(d), ctypes.byref(z), None, None) == cb.CBW_ERR_INVALID_ARG
+
+
+def test_peaks_library_exports_its_header():
+    import paper_2109_07710_amd.peaks as pk
+    if not os.path.exists(pk.LIB_PATH):
+        pytest.skip("library not built")
+    text = open(os.path.join(ROOT, "include", "cbw_peaks.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M))
+    assert names == {"cbw_peak_seed_bytes", "cbw_peak_sink_words", "cbw_peak_mfma_flops", "cbw_peak_mfma",
+                     "cbw_peak_hbm_read", "cbw_peak_hbm_copy"}
+    PL = pk.lib()
+    for n in names:
+        assert hasattr(PL, n), n
+    # host-only queries and argument checks (nothing is launched on an error)
+    assert pk.mfma_flops(pk.MFMA_16X16X32, 2, 3) == 2 * 16 * 16 * 32 * 8 * 3 * 2 * 4
+    assert pk.mfma_flops(pk.MFMA_32X32X16, 1, 1) == 2 * 32 * 32 * 16 * 4 * 4
+    assert PL.cbw_peak_mfma(7, 1, 1, None, None, None) == -1
+    assert PL.cbw_peak_hbm_copy(None, None, 16, None) == -1

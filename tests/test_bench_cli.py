@@ -25,3 +25,26 @@ def test_adaptive_choice():
     assert bench.adaptive_choice(st(90, 100), wt(5, 100)) == (True, True)        # at the thresholds
     assert bench.adaptive_choice(st(91, 100), wt(4, 100)) == (False, False)
     assert bench.adaptive_choice(None, wt(50, 100)) == (False, True)             # no data gradient
+
+
+def test_alternate_rotates_the_order():
+    import bench
+    calls = []
+    out = bench.alternate({"a": "a", "b": "b"}, lambda f: calls.append(f) or len(calls), 4)
+    assert calls == ["a", "b", "b", "a", "a", "b", "b", "a"]
+    assert out["a"] == [1, 4, 5, 8] and out["b"] == [2, 3, 6, 7]
+    calls.clear()
+    bench.alternate({"a": "a", "b": "b", "c": "c"}, lambda f: calls.append(f), 3)
+    assert calls == ["a", "b", "c", "b", "c", "a", "c", "a", "b"]
+
+
+def test_step_bytes_of_the_bench_layer():
+    """Algorithmic bytes of the benchmark layer: dX 107.2 MB (dY, W, footprint
+    bits, dX) and dW 105.1 MB (X, dY, fp32 dW)."""
+    import bench
+    import workloads as wl
+    spec = wl.config2()[0]
+    act = 32 * 56 * 56 * 256 * 2
+    w = 256 * 9 * 256
+    assert bench.step_bytes(spec) == (act + 2 * w + act // 16 + act) + (act + act + 4 * w)
+    assert abs(bench.step_bytes(spec) / 1e6 - 212.27) < 0.01

@@ -136,3 +136,27 @@ def test_config5_pooled_inputs():
 def test_dense_flops_config2():
     s = wl.config2()[0]
     assert s.dense_flops() == 2 * 32 * 256 * 56 * 56 * 256 * 9
+
+
+def test_draw_on_device_vgg_recipes_on_the_host():
+    """The device-side generator (used for the VGG-16 stack inside the
+    benchmark) follows the recipes: post-pool inputs are 2x2 maxima of a
+    ReLU output of density d (density 1 - (1 - d)^4), max-pool-routed dY has
+    at most one live position per 2x2 window, and the image's padded
+    channels are exactly zero.  Run with the CPU generator at reduced size."""
+    specs = wl.config5(N=2, scale=8)
+    d = wl.draw_on_device(specs[2], device="cpu")          # conv2_1: pooled input
+    dens_in = wl.vgg_density(2)
+    x_live = (d["x"].float() > 0).float().mean().item()
+    assert abs(x_live - (1 - (1 - dens_in) ** 4)) < 0.02
+    d = wl.draw_on_device(specs[1], device="cpu")          # conv1_2: followed by a pool
+    live = d["dy"].float() != 0
+    n, p, q, k = live.shape
+    per_win = live.view(n, p // 2, 2, q // 2, 2, k).sum(dim=(2, 4))
+    assert per_win.max().item() <= 1
+    d_l = wl.vgg_density(2)
+    assert abs(per_win.float().mean().item() - (1 - (1 - d_l) ** 4)) < 0.02
+    d = wl.draw_on_device(specs[0], device="cpu")          # conv1_1: 3 channels stored as 8
+    assert d["x"].shape[-1] == 8 and not d["x"][..., 3:].any() and not d["w"][..., 3:].any()
+    assert d["x"][..., :3].any()
+    assert d["dy"].dtype == torch.bfloat16

@@ -225,22 +225,44 @@ def draw(spec: LayerSpec, want=("x", "w", "dy")):
 def draw_on_device(spec: LayerSpec, device="cuda"):
     """The layer's tensors drawn directly in device memory with torch's
     seeded device generator: for sizes whose host-side generation would take
-    minutes (the largest tensors a buffer descriptor can address).  Same
-    recipe as draw() for "shifted_gauss" X and "bernoulli" dY (values differ
-    from draw(): another generator).  bf16 only."""
-    assert spec.dtype == "bf16" and spec.x_kind == "shifted_gauss" and spec.dy_kind == "bernoulli"
+    minutes (the largest tensors a buffer descriptor can address, the VGG-16
+    stack inside the benchmark).  Same recipe as draw() for "shifted_gauss"
+    and "pooled_gauss" X, "bernoulli" dY (with the max-pool routing of
+    spec.extra["maxpool_route"]) and zero-padded image channels; the values
+    differ from draw() (another generator).  bf16 only."""
+    assert spec.dtype == "bf16" and spec.x_kind in ("shifted_gauss", "pooled_gauss") and spec.dy_kind == "bernoulli"
     g = torch.Generator(device=device)
     g.manual_seed(ROOT_SEED * 1000 + spec.config_id * 100 + spec.layer_id)
     n, c, h, w_, k = spec.N, spec.C, spec.H, spec.W, spec.K
-    x = torch.randn((n, h, w_, c), generator=g, device=device, dtype=torch.float32)
-    x.sub_(spec.x_param).clamp_(min=0.0)
-    x = x.to(torch.bfloat16)
+    c_store, c = c, spec.extra.get("true_c", c)
+    if spec.x_kind == "shifted_gauss":
+        x = torch.randn((n, h, w_, c), generator=g, device=device, dtype=torch.float32)
+        x.sub_(spec.x_param).clamp_(min=0.0)
+    else:
+        # the previous layer's ReLU output at twice the size, max-pooled 2x2
+        z = torch.randn((n, 2 * h, 2 * w_, c), generator=g, device=device, dtype=torch.float32)
+        z.sub_(spec.x_param).clamp_(min=0.0)
+        x = z.view(n, h, 2, w_, 2, c).amax(dim=(2, 4))
+        del z
     wt = torch.randn((k, spec.R, spec.S, c), generator=g, device=device, dtype=torch.float32)
     wt.mul_(sqrt(2.0 / (c * spec.R * spec.S)))
+    if c_store != c:
+        x = torch.nn.functional.pad(x, (0, c_store - c))
+        wt = torch.nn.functional.pad(wt, (0, c_store - c))
+    x = x.to(torch.bfloat16)
     wt = wt.to(torch.bfloat16)
-    dy = torch.randn((n, spec.P, spec.Q, k), generator=g, device=device, dtype=torch.float32)
-    live = torch.rand((n, spec.P, spec.Q, k), generator=g, device=device) < spec.dy_param
-    dy.mul_(live)
+    p, q = spec.P, spec.Q
+    dy = torch.randn((n, p, q, k), generator=g, device=device, dtype=torch.float32)
+    live = torch.rand((n, p, q, k), generator=g, device=device) < spec.dy_param
+    if spec.extra.get("maxpool_route"):
+        # at most one live position per 2x2 window, chosen uniformly
+        win = live.view(n, p // 2, 2, q // 2, 2, k).any(dim=4).any(dim=2)
+        pick = torch.randint(0, 4, win.shape, generator=g, device=device)
+        routed = torch.zeros((n, p // 2, 2, q // 2, 2, k), dtype=torch.bool, device=device)
+        for i in range(4):
+            routed[:, :, i // 2, :, i % 2, :] = win & (pick == i)
+        live = routed.view(n, p, q, k)
+        del win, pick, routed
     dy.masked_fill_(~live, 0.0)          # +0.0 where dead
     dy = dy.to(torch.bfloat16)
     return {"x": x, "w": wt, "dy": dy}
