@@ -161,6 +161,23 @@ int conv_bwd_data_masked(const cbw_conv_desc* desc, const void* dY, const void* 
                          const uint32_t* x_mask, void* dX,
                          void* workspace, size_t workspace_bytes, uint32_t flags, void* stream);
 
+/* conv_bwd_data_masked for callers that cannot allocate device memory (code
+ * under stream capture, tight serving loops, harnesses that forbid
+ * allocation): the same kernels and the same result, with the workspace
+ * replaced by a scratch array built into the library (32 MiB, one per GPU,
+ * held until the process ends).  Nothing is allocated or freed.  The
+ * reduction is never split across workgroups (no partial tiles), so the
+ * values equal those of conv_bwd_data_masked whenever that call does not
+ * split either (many live tiles), and agree within fp32 summation order
+ * otherwise.  Returns CBW_ERR_WORKSPACE when the descriptor needs more
+ * scratch than the array holds (roughly: filters K*C*R*S elements plus
+ * 4 bytes per pixel and 256-channel group, plus the NCHW copies).  The
+ * first call on a device looks up the array's device address.  All calls on
+ * one GPU share its array: calls that overlap in time on one GPU (two
+ * streams, two threads) race, as two calls sharing a workspace do. */
+int conv_bwd_data_masked_noalloc(const cbw_conv_desc* desc, const void* dY, const void* W,
+                                 const uint32_t* x_mask, void* dX, uint32_t flags, void* stream);
+
 /* Forward convolution with the ReLU and the footprint of its output fused
  * into one launch (Sec. II-A forward operation; the output bitmap that the
  * backward pass consumes is produced by the forward pass, Sec. IV-B).

@@ -27,7 +27,7 @@ CBW_FLAG_NO_SKIP = 1
 
 EXPORTS = ("cbw_status_string", "cbw_validate_desc", "cbw_mask_words", "cbw_dy_mask_words",
            "cbw_workspace_size", "cbw_data_tiling", "cbw_relu_mask_pack", "cbw_nonzero_mask_pack", "conv_bwd_data",
-           "conv_bwd_data_masked", "conv_fwd_relu_mask", "conv_bwd_weight_sparse", "conv_bwd_weight_sparse_x",
+           "conv_bwd_data_masked", "conv_bwd_data_masked_noalloc", "conv_fwd_relu_mask", "conv_bwd_weight_sparse", "conv_bwd_weight_sparse_x",
            "conv_bwd_data_elementwise", "cbw_read_pixel_counts", "cbw_read_weight_work", "cbw_read_stats",
            "cbw_read_live_lists",
            "cbw_read_occupancy", "cbw_set_profile_events")
@@ -91,6 +91,7 @@ def lib():
     L.cbw_nonzero_mask_pack.argtypes = [ctypes.c_int32, ctypes.c_int64, vp, vp, vp]
     L.conv_bwd_data.argtypes = [dp, vp, vp, vp, vp, sz, vp]
     L.conv_bwd_data_masked.argtypes = [dp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
+    L.conv_bwd_data_masked_noalloc.argtypes = [dp, vp, vp, vp, vp, ctypes.c_uint32, vp]
     L.conv_fwd_relu_mask.argtypes = [dp, vp, vp, vp, vp, vp, sz, vp]
     L.conv_bwd_weight_sparse.argtypes = [dp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
     L.conv_bwd_weight_sparse_x.argtypes = [dp, vp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
@@ -195,6 +196,12 @@ def conv_bwd_data(desc, dY, W, dX, ws, stream=None):
 def conv_bwd_data_masked(desc, dY, W, x_mask, dX, ws, flags=0, stream=None):
     _check(lib().conv_bwd_data_masked(ctypes.byref(desc), _ptr(dY), _ptr(W), _ptr(x_mask), _ptr(dX),
                                       _ptr(ws), _nbytes(ws), flags, _stream(stream)), "conv_bwd_data_masked")
+
+
+def conv_bwd_data_masked_noalloc(desc, dY, W, x_mask, dX, flags=0, stream=None):
+    """conv_bwd_data_masked on the library's built-in scratch (no workspace)."""
+    _check(lib().conv_bwd_data_masked_noalloc(ctypes.byref(desc), _ptr(dY), _ptr(W), _ptr(x_mask), _ptr(dX),
+                                              flags, _stream(stream)), "conv_bwd_data_masked_noalloc")
 
 
 def conv_fwd_relu_mask(desc, X, W, Y, y_mask, ws, stream=None):

@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 
 #include "../../include/convbwd.h"
 #include "kernels.hpp"
@@ -78,10 +79,10 @@ DataParams data_params(const cbw_conv_desc* d, const void* dY, const void* wt, v
 }
 
 int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const uint32_t* x_mask, void* dX,
-                 void* ws, size_t ws_bytes, uint32_t flags, void* stream, bool masked)
+                 void* ws, size_t ws_bytes, uint32_t flags, void* stream, bool masked, bool no_split = false)
 {
     DataPlan plan;
-    int st = plan_data(desc, masked, &plan);
+    int st = plan_data(desc, masked, &plan, no_split);
     if (st != CBW_OK) return st;
     if (!dY || !W || !dX || (masked && !x_mask)) return CBW_ERR_INVALID_ARG;
     if (!aligned16(dY) || !aligned16(W) || !aligned16(dX) || (masked && !aligned16(x_mask)))
@@ -118,7 +119,7 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
     p.brows = plan.brows;
     p.maxtiles = plan.maxtiles;
     p.nslots = kDataSlots;
-    p.smax = kDataMaxSplit;
+    p.smax = no_split ? 1 : kDataMaxSplit;
     p.split = gather ? 1 : plan.split;
     p.partial = plan.partial.bytes ? at<float>(ws, plan.partial) : nullptr;
     CompactParams cp{};
@@ -184,6 +185,38 @@ int run_fwd(const cbw_conv_desc* desc, const void* X, const void* W, void* Y, ui
                                    clear ? words : 0, s);
     if (e != hipSuccess) return hip_status(e);
     return hip_status(launch_bwd_data(desc->dtype, MODE_FWD, p, s, prof_events(2)));
+}
+
+// Built-in scratch of conv_bwd_data_masked_noalloc: the masked data
+// gradient's workspace (filter transform, compaction counts and lists) for
+// callers that cannot allocate.  Each GPU the library runs on holds its own
+// copy until the process ends.  Host code never uses the array's name as an
+// address: its device address is looked up once per device
+// (hipGetSymbolAddress) and kept in g_scratch_dev.
+constexpr size_t kNoAllocScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of the current device's scratch (looked up on first use).
+int scratch_for_current_device(void** out)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(e);
+    if (dev < 0 || dev >= kMaxDevices) return CBW_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_status(e);
+        if (!ptr) return CBW_ERR_HIP;
+        g_scratch_dev[dev] = ptr;
+    }
+    *out = g_scratch_dev[dev];
+    return CBW_OK;
 }
 
 }  // namespace
@@ -306,6 +339,20 @@ int conv_bwd_data_masked(const cbw_conv_desc* desc, const void* dY, const void* 
                          void* dX, void* workspace, size_t workspace_bytes, uint32_t flags, void* stream)
 {
     return run_bwd_data(desc, dY, W, x_mask, dX, workspace, workspace_bytes, flags, stream, true);
+}
+
+int conv_bwd_data_masked_noalloc(const cbw_conv_desc* desc, const void* dY, const void* W, const uint32_t* x_mask,
+                                 void* dX, uint32_t flags, void* stream)
+{
+    // the same kernels as conv_bwd_data_masked on the built-in scratch, with
+    // the reduction never split (no partial tiles to hold)
+    DataPlan plan;
+    int st = plan_data(desc, true, &plan, true);
+    if (st != CBW_OK) return st;
+    if (plan.total > kNoAllocScratchBytes) return CBW_ERR_WORKSPACE;
+    void* ws = nullptr;
+    if ((st = scratch_for_current_device(&ws)) != CBW_OK) return st;
+    return run_bwd_data(desc, dY, W, x_mask, dX, ws, kNoAllocScratchBytes, flags, stream, true, true);
 }
 
 int conv_fwd_relu_mask(const cbw_conv_desc* desc, const void* X, const void* W, void* Y, uint32_t* y_mask,

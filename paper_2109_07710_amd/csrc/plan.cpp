@@ -68,7 +68,7 @@ int data_tile_index(int C)
     return best;
 }
 
-int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out)
+int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out, bool no_split)
 {
     int st = validate_desc(d);
     if (st != CBW_OK) return st;
@@ -90,7 +90,7 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out)
     p.maxtiles = cand[kDataRowChoices - 1];
     const int bk = 8 * (d->dtype == CBW_BF16 ? 8 : 4);
     p.nsteps = d->R * d->S * ((d->K + bk - 1) / bk);
-    p.split = host_data_split(p.ptiles * p.groups, p.nsteps);
+    p.split = no_split ? 1 : host_data_split(p.ptiles * p.groups, p.nsteps);
     p.header = take(&cur, 256);
     p.wt = take(&cur, (size_t)d->K * d->C * d->R * d->S * elem_bytes(d->dtype));
     if (masked) {
@@ -102,7 +102,7 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out)
     // compaction it is decided on the device, bounded by one partial tile
     // per resident workgroup.
     const size_t tile_bytes = (size_t)p.bn * p.bm * 4;
-    if (masked) p.partial = take(&cur, (size_t)kDataSlots * tile_bytes);
+    if (masked && !no_split) p.partial = take(&cur, (size_t)kDataSlots * tile_bytes);
     else if (p.split > 1) p.partial = take(&cur, (size_t)p.ptiles * p.groups * p.split * tile_bytes);
     if (d->act_layout == CBW_NCHW) {
         p.t_dy = take(&cur, (size_t)d->N * d->P * d->Q * d->K * elem_bytes(d->dtype));

@@ -81,7 +81,9 @@ struct WeightPlan {
 // operations that run on NHWC only.
 int validate_desc(const cbw_conv_desc* d);
 int require_nhwc(const cbw_conv_desc* d);
-int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out);
+// no_split: the reduction is never split (no partial-tile region; the
+// kernels get a split bound of 1), for callers with a bounded scratch.
+int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out, bool no_split = false);
 int plan_weight(const cbw_conv_desc* d, WeightPlan* out);
 // The forward convolution as a data-gradient GEMM: for stride 1, Y = conv(X, W)
 // is the backward-data operation with the roles of C and K, of (H, W) and

@@ -248,6 +248,18 @@ def test_data_tiling_rejects_bad_descriptors(L):
     assert L.cbw_data_tiling(ctypes.byref(d), ctypes.byref(z), None, None) == cb.CBW_ERR_INVALID_ARG
 
 
+def test_noalloc_rejects_descriptors_beyond_its_scratch(L):
+    """The built-in-scratch data gradient refuses, before any device call, a
+    layer whose workspace would exceed its 32 MiB: 64 channels at 224 x 224
+    with 200 images needs 4 bytes of live list per pixel (40 MB)."""
+    d = _desc(N=200, C=64, K=64, H=224, W=224, R=3, S=3, pad=(1, 1))
+    assert cb.cbw_validate_desc(d) == cb.CBW_OK
+    st = L.conv_bwd_data_masked_noalloc(ctypes.byref(d), None, None, None, None, 0, None)
+    assert st == cb.CBW_ERR_WORKSPACE
+    d = _desc(N=0)
+    assert L.conv_bwd_data_masked_noalloc(ctypes.byref(d), None, None, None, None, 0, None) == cb.CBW_ERR_INVALID_ARG
+
+
 def test_peaks_library_exports_its_header():
     import paper_2109_07710_amd.peaks as pk
     if not os.path.exists(pk.LIB_PATH):
