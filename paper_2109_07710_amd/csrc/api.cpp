@@ -91,7 +91,9 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
     if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;
     hipStream_t s = static_cast<hipStream_t>(stream);
 
-    const bool gather = masked && !(flags & CBW_FLAG_NO_SKIP);
+    // compaction needs at most kGatherMaxGroups channel groups; wider layers
+    // keep the footprint select without it
+    const bool gather = masked && !(flags & CBW_FLAG_NO_SKIP) && plan.groups <= kGatherMaxGroups;
     const int mode = !masked ? MODE_DENSE : (gather ? MODE_GATHER : MODE_SELECT);
     hipError_t e;
     void* dX_out = dX;
@@ -120,14 +122,12 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
     p.maxtiles = plan.maxtiles;
     p.nslots = kDataSlots;
     p.smax = no_split ? 1 : kDataMaxSplit;
-    p.split = gather ? 1 : plan.split;
+    p.split = plan.split;   // gather mode: the split of its dense tiles, which it checks on the device
     p.partial = plan.partial.bytes ? at<float>(ws, plan.partial) : nullptr;
     CompactParams cp{};
     if (gather) {
         cp.mask = x_mask;
         cp.blk_counts = at<int32_t>(ws, plan.blk_counts);
-        cp.counts = at<int32_t>(ws, plan.counts);
-        cp.lists = at<int32_t>(ws, plan.lists);
         cp.dx = dX;
         cp.npix = (int)plan.npix;
         cp.C = desc->C;
@@ -135,13 +135,14 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
         cp.groups = plan.groups;
         cp.nblk = plan.nblk;
         cp.elem_bytes = elem_bytes(desc->dtype);
-        p.lists = cp.lists;
-        p.counts = cp.counts;
+        p.blk_counts = cp.blk_counts;
+        p.nblk = plan.nblk;
+        p.lists = at<int32_t>(ws, plan.lists);
+        p.counts = at<int32_t>(ws, plan.counts);
     }
     e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S, desc->w_layout == CBW_KRSC,
                          header, mode, gather ? &cp : nullptr, s);
     if (e != hipSuccess) return hip_status(e);
-    if (gather && (e = launch_compact_scatter(cp, s)) != hipSuccess) return hip_status(e);
     if ((e = launch_bwd_data(desc->dtype, mode, p, s, prof_events(0))) != hipSuccess) return hip_status(e);
     if (dX != dX_out)
         e = launch_transpose(desc->dtype, dX, dX_out, desc->N, desc->H * desc->W, desc->C, s);
@@ -646,7 +647,10 @@ int cbw_read_live_lists(const cbw_conv_desc* desc, const void* workspace, size_t
     if (n < 0 || n > plan.npix) return CBW_ERR_INVALID_ARG;  // workspace not written by a gather call
     *count = n;
     *group_width = plan.bm;
-    if (pixels && n > 0) {
+    if (pixels && n == plan.npix) {
+        // a fully live group's list (0, 1, 2, ...) is never stored
+        for (int32_t i = 0; i < n; ++i) pixels[i] = i;
+    } else if (pixels && n > 0) {
         e = hipMemcpyAsync(pixels, at<int32_t>(ws, plan.lists) + (int64_t)group * plan.npix,
                            (size_t)n * sizeof(int32_t), hipMemcpyDeviceToHost, s);
         if (e == hipSuccess) e = hipStreamSynchronize(s);

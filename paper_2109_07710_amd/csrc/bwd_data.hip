@@ -15,9 +15,11 @@
 //             (never acc * bit, which would give -0.0 for a negative acc).
 //   gather  : the rows of channel group g are the compacted ascending list of
 //             pixels live in that group (output-bitmap-driven address
-//             generation, Sec. IV-B); the epilogue applies the per-element
-//             select.  Rows dead for the whole group were zero-filled by the
-//             compaction kernel and are never touched here.
+//             generation, Sec. IV-B), which each tile derives for itself from
+//             the footprint and the preparation launch's counts; the epilogue
+//             applies the per-element select.  Rows dead for the whole group
+//             were zero-filled by the preparation launch and are never
+//             touched here.
 //
 // Main loop: both operand tiles are copied by the load unit straight from
 // global memory into a double-buffered LDS ring (no staging registers, one
@@ -139,6 +141,88 @@ __device__ __forceinline__ void gather_tile(const int32_t* counts, int groups, i
     ptile = tmax;
 }
 
+// Sum over the 64 lanes of a wave (every lane gets the total).
+__device__ __forceinline__ int wave_sum(int v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+// Gather mode: lists the live pixels of ranks [row0, row_end) of group g
+// (live pixels in ascending pixel order, Sec. IV-B's output-bitmap-driven
+// address generation) into pix_s[0, row_end - row0), straight from the
+// footprint, so no list has to be built by an earlier launch.  An exclusive
+// scan of the preparation launch's 256-pixel block counts over the threads
+// locates the block holding rank row0; from there the workgroup tests NT
+// pixels at a time: wave ballots and popcounts rank each live pixel, and
+// those inside the range are stored.  scr: 64 ints of LDS.  Called by the
+// whole workgroup; every loop bound is uniform.
+template <int NT>
+__device__ void gather_list(const DataParams& p, int G, int g, int row0, int row_end, int* pix_s, int* scr)
+{
+    constexpr int NWV = NT / 64;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // (a) the block holding rank row0: each thread sums a contiguous run of
+    // block counts (loads of up to 8 in flight), then an exclusive scan
+    const int32_t* bc = p.blk_counts + (int64_t)g * p.nblk;
+    const int per = (p.nblk + NT - 1) / NT;
+    const int b0 = min(p.nblk, tid * per), b1 = min(p.nblk, b0 + per);
+    int cnt = 0;
+    for (int b = b0; b < b1; b += 8) {
+        int v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = b + u < b1 ? bc[b + u] : 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) cnt += v[u];
+    }
+    int incl = cnt;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int v = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += v;
+    }
+    if (lane == 63) scr[wave] = incl;
+    __syncthreads();
+    int run = incl - cnt;
+    for (int w = 0; w < wave; ++w) run += scr[w];
+    if (run <= row0 && row0 < run + cnt) {
+        // this thread's run holds rank row0 (exactly one thread's does)
+        for (int b = b0; b < b1; ++b) {
+            const int c = bc[b];
+            if (row0 < run + c) {
+                scr[16] = b * kCompactThreads;
+                scr[17] = run;
+                break;
+            }
+            run += c;
+        }
+    }
+    __syncthreads();
+    // (b) rank the pixels from that block on until rank row_end is passed
+    int px0 = scr[16], base = scr[17], buf = 0;
+    const uint64_t below = lane == 0 ? 0ull : ((~0ull) >> (64 - lane));
+    while (base < row_end && px0 < p.npix) {
+        const int px = px0 + tid;
+        const bool live = pixel_live_bits(p.mask, p.npix, p.C, G, px, g);
+        const uint64_t bal = __ballot(live);
+        if (lane == 0) scr[32 + buf * NWV + wave] = __popcll(bal);
+        __syncthreads();
+        int wb = 0, tot = 0;
+#pragma unroll
+        for (int w = 0; w < NWV; ++w) {
+            const int v = scr[32 + buf * NWV + w];
+            if (w < wave) wb += v;
+            tot += v;
+        }
+        const int rank = base + wb + __popcll(bal & below);
+        if (live && rank >= row0 && rank < row_end) pix_s[rank - row0] = px;
+        base += tot;
+        px0 += NT;
+        buf ^= 1;   // the next round's counts go to the other half (no barrier needed before writing them)
+    }
+}
+
 template <typename T, int MODE, bool UNIT, int TI>
 __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
 {
@@ -161,71 +245,90 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     int wm, wn;
     wave_coords<WN>(wave, wm, wn);
 
-    // Work items are (tile, reduction split).  In gather mode the number of
-    // live tiles T follows from the compaction counts; when T is small
+    // Work items are (tile, reduction split).  When the tiles are few
     // against the resident workgroups, each tile's reduction (taps x channel
     // chunks) is split S ways and the partial tiles are summed afterwards
-    // (splitk_data_reduce_kernel) -- every workgroup derives the same S.
+    // (splitk_data_reduce_kernel); every workgroup derives the same S.
+    //
+    // Gather mode speculates: it first takes the dense mode's tiles, which
+    // are exactly its own when every pixel of every group is live (the usual
+    // case for element-wise footprints), and issues their first copies at
+    // once.  The groups' live totals, summed from the preparation launch's
+    // block counts while those copies fly, confirm it; otherwise the copies
+    // are dropped and the tiles are rebuilt over the live lists.
     const int kchunks = (p.K + (CH * Elem<T>::E) - 1) / (CH * Elem<T>::E);
     const int nsteps = p.R * p.S * kchunks;
-    int ntiles, nsplit, brows;
-    if (MODE == MODE_GATHER) {
-        brows = gather_rows<BN>(p.counts, p.ctiles, p.nslots);
-        ntiles = 0;
-        for (int g = 0; g < p.ctiles; ++g) ntiles += (p.counts[g] + brows - 1) / brows;
-        nsplit = data_split(ntiles, nsteps, p.nslots, p.smax);
-    } else {
-        brows = p.brows;
-        ntiles = p.ptiles * p.ctiles;
-        nsplit = p.split;
-    }
-    // The grid may hold more workgroups than items (gather mode sizes it for
-    // the most tiles any row choice gives); the surplus exits, and the XCD
-    // remap runs over the items alone so that every XCD gets its share.
-    const int nitems = ntiles * nsplit;
-    if ((int)blockIdx.x >= nitems) return;  // uniform across the workgroup
-    const int item = xcd_remap(blockIdx.x, nitems);
-    const int tile = item / nsplit, z = item - tile * nsplit;
-    int ctile, ptile;
-    if (MODE == MODE_GATHER) {
-        gather_tile(p.counts, p.ctiles, brows, tile, ctile, ptile);
-    } else {
-        ptile = tile / p.ctiles;
-        ctile = tile - ptile * p.ctiles;
-    }
-    const int c0 = ctile * BM;
-    const int row0 = ptile * brows;
-    // The tile's brows / 16 pixel blocks are shared out among the WN pixel
-    // columns of waves as evenly as possible: this wave's column covers fnw
-    // blocks (FN or FN - 1) from row wrow0.
-    const int nblk16 = brows >> 4;
-    const int fn_base = nblk16 / WN, fn_rem = nblk16 - fn_base * WN;
-    const int fnw = __builtin_amdgcn_readfirstlane(fn_base + (wn < fn_rem ? 1 : 0));
-    const int wrow0 = 16 * (wn * fn_base + (wn < fn_rem ? wn : fn_rem));
-    const int nrows = MODE == MODE_GATHER ? p.counts[ctile] : p.npix;
-    const int st_begin = (int)((int64_t)z * nsteps / nsplit);
-    const int st_end = (int)((int64_t)(z + 1) * nsteps / nsplit);
-    const int nloc = st_end - st_begin;
+    constexpr int GG = MODE == MODE_GATHER ? kGatherMaxGroups : 1;
+    __shared__ int gsum_s[GG * NW];
+    __shared__ int gtot_s[GG];
+    __shared__ int gscr_s[MODE == MODE_GATHER ? 64 : 1];
 
     const u32x4_t rs_wt = make_rsrc_words(p.wt, p.wt_bytes);
     const u32x4_t rs_dy = make_rsrc_words(p.dy, p.dy_bytes);
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
     const bool kfull = (p.K % BK) == 0;
-
     // Staging: every wave copies whole groups of 8 LDS rows (1 KB) straight
     // from global memory into LDS.  Row group g = wave + NW*j; lane l serves
     // row 8g + l/8 at physical chunk l%8, i.e. logical chunk (l%8) ^ swz(row).
     const int lrow8 = lane >> 3, pch = lane & 7;
+
+    // The work item of this workgroup and everything derived from it.
+    int nsplit = 1, brows = 0, item = 0, z = 0, ctile = 0, ptile = 0, c0 = 0, row0 = 0;
+    int fnw = 0, wrow0 = 0, nrows = 0, st_begin = 0, nloc = 0;
+    bool active = false, listed = false;
     uint32_t a_off[IA];   // A: byte offset without the step part, kOOB when no such channel
     int a_lc[IA];
+    auto map_item = [&](bool dense_rule) {
+        int ntiles;
+        if (dense_rule) {
+            brows = p.brows;
+            ntiles = p.ptiles * p.ctiles;
+            nsplit = p.split;
+        } else {
+            brows = gather_rows<BN>(gtot_s, p.ctiles, p.nslots);
+            ntiles = 0;
+            for (int g = 0; g < p.ctiles; ++g) ntiles += (gtot_s[g] + brows - 1) / brows;
+            nsplit = data_split(ntiles, nsteps, p.nslots, p.smax);
+        }
+        // The grid may hold more workgroups than items (gather mode sizes it
+        // for the most tiles any row choice gives); the surplus has no item,
+        // and the XCD remap runs over the items alone so that every XCD gets
+        // its share.
+        const int nitems = ntiles * nsplit;
+        active = (int)blockIdx.x < nitems;   // uniform across the workgroup
+        if (!active) return;
+        item = xcd_remap(blockIdx.x, nitems);
+        const int tile = item / nsplit;
+        z = item - tile * nsplit;
+        if (dense_rule) {
+            ptile = tile / p.ctiles;
+            ctile = tile - ptile * p.ctiles;
+        } else {
+            gather_tile(gtot_s, p.ctiles, brows, tile, ctile, ptile);
+        }
+        c0 = ctile * BM;
+        row0 = ptile * brows;
+        // The tile's brows / 16 pixel blocks are shared out among the WN
+        // pixel columns of waves as evenly as possible: this wave's column
+        // covers fnw blocks (FN or FN - 1) from row wrow0.
+        const int nblk16 = brows >> 4;
+        const int fn_base = nblk16 / WN, fn_rem = nblk16 - fn_base * WN;
+        fnw = __builtin_amdgcn_readfirstlane(fn_base + (wn < fn_rem ? 1 : 0));
+        wrow0 = 16 * (wn * fn_base + (wn < fn_rem ? wn : fn_rem));
+        nrows = dense_rule ? p.npix : gtot_s[ctile];
+        listed = !dense_rule && nrows < p.npix;
+        st_begin = (int)((int64_t)z * nsteps / nsplit);
+        nloc = (int)((int64_t)(z + 1) * nsteps / nsplit) - st_begin;
 #pragma unroll
-    for (int j = 0; j < IA; ++j) {
-        const int row = 8 * (wave + NW * j) + lrow8;
-        const int lc = pch ^ swz8(row);
-        const int c = c0 + row;
-        a_lc[j] = lc;
-        a_off[j] = (row < BM && c < p.C) ? (uint32_t)(c * p.K + lc * E) * ESZ : kOOB;
-    }
+        for (int j = 0; j < IA; ++j) {
+            const int row = 8 * (wave + NW * j) + lrow8;
+            const int lc = pch ^ swz8(row);
+            const int c = c0 + row;
+            a_lc[j] = lc;
+            a_off[j] = (row < BM && c < p.C) ? (uint32_t)(c * p.K + lc * E) * ESZ : kOOB;
+        }
+    };
+
     // Queue the copies of step (tap, k0) into LDS buffer `buf`.  The A part
     // (filters) does not depend on the pixel list, so step 0's is issued
     // before the list is read.
@@ -241,42 +344,10 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
             }
         }
     };
-    load_a(0, st_begin / kchunks, (st_begin % kchunks) * BK);
 
-    for (int i = tid; i < BN; i += NT) {
-        const int r = row0 + i;
-        int pix = -1;
-        if (i < brows && r < nrows) pix = (MODE == MODE_GATHER) ? p.lists[(int64_t)ctile * p.npix + r] : r;
-        pix_s[i] = pix;
-    }
-    __syncthreads();
     int bn_[IB], bh_[IB], bw_[IB], bbase[IB], b_lc[IB];
-#pragma unroll
-    for (int j = 0; j < IB; ++j) {
-        const int row = 8 * (wave + NW * j) + lrow8;
-        const int lc = pch ^ swz8(row);
-        b_lc[j] = lc;
-        const int pix = row < BN ? pix_s[row] : -1;
-        bn_[j] = -1; bh_[j] = 0; bw_[j] = 0;
-        if (pix >= 0) {
-            const uint32_t nh = fdiv((uint32_t)pix, p.div_w);
-            bw_[j] = pix - (int)nh * p.W;
-            const uint32_t n = fdiv(nh, p.div_h);
-            bh_[j] = (int)nh - (int)n * p.H;
-            bn_[j] = (int)n;
-        }
-        // unit stride: element offset of dY at (n, h, w) before the tap shift
-        bbase[j] = ((bn_[j] * p.P + bh_[j]) * p.Q + bw_[j]) * p.K + lc * E;
-    }
-
-    floatx4 acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-
     uint32_t b_off[IB];   // B byte offset for the current tap, kOOB when the tap misses
-    int ld_tap = st_begin / kchunks, ld_kc = st_begin % kchunks;  // next step to load
+    int ld_tap = 0, ld_kc = 0;  // next step to load
 
     auto set_tap = [&](int tap) {
         const int r = tap / p.S, s = tap - r * p.S;
@@ -322,6 +393,12 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
         if (++ld_kc == kchunks) { ld_kc = 0; ++ld_tap; }
     };
 
+    floatx4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
     // NB: the wave's pixel blocks (fnw, a compile-time FN or FN - 1)
     auto compute = [&](int buf, auto nb_tag) {
         constexpr int NB = decltype(nb_tag)::value;
@@ -347,18 +424,13 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
         }
     };
 
-    // Prologue: step 0's B copies.
-    set_tap(ld_tap);
-    load_b(0, ld_kc * BK);
-    if (++ld_kc == kchunks) { ld_kc = 0; ++ld_tap; }
-
     // Footprint words of the tile (pixel row x 32-channel word, valid when
     // every pixel's group of BM channels starts on a word).  Only the
     // epilogue needs them: they are fetched together with step 0's copies
     // (their latency hides under the copies'), held in registers through the
     // main loop and staged in LDS after it.  (Fetching them next to step 1's
     // copies instead measured 1.5 us slower per launch.)
-    const bool mask_lds = SEL && (p.C % 32) == 0 && nsplit == 1;
+    bool mask_lds = false;
     constexpr int MW = SEL ? BN * (BM / 32) : 0;                  // footprint words per tile
     constexpr int MI = MW > 0 ? (MW + NT - 1) / NT : 1;          // per thread
     uint32_t mwords[MI];
@@ -375,9 +447,96 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
             mwords[u] = word;
         }
     };
-    if (mask_lds) fetch_mask();
-    wait_vmem();
-    __syncthreads();
+
+    // Step 0 of the work item: the filter copies, the tile's pixel rows
+    // (consecutive pixels, or in gather mode the group's live pixels of ranks
+    // row0 .. row0 + brows - 1), the dY copies and the footprint words.
+    auto start_item = [&]() {
+        ld_tap = st_begin / kchunks;
+        ld_kc = st_begin % kchunks;
+        load_a(0, ld_tap, ld_kc * BK);
+        for (int i = tid; i < BN; i += NT) {
+            const int r = row0 + i;
+            pix_s[i] = (!listed && i < brows && r < nrows) ? r : -1;
+        }
+        if (listed) gather_list<NT>(p, BM, ctile, row0, min(row0 + brows, nrows), pix_s, gscr_s);
+        __syncthreads();
+        if (listed) {
+            // the rows' pixels, for the split reduction and the list readers
+            const int n = min(brows, nrows - row0);
+            for (int i = tid; i < n; i += NT) p.lists[(int64_t)ctile * p.npix + row0 + i] = pix_s[i];
+        }
+#pragma unroll
+        for (int j = 0; j < IB; ++j) {
+            const int row = 8 * (wave + NW * j) + lrow8;
+            const int lc = pch ^ swz8(row);
+            b_lc[j] = lc;
+            const int pix = row < BN ? pix_s[row] : -1;
+            bn_[j] = -1; bh_[j] = 0; bw_[j] = 0;
+            if (pix >= 0) {
+                const uint32_t nh = fdiv((uint32_t)pix, p.div_w);
+                bw_[j] = pix - (int)nh * p.W;
+                const uint32_t n = fdiv(nh, p.div_h);
+                bh_[j] = (int)nh - (int)n * p.H;
+                bn_[j] = (int)n;
+            }
+            // unit stride: element offset of dY at (n, h, w) before the tap shift
+            bbase[j] = ((bn_[j] * p.P + bh_[j]) * p.Q + bw_[j]) * p.K + lc * E;
+        }
+        set_tap(ld_tap);
+        load_b(0, ld_kc * BK);
+        if (++ld_kc == kchunks) { ld_kc = 0; ++ld_tap; }
+        mask_lds = SEL && (p.C % 32) == 0 && nsplit == 1;
+        if (mask_lds) fetch_mask();
+    };
+
+    map_item(true);
+    if (active) start_item();
+    bool published = false;   // step 0's copies have landed and a barrier has published them
+    if (MODE == MODE_GATHER) {
+        // every group's live-pixel total; the block counts' loads complete
+        // with the copies above, and the barrier that publishes those copies
+        // also publishes the per-wave sums
+        for (int g = 0; g < p.ctiles; ++g) {
+            const int32_t* bc = p.blk_counts + (int64_t)g * p.nblk;
+            int v = 0;
+            for (int i0 = 0; i0 < p.nblk; i0 += 8 * NT) {
+                int c[8];   // eight loads in flight
+#pragma unroll
+                for (int u = 0; u < 8; ++u) c[u] = i0 + u * NT + tid < p.nblk ? bc[i0 + u * NT + tid] : 0;
+#pragma unroll
+                for (int u = 0; u < 8; ++u) v += c[u];
+            }
+            v = wave_sum(v);
+            if (lane == 0) gsum_s[g * NW + wave] = v;
+        }
+        wait_vmem();
+        __syncthreads();
+        bool all_live = true;
+        for (int g = 0; g < p.ctiles; ++g) {
+            int tot = 0;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) tot += gsum_s[g * NW + w];
+            all_live &= tot == p.npix;
+            if (tid == 0) gtot_s[g] = tot;
+            // workgroup 0 also stores them for the reduction kernel and the readers
+            if (blockIdx.x == 0 && tid == 0) p.counts[g] = tot;
+        }
+        if (!all_live) {
+            // speculation failed: the copies have landed; start over on the
+            // live lists
+            __syncthreads();   // gtot_s
+            map_item(false);
+            if (active) start_item();
+        } else {
+            published = true;
+        }
+    }
+    if (!active) return;   // uniform across the workgroup
+    if (!published) {
+        wait_vmem();
+        __syncthreads();
+    }
     auto main_loop = [&](auto nb_tag) {
         for (int step = 0; step < nloc; ++step) {
             const int buf = step & 1;
@@ -578,7 +737,8 @@ __device__ __forceinline__ void transform_filters(const T* __restrict__ w, T* __
 
 // One launch for the data gradient's preparation: blocks [0, ntb) transform
 // the filters (block 0 also stamps the workspace header), the remaining
-// blocks count live pixels per compaction block (gather mode).
+// blocks (gather mode) count the live pixels of one compaction block each
+// and clear the dX rows of its dead pixels.
 template <typename T>
 __global__ __launch_bounds__(256) void data_prep_kernel(const T* __restrict__ w, T* __restrict__ wt, int K, int C,
                                                         int RS, int krsc, int* header, int mode, int ntb,
@@ -676,7 +836,8 @@ __global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
         const int nrows = MODE == MODE_GATHER ? p.counts[ctile] : p.npix;
         const int c = ctile * BM + cl;
         if (r >= nrows || c >= p.C) continue;
-        const int pix = MODE == MODE_GATHER ? p.lists[(int64_t)ctile * p.npix + r] : r;
+        // (a fully live group's list is 0, 1, 2, ... and is not stored)
+        const int pix = MODE == MODE_GATHER && nrows < p.npix ? p.lists[(int64_t)ctile * p.npix + r] : r;
         // every split's partial is loaded before any is added (latency, not
         // bandwidth, bounds a serial chain of loads); the sum runs in split order
         const float* __restrict__ base = p.partial + ((int64_t)tile * nsplit * BN + pr) * BM + cl;

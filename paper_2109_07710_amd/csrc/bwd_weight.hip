@@ -64,14 +64,18 @@ constexpr int OCC_WIN = 1024;   // occupancy bytes cached per workgroup
 constexpr int TILE_LIVE_CAP = 16384;
 constexpr int SPLIT_SCRATCH_BYTES = 256 + TILE_LIVE_CAP;
 
-__device__ void split_range(const WeightParams& p, int kt, int combo, int z, int& begin, int& end,
+//
+// Returns true when the range needs no liveness tests: no skipping, or every
+// chunk of the tile live.  The main loop then runs exactly as without
+// skipping, with no per-step liveness probe.
+__device__ bool split_range(const WeightParams& p, int kt, int combo, int z, int& begin, int& end,
                             uint8_t* live_s, uint8_t* scratch)
 {
     const int nch = p.nchunks, T = blockDim.x, tid = threadIdx.x;
     if (p.occ == nullptr) {
         begin = min(nch, z * p.chunks_per_split);
         end = min(nch, begin + p.chunks_per_split);
-        return;
+        return true;
     }
     const int ncombo = p.tgroups * p.ctiles;
     auto live = [&](int c) -> int {
@@ -112,10 +116,7 @@ __device__ void split_range(const WeightParams& p, int kt, int combo, int z, int
     if (__syncthreads_and(all)) {
         begin = min(nch, z * p.chunks_per_split);
         end = min(nch, begin + p.chunks_per_split);
-        const int n = min(OCC_WIN, max(end - begin, 0));
-        for (int i = tid; i < n; i += T) live_s[i] = 1;
-        __syncthreads();
-        return;
+        return true;
     }
     if (staged) {
         for (int c = s0; c < s1; ++c) {
@@ -175,6 +176,7 @@ __device__ void split_range(const WeightParams& p, int kt, int combo, int z, int
         live_s[i] = staged ? tl[c] : (uint8_t)live(c);
     }
     __syncthreads();
+    return false;
 }
 // The first live chunk in [chunk, end) (end when there is none), counting the
 // dead chunks passed in skipped.  Each lane tests one of 64 consecutive
@@ -387,9 +389,9 @@ __global__ __launch_bounds__(NT) void bwd_weight_kernel(WeightParams p)
     const int combo = tap * p.ctiles + ct;
     int ch_begin, ch_end;
     static_assert(sizeof(As[1]) >= SPLIT_SCRATCH_BYTES, "ranking scratch fits the second operand buffer");
-    split_range(p, kt, combo, z, ch_begin, ch_end, live_s, reinterpret_cast<uint8_t*>(As[1]));
+    const bool all_live = split_range(p, kt, combo, z, ch_begin, ch_end, live_s, reinterpret_cast<uint8_t*>(As[1]));
     auto next_live = [&](int chunk) {
-        return next_live_chunk(p, live_s, ch_begin, ch_end, kt, combo, chunk, skipped);
+        return all_live ? chunk : next_live_chunk(p, live_s, ch_begin, ch_end, kt, combo, chunk, skipped);
     };
 
     int chunk = next_live(ch_begin);
@@ -620,10 +622,10 @@ __global__ __launch_bounds__(WTile<BKT>::NT) void bwd_weight_tr_kernel(WeightPar
     const int combo = tg * p.ctiles + ct;
     int ch_begin, ch_end;
     static_assert(sizeof(As[1]) >= SPLIT_SCRATCH_BYTES, "ranking scratch fits the second operand buffer");
-    split_range(p, kt, combo, z, ch_begin, ch_end, live_s, reinterpret_cast<uint8_t*>(As[1]));
+    const bool all_live = split_range(p, kt, combo, z, ch_begin, ch_end, live_s, reinterpret_cast<uint8_t*>(As[1]));
     int skipped = 0;
     auto next_live = [&](int chunk) {
-        return next_live_chunk(p, live_s, ch_begin, ch_end, kt, combo, chunk, skipped);
+        return all_live ? chunk : next_live_chunk(p, live_s, ch_begin, ch_end, kt, combo, chunk, skipped);
     };
 
     int chunk = next_live(ch_begin);

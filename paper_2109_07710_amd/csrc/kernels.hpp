@@ -18,8 +18,13 @@ struct DataParams {
     const void* wt;          // [R*S][C][K]
     void* dx;                // [N*H*W][C]
     const uint32_t* mask;    // packed footprint of X (select / gather)
-    const int32_t* lists;    // [groups][npix] live pixels (gather)
-    const int32_t* counts;   // [groups] live-pixel counts (gather)
+    // gather mode: the compaction counts written by the preparation launch,
+    // and the outputs the GEMM writes for the reduction kernel and readers
+    const int32_t* blk_counts;   // [groups][nblk] live pixels per 256-pixel block
+    int nblk;
+    int32_t* lists;          // [groups][npix] live pixels, ascending (written by the tiles of
+                             // groups with dead pixels; a fully live group's list is 0, 1, 2, ...)
+    int32_t* counts;         // [groups] live-pixel counts (written by workgroup 0)
     int N, H, W, C, K, R, S, P, Q;
     int stride_h, stride_w, pad_h, pad_w;
     int npix;                // N*H*W
@@ -38,9 +43,7 @@ struct DataParams {
 
 struct CompactParams {
     const uint32_t* mask;    // packed footprint, NHWC bit order
-    int32_t* blk_counts;     // [groups][nblk]
-    int32_t* counts;         // [groups]
-    int32_t* lists;          // [groups][npix]
+    int32_t* blk_counts;     // [groups][nblk] live pixels per 256-pixel block
     void* dx;                // zero-filled at (pixel, group) rows dead for the whole group
     int npix, C, G, groups, nblk, elem_bytes;
 };
@@ -106,7 +109,8 @@ int weight_tile_k();
 int weight_chunk(int dtype);
 int compact_block_pixels();
 
-// Filter transform (and, when cp is given, the compaction count) in one launch.
+// Filter transform (and, when cp is given, the compaction counts and the
+// dead-row zero fill) in one launch.
 hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, int RS, int krsc, int* header,
                             int mode, const CompactParams* cp, hipStream_t stream);
 // Optional timing events attached to the dispatch of a GEMM kernel (both
@@ -120,7 +124,6 @@ hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t
 // `zero` cleared (footprint words filled by atomic OR), in one launch.
 hipError_t launch_fwd_prep(int dtype, const void* w, void* wt, int K, int C, int R, int S, int krsc, int* header,
                            uint32_t* zero, int64_t zero_words, hipStream_t stream);
-hipError_t launch_compact_scatter(const CompactParams& p, hipStream_t stream);
 // Boundary layout conversion (NCHW callers): dst[b][c][r] = src[b][r][c] for
 // `batch` matrices of rows x cols elements, and footprint bits in NCHW
 // element order reordered to NHWC element order.

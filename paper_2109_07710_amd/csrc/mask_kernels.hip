@@ -1,5 +1,6 @@
-// Integer kernels around the GEMMs: footprint bitmaps, per-group compaction
-// of live pixels, dY block occupancy and the split-K reduction of dW.
+// Integer kernels around the GEMMs: footprint bitmaps, dY block occupancy
+// and the split-K reduction of dW.  (The compaction counts run in the
+// data-gradient preparation launch, the live lists inside the GEMM.)
 #include "common.hpp"
 #include "kernels.hpp"
 #include "footprint.hpp"
@@ -70,55 +71,6 @@ __global__ void mask_pack_kernel(const T* __restrict__ x, uint32_t* __restrict__
     if (lane % L == 0 && v < nvec) bits[v / L] = b;
 }
 
-
-// Writes the ascending list of live pixels of group g (rank = live pixels
-// before it in the block, by wave ballot and popcount, plus the counts of all
-// earlier blocks) and zero-fills the dX rows of pixels dead for the group.
-__global__ __launch_bounds__(CNT) void compact_scatter_kernel(CompactParams p)
-{
-    __shared__ int red[4];
-    __shared__ int wcnt[4], wdead[4];
-    __shared__ int dead_s[CNT];
-    const int blk = blockIdx.x, g = blockIdx.y;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-
-    int before = 0;
-    for (int b = tid; b < blk; b += CNT) before += p.blk_counts[(int64_t)g * p.nblk + b];
-    for (int off = 32; off > 0; off >>= 1) before += __shfl_xor(before, off);
-    if (lane == 0) red[wave] = before;
-
-    const int px = blk * CNT + tid;
-    const bool live = pixel_live(p, px, g);
-    const bool dead = px < p.npix && !live;
-    const uint64_t bal = __ballot(live), dbal = __ballot(dead);
-    if (lane == 0) {
-        wcnt[wave] = __popcll(bal);
-        wdead[wave] = __popcll(dbal);
-    }
-    __syncthreads();
-    const int offset = red[0] + red[1] + red[2] + red[3];
-    int wbase = 0, dbase = 0;
-    for (int w = 0; w < wave; ++w) {
-        wbase += wcnt[w];
-        dbase += wdead[w];
-    }
-    const uint64_t below = lane == 0 ? 0ull : ((~0ull) >> (64 - lane));
-    if (live) p.lists[(int64_t)g * p.npix + offset + wbase + __popcll(bal & below)] = px;
-    if (dead) dead_s[dbase + __popcll(dbal & below)] = px;
-    if (blk == p.nblk - 1 && tid == 0) p.counts[g] = offset + wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
-    __syncthreads();
-    // The dead pixels' rows of dX are cleared by the whole block together:
-    // consecutive threads write consecutive 16-byte pieces of one row, so a
-    // wave covers whole rows rather than one 16-byte piece of 64 rows.
-    const int ndead = wdead[0] + wdead[1] + wdead[2] + wdead[3];
-    const int lo = g * p.G, hi = min(p.C, lo + p.G);
-    const int nvec = (hi - lo) * p.elem_bytes / 16;
-    for (int q = tid; q < ndead * nvec; q += CNT) {
-        const int d = q / nvec, v = q - d * nvec;
-        uint4* row = reinterpret_cast<uint4*>(static_cast<char*>(p.dx) + ((int64_t)dead_s[d] * p.C + lo) * p.elem_bytes);
-        row[v] = make_uint4(0, 0, 0, 0);
-    }
-}
 
 // occ[chunk][kt] = 1 iff dY has a non-zero in pixels of the chunk and
 // channels of k-tile kt (from the packed footprint when given: one (pixel,
@@ -294,13 +246,6 @@ hipError_t launch_relu_mask_pack(int dtype, int64_t count, const void* x, uint32
     else
         mask_pack_kernel<float><<<(unsigned)blocks, 256, 0, stream>>>((const float*)x, bits, count, nvec,
                                                                       relu != 0);
-    return hipGetLastError();
-}
-
-hipError_t launch_compact_scatter(const CompactParams& p, hipStream_t stream)
-{
-    dim3 grid(p.nblk, p.groups);
-    compact_scatter_kernel<<<grid, CNT, 0, stream>>>(p);
     return hipGetLastError();
 }
 

@@ -33,6 +33,9 @@ struct DataTile {
     int bm, bn, wm, wn;
 };
 constexpr int kDataTileCount = 3;
+// Compaction groups (channel tiles) the gather mode handles; wider layers
+// run the masked data gradient without compaction (footprint select only).
+constexpr int kGatherMaxGroups = 16;
 constexpr DataTile kDataTiles[kDataTileCount] = {{256, 224, 8, 2}, {128, 448, 4, 4}, {64, 512, 2, 8}};
 
 // Pixel rows a data-gradient tile actually covers: its capacity BN, or 16 or
