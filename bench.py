@@ -105,6 +105,8 @@ def main():
         cb.cbw_relu_mask_pack(desc, x, xm)
         cb.cbw_nonzero_mask_pack(desc.dtype, dy.numel(), dy, dym)
 
+    ws_b = cb.workspace(desc, cb.CBW_OP_BWD_BOTH, dev)
+
     def sparse_dx():
         cb.conv_bwd_data_masked(desc, dy, w, xm, dx, ws_m, 0)
 
@@ -117,14 +119,24 @@ def main():
     def dense_dw():
         cb.conv_bwd_weight_sparse(desc, x, dy, None, dw, ws_w, cb.CBW_FLAG_NO_SKIP)
 
-    # One stream, data gradient then weight gradient.  (Forking the two
-    # independent gradients onto two streams was measured slower: both GEMMs
-    # want every CU.)
+    # The step is one conv_bwd_sparse call: both gradients, with the integer
+    # passes of both in one launch and both split reductions in another, so
+    # the skipping and the dense step take the same four launches.  The dense
+    # step is the same call with no footprint and CBW_FLAG_NO_SKIP.  (Forking
+    # the two gradients onto two streams was measured slower: both GEMMs want
+    # every CU.)
     def sparse_step():
+        cb.conv_bwd_sparse(desc, x, dy, w, xm, dym, dx, dw, ws_b, 0)
+
+    def dense_step():
+        cb.conv_bwd_sparse(desc, x, dy, w, None, None, dx, dw, ws_b, cb.CBW_FLAG_NO_SKIP)
+
+    # The same work through the separate calls (three entry points).
+    def separate_sparse_step():
         sparse_dx()
         sparse_dw()
 
-    def dense_step():
+    def separate_dense_step():
         dense_dx()
         dense_dw()
 
@@ -186,8 +198,7 @@ def main():
 
     sparse_step()
     torch.cuda.synchronize()
-    st_dx = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_DATA_MASKED, ws_m)
-    st_dw = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws_w)
+    st_dx = st_dw = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_BOTH, ws_b)
     log("parity of the timed step's outputs against the oracle (sampled)")
     parity = check_against_oracle(spec, t_cpu, dx, dw, x)
 
@@ -283,21 +294,6 @@ def main():
     dist = {"hot": distribution(False), "cold": distribution(True)}
     del flush
 
-    # A caller's per-layer dispatch: from one earlier call's statistics, the
-    # data gradient compacts only when at most 90% of its pixel rows were
-    # live (else the same kernel applies the footprint in its epilogue,
-    # CBW_FLAG_NO_SKIP, with no compaction pass), and the weight gradient
-    # skips only when at least 5% of its blocks were skippable (else no
-    # occupancy pass).  Outputs are the same either way.
-    dx_skip, dw_skip = adaptive_choice(st_dx, st_dw)
-
-    def adaptive_step():
-        cb.conv_bwd_data_masked(desc, dy, w, xm, dx, ws_m, 0 if dx_skip else cb.CBW_FLAG_NO_SKIP)
-        if dw_skip:
-            cb.conv_bwd_weight_sparse(desc, x, dy, dym, dw, ws_w, 0)
-        else:
-            cb.conv_bwd_weight_sparse(desc, x, dy, None, dw, ws_w, cb.CBW_FLAG_NO_SKIP)
-
     # The semantic equivalent without output sparsity: the dense step followed
     # by a separate multiply of dX with the 0/1 ReLU derivative.
     relu_d = (x > 0).to(x.dtype)
@@ -308,11 +304,14 @@ def main():
         dense_dw()
 
     for _ in range(10):
-        adaptive_step()
+        separate_sparse_step()
+        separate_dense_step()
         dense_mask_step()
-    extra = alternate({"adaptive": adaptive_step, "dense_mask": dense_mask_step, "dense": dense_step},
+    extra = alternate({"separate_sparse": separate_sparse_step, "separate_dense": separate_dense_step,
+                       "dense_mask": dense_mask_step, "dense": dense_step},
                       lambda fn: timed(fn, args.steps)[0], 3)
-    ms_adaptive = float(np.median(extra["adaptive"]))
+    ms_sep_sparse = float(np.median(extra["separate_sparse"]))
+    ms_sep_dense = float(np.median(extra["separate_dense"]))
     ms_dense_mask = float(np.median(extra["dense_mask"]))
     ms_dense_here = float(np.median(extra["dense"]))
     del relu_d
@@ -436,13 +435,11 @@ def main():
                        "step_with_events": round(ms_sparse_k, 4)},
         "step_distribution": dist,
         "parity": parity,
-        "adaptive_dispatch": {"ms_per_step": round(ms_adaptive, 4),
-                              "speedup_vs_dense": round(ms_dense_here / ms_adaptive, 4),
-                              "dense_ms_same_rounds": round(ms_dense_here, 4),
-                              "dx_call": "compacting" if dx_skip else "non-skipping (footprint in the epilogue)",
-                              "dw_call": "skipping" if dw_skip else "non-skipping",
-                              "rule": "compact dX if <= 90% of rows were live, skip dW blocks if >= 5% were "
-                                      "skippable, from an earlier call's statistics"},
+        "separate_calls": {"sparse_ms": round(ms_sep_sparse, 4), "dense_ms": round(ms_sep_dense, 4),
+                           "speedup_vs_dense": round(ms_sep_dense / ms_sep_sparse, 4),
+                           "combined_dense_ms_same_rounds": round(ms_dense_here, 4),
+                           "note": "the same step through conv_bwd_data_masked + conv_bwd_weight_sparse "
+                                   "(dense: conv_bwd_data + conv_bwd_weight_sparse NO_SKIP), 6-7 and 4 launches"},
         "dense_plus_mask_multiply_ms": round(ms_dense_mask, 4),
         "speedup_vs_dense_plus_mask_multiply": round(ms_dense_mask / ms_sparse, 4),
         "nchw_boundary": {"sparse_step_ms": round(ms_nchw, 4), "added_ms": round(ms_nchw - ms_sparse, 4),
@@ -558,10 +555,12 @@ def measure_peaks(torch, stream):
 
 def vgg16_stack(cb, torch, steps, rounds):
     """The VGG-16 conv stack (13 layers, N = 32, 224 x 224 input) as one
-    step: every layer's sparse backward (masked dX where the footprint
-    applies, dense dX after a pool, no dX for conv1_1; skipping dW), against
-    the same layers' dense step and the per-layer dispatch.  Inputs drawn on
-    the device (workloads.draw_on_device, same recipe as the tests)."""
+    step: every layer's sparse backward through conv_bwd_sparse (masked dX
+    where the footprint applies, dense dX after a pool, no dX for conv1_1;
+    skipping dW), against the same layers' dense step (the same call with no
+    footprint and CBW_FLAG_NO_SKIP) and the sparse step through the separate
+    calls.  Inputs drawn on the device (workloads.draw_on_device, same recipe
+    as the tests)."""
     import numpy as np
     import workloads as wl
     dev = torch.device("cuda:0")
@@ -577,7 +576,8 @@ def vgg16_stack(cb, torch, steps, rounds):
              "dw": torch.empty((spec.K, spec.R, spec.S, spec.C), dtype=torch.float32, device=dev),
              "ws_m": cb.workspace(desc, cb.CBW_OP_BWD_DATA_MASKED, dev) if spec.need_dx and spec.masked else None,
              "ws_d": cb.workspace(desc, cb.CBW_OP_BWD_DATA, dev) if spec.need_dx else None,
-             "ws_w": cb.workspace(desc, cb.CBW_OP_BWD_WEIGHT, dev)}
+             "ws_w": cb.workspace(desc, cb.CBW_OP_BWD_WEIGHT, dev),
+             "ws_b": cb.workspace(desc, cb.CBW_OP_BWD_BOTH, dev)}
         cb.cbw_relu_mask_pack(desc, x, L["xm"])
         cb.cbw_nonzero_mask_pack(desc.dtype, dy.numel(), dy, L["dym"])
         true_c = spec.extra.get("true_c", spec.C)
@@ -589,6 +589,15 @@ def vgg16_stack(cb, torch, steps, rounds):
         layers.append(L)
 
     def sparse(L):
+        s = L["spec"]
+        cb.conv_bwd_sparse(L["desc"], L["x"], L["dy"], L["w"], L["xm"] if s.need_dx and s.masked else None,
+                           L["dym"], L["dx"], L["dw"], L["ws_b"], 0)
+
+    def dense(L):
+        cb.conv_bwd_sparse(L["desc"], L["x"], L["dy"], L["w"], None, None, L["dx"], L["dw"], L["ws_b"],
+                           cb.CBW_FLAG_NO_SKIP)
+
+    def separate(L):
         d, s = L["desc"], L["spec"]
         if s.need_dx:
             if s.masked:
@@ -596,35 +605,6 @@ def vgg16_stack(cb, torch, steps, rounds):
             else:
                 cb.conv_bwd_data(d, L["dy"], L["w"], L["dx"], L["ws_d"])
         cb.conv_bwd_weight_sparse(d, L["x"], L["dy"], L["dym"], L["dw"], L["ws_w"], 0)
-
-    def dense(L):
-        d, s = L["desc"], L["spec"]
-        if s.need_dx:
-            cb.conv_bwd_data(d, L["dy"], L["w"], L["dx"], L["ws_d"])
-        cb.conv_bwd_weight_sparse(d, L["x"], L["dy"], None, L["dw"], L["ws_w"], cb.CBW_FLAG_NO_SKIP)
-
-    for L in layers:
-        sparse(L)
-    torch.cuda.synchronize()
-    for L in layers:
-        s = L["spec"]
-        st_dx = (cb.cbw_read_stats(L["desc"], cb.CBW_OP_BWD_DATA_MASKED, L["ws_m"])
-                 if s.need_dx and s.masked else None)
-        L["choice"] = adaptive_choice(st_dx, cb.cbw_read_stats(L["desc"], cb.CBW_OP_BWD_WEIGHT, L["ws_w"]))
-
-    def adaptive(L):
-        d, s = L["desc"], L["spec"]
-        dx_skip, dw_skip = L["choice"]
-        if s.need_dx:
-            if s.masked:
-                cb.conv_bwd_data_masked(d, L["dy"], L["w"], L["xm"], L["dx"], L["ws_m"],
-                                        0 if dx_skip else cb.CBW_FLAG_NO_SKIP)
-            else:
-                cb.conv_bwd_data(d, L["dy"], L["w"], L["dx"], L["ws_d"])
-        if dw_skip:
-            cb.conv_bwd_weight_sparse(d, L["x"], L["dy"], L["dym"], L["dw"], L["ws_w"], 0)
-        else:
-            cb.conv_bwd_weight_sparse(d, L["x"], L["dy"], None, L["dw"], L["ws_w"], cb.CBW_FLAG_NO_SKIP)
 
     def tm(fn):
         torch.cuda.synchronize()
@@ -636,7 +616,7 @@ def vgg16_stack(cb, torch, steps, rounds):
         torch.cuda.synchronize()
         return a.elapsed_time(b) / steps
 
-    kinds = {"sparse": sparse, "dense": dense, "adaptive": adaptive}
+    kinds = {"sparse": sparse, "dense": dense, "separate": separate}
     for _ in range(3):
         for fn in kinds.values():
             for L in layers:
@@ -653,12 +633,11 @@ def vgg16_stack(cb, torch, steps, rounds):
     useful = sum(L["useful"] for L in layers)
     dense_flops = sum(L["dense_flops"] for L in layers)
     out = {"sparse_ms": round(res["sparse"], 4), "dense_ms": round(res["dense"], 4),
-           "adaptive_ms": round(res["adaptive"], 4),
+           "separate_calls_ms": round(res["separate"], 4),
            "speedup_vs_dense": round(res["dense"] / res["sparse"], 4),
-           "adaptive_speedup_vs_dense": round(res["dense"] / res["adaptive"], 4),
+           "separate_calls_speedup_vs_dense": round(res["dense"] / res["separate"], 4),
            "dense_equiv_tflops": round(dense_flops / (res["sparse"] * 1e-3) / 1e12, 2),
            "useful_tflops": round(useful / (res["sparse"] * 1e-3) / 1e12, 2),
-           "useful_tflops_adaptive": round(useful / (res["adaptive"] * 1e-3) / 1e12, 2),
            "dense_gflop": round(dense_flops / 1e9, 1), "useful_gflop": round(useful / 1e9, 1),
            "steps_per_round": steps, "rounds": rounds, "layers": per_layer,
            "inputs": "drawn on the device (workloads.draw_on_device), N=32, 224x224"}

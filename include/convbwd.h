@@ -88,12 +88,15 @@ typedef struct {
 
 /* Operation selector for cbw_workspace_size / cbw_read_stats. */
 enum { CBW_OP_BWD_DATA = 0, CBW_OP_BWD_DATA_MASKED = 1, CBW_OP_BWD_WEIGHT = 2, CBW_OP_FWD = 3,
-       CBW_OP_BWD_DATA_ELEMENTWISE = 4 };
+       CBW_OP_BWD_DATA_ELEMENTWISE = 4, CBW_OP_BWD_BOTH = 5 };
 
 /* Flags. CBW_FLAG_NO_SKIP runs the same kernels with every skip disabled:
  * the masked data gradient computes all rows and applies the mask in its
  * epilogue; the weight gradient processes every dY block. */
 #define CBW_FLAG_NO_SKIP 1u
+/* conv_bwd_sparse only: with x_mask given, the weight gradient also skips
+ * blocks whose X operand is entirely zero (as conv_bwd_weight_sparse_x). */
+#define CBW_FLAG_SKIP_X_BLOCKS 2u
 
 /* Execution statistics written by the kernels into the workspace. */
 typedef struct {
@@ -222,6 +225,35 @@ int conv_bwd_weight_sparse(const cbw_conv_desc* desc, const void* X, const void*
 int conv_bwd_weight_sparse_x(const cbw_conv_desc* desc, const void* X, const void* dY,
                              const uint32_t* x_mask, const uint32_t* dy_mask, float* dW,
                              void* workspace, size_t workspace_bytes, uint32_t flags, void* stream);
+
+/* Both gradients of one layer in one call: the backward-pass phase (data
+ * gradient) and the weight-gradient phase of Sec. IV-B, with the results of
+ *   - dX: conv_bwd_data_masked(desc, dY, W, x_mask, dX, .., flags & NO_SKIP)
+ *     when x_mask is set (output sparsity, Sec. III-B), conv_bwd_data when
+ *     x_mask is NULL (dense);
+ *   - dW: conv_bwd_weight_sparse(desc, X, dY, dy_mask, dW, .., flags &
+ *     NO_SKIP) (input sparsity), or with CBW_FLAG_SKIP_X_BLOCKS and x_mask
+ *     set conv_bwd_weight_sparse_x(desc, X, dY, x_mask, dy_mask, ...).
+ * Values are those of the separate calls (bitwise, unless a reduction is
+ * split differently).  The integer work of both gradients (filter
+ * transform, compaction counts, dY block occupancy) shares one launch and
+ * their split reductions share one, so with NHWC tensors the call always
+ * takes four launches, skipping or not; the skipping and the
+ * CBW_FLAG_NO_SKIP calls therefore differ only in the kernels' own work.
+ * NCHW tensors are served by the two separate calls.  Arguments as in the
+ * separate calls (X, dY, W, dX, dW and the footprints 16-byte aligned);
+ * dX = NULL computes the weight gradient alone (a first layer, whose input
+ * needs no gradient; W may then be NULL too); flags: CBW_FLAG_NO_SKIP,
+ * CBW_FLAG_SKIP_X_BLOCKS.
+ * Workspace: cbw_workspace_size(desc, CBW_OP_BWD_BOTH) bytes; its first
+ * cbw_workspace_size(desc, CBW_OP_BWD_DATA_MASKED) bytes are the data
+ * gradient's workspace, and the weight gradient's starts at that size
+ * rounded up to a multiple of 256 (for cbw_read_live_lists,
+ * cbw_read_occupancy and cbw_read_weight_work); cbw_read_stats with
+ * CBW_OP_BWD_BOTH reads both. */
+int conv_bwd_sparse(const cbw_conv_desc* desc, const void* X, const void* dY, const void* W, const uint32_t* x_mask,
+                    const uint32_t* dy_mask, void* dX, float* dW, void* workspace, size_t workspace_bytes,
+                    uint32_t flags, void* stream);
 
 /* Data gradient with per-element input and output sparsity on the vector
  * ALUs (Sec. III-B, input and output sparsity; Sec. IV-B, lanes that walk

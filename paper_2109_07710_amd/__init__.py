@@ -23,11 +23,13 @@ CBW_NCHW, CBW_NHWC = 0, 1
 CBW_KCRS, CBW_KRSC = 0, 1
 CBW_F32, CBW_BF16 = 0, 1
 CBW_OP_BWD_DATA, CBW_OP_BWD_DATA_MASKED, CBW_OP_BWD_WEIGHT, CBW_OP_FWD, CBW_OP_BWD_DATA_ELEMENTWISE = 0, 1, 2, 3, 4
+CBW_OP_BWD_BOTH = 5
 CBW_FLAG_NO_SKIP = 1
+CBW_FLAG_SKIP_X_BLOCKS = 2
 
 EXPORTS = ("cbw_status_string", "cbw_validate_desc", "cbw_mask_words", "cbw_dy_mask_words",
            "cbw_workspace_size", "cbw_data_tiling", "cbw_relu_mask_pack", "cbw_nonzero_mask_pack", "conv_bwd_data",
-           "conv_bwd_data_masked", "conv_bwd_data_masked_noalloc", "conv_fwd_relu_mask", "conv_bwd_weight_sparse", "conv_bwd_weight_sparse_x",
+           "conv_bwd_data_masked", "conv_bwd_data_masked_noalloc", "conv_fwd_relu_mask", "conv_bwd_weight_sparse", "conv_bwd_weight_sparse_x", "conv_bwd_sparse",
            "conv_bwd_data_elementwise", "cbw_read_pixel_counts", "cbw_read_weight_work", "cbw_read_stats",
            "cbw_read_live_lists",
            "cbw_read_occupancy", "cbw_set_profile_events")
@@ -95,6 +97,7 @@ def lib():
     L.conv_fwd_relu_mask.argtypes = [dp, vp, vp, vp, vp, vp, sz, vp]
     L.conv_bwd_weight_sparse.argtypes = [dp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
     L.conv_bwd_weight_sparse_x.argtypes = [dp, vp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
+    L.conv_bwd_sparse.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, sz, ctypes.c_uint32, vp]
     L.conv_bwd_data_elementwise.argtypes = [dp, vp, vp, vp, vp, vp, sz, vp]
     L.cbw_read_pixel_counts.argtypes = [dp, vp, sz, vp, ctypes.POINTER(ctypes.c_int64), vp]
     L.cbw_read_weight_work.argtypes = [dp, vp, sz, vp, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), vp]
@@ -220,6 +223,18 @@ def conv_bwd_weight_sparse_x(desc, X, dY, x_mask, dy_mask, dW, ws, flags=0, stre
     _check(lib().conv_bwd_weight_sparse_x(ctypes.byref(desc), _ptr(X), _ptr(dY), _ptr(x_mask), _ptr(dy_mask),
                                           _ptr(dW), _ptr(ws), _nbytes(ws), flags, _stream(stream)),
            "conv_bwd_weight_sparse_x")
+
+
+def conv_bwd_sparse(desc, X, dY, W, x_mask, dy_mask, dX, dW, ws, flags=0, stream=None):
+    """Both gradients in one call (x_mask None: dense data gradient)."""
+    _check(lib().conv_bwd_sparse(ctypes.byref(desc), _ptr(X), _ptr(dY), _ptr(W), _ptr(x_mask), _ptr(dy_mask),
+                                 _ptr(dX), _ptr(dW), _ptr(ws), _nbytes(ws), flags, _stream(stream)),
+           "conv_bwd_sparse")
+
+
+def both_weight_offset(desc):
+    """Byte offset of the weight-gradient part in a conv_bwd_sparse workspace."""
+    return (cbw_workspace_size(desc, CBW_OP_BWD_DATA_MASKED) + 255) // 256 * 256
 
 
 def conv_bwd_data_elementwise(desc, dY, W, x_mask, dX, ws, stream=None):

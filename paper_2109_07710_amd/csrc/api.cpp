@@ -9,6 +9,7 @@
 #include "../../include/convbwd.h"
 #include "kernels.hpp"
 #include "plan.hpp"
+#include "reduce.hpp"
 
 using namespace cbw;
 
@@ -78,42 +79,12 @@ DataParams data_params(const cbw_conv_desc* d, const void* dY, const void* wt, v
     return p;
 }
 
-int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const uint32_t* x_mask, void* dX,
-                 void* ws, size_t ws_bytes, uint32_t flags, void* stream, bool masked, bool no_split = false)
+// Kernel parameters of the data gradient on NHWC tensors (dY, dX, x_mask
+// already in NHWC order), from a validated plan.
+void data_gemm_params(const cbw_conv_desc* desc, const DataPlan& plan, const void* dY, const void* wt,
+                      const uint32_t* x_mask, void* dX, void* ws, bool gather, bool no_split, DataParams* out,
+                      CompactParams* cpo)
 {
-    DataPlan plan;
-    int st = plan_data(desc, masked, &plan, no_split);
-    if (st != CBW_OK) return st;
-    if (!dY || !W || !dX || (masked && !x_mask)) return CBW_ERR_INVALID_ARG;
-    if (!aligned16(dY) || !aligned16(W) || !aligned16(dX) || (masked && !aligned16(x_mask)))
-        return CBW_ERR_UNSUPPORTED;
-    if ((st = check_ws(ws, ws_bytes, plan.total)) != CBW_OK) return st;
-    if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-
-    // compaction needs at most kGatherMaxGroups channel groups; wider layers
-    // keep the footprint select without it
-    const bool gather = masked && !(flags & CBW_FLAG_NO_SKIP) && plan.groups <= kGatherMaxGroups;
-    const int mode = !masked ? MODE_DENSE : (gather ? MODE_GATHER : MODE_SELECT);
-    hipError_t e;
-    void* dX_out = dX;
-    if (desc->act_layout == CBW_NCHW) {
-        // the kernels read an NHWC copy of dY (and an NHWC-order footprint)
-        // and write an NHWC dX, transposed into the caller's dX at the end
-        void* tdy = at<void>(ws, plan.t_dy);
-        if ((e = launch_transpose(desc->dtype, dY, tdy, desc->N, desc->K, desc->P * desc->Q, s)) != hipSuccess)
-            return hip_status(e);
-        dY = tdy;
-        dX = at<void>(ws, plan.t_dx);
-        if (masked) {
-            uint32_t* t = at<uint32_t>(ws, plan.t_mask);
-            if ((e = launch_bits_nchw_to_nhwc(x_mask, t, desc->N, desc->C, desc->H * desc->W, s)) != hipSuccess)
-                return hip_status(e);
-            x_mask = t;
-        }
-    }
-    int* header = at<int>(ws, plan.header);
-    void* wt = at<void>(ws, plan.wt);
     DataParams p = data_params(desc, dY, wt, dX, plan.npix, plan.groups);
     p.tile = plan.tile;
     p.mask = x_mask;
@@ -140,6 +111,68 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
         p.lists = at<int32_t>(ws, plan.lists);
         p.counts = at<int32_t>(ws, plan.counts);
     }
+    *out = p;
+    *cpo = cp;
+}
+
+// compaction needs at most kGatherMaxGroups channel groups; wider layers
+// keep the footprint select without it
+bool data_gathers(const DataPlan& plan, bool masked, uint32_t flags)
+{
+    return masked && !(flags & CBW_FLAG_NO_SKIP) && plan.groups <= kGatherMaxGroups;
+}
+
+// Offset of the weight-gradient part in the workspace of the call that
+// computes both gradients: after the masked data gradient's workspace.
+int both_offset(const cbw_conv_desc* desc, size_t* off, size_t* total)
+{
+    DataPlan dp;
+    WeightPlan wp;
+    int st = plan_data(desc, true, &dp);
+    if (st != CBW_OK) return st;
+    if ((st = plan_weight(desc, &wp)) != CBW_OK) return st;
+    *off = (dp.total + 255) & ~(size_t)255;
+    *total = *off + wp.total;
+    return CBW_OK;
+}
+
+int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const uint32_t* x_mask, void* dX,
+                 void* ws, size_t ws_bytes, uint32_t flags, void* stream, bool masked, bool no_split = false)
+{
+    DataPlan plan;
+    int st = plan_data(desc, masked, &plan, no_split);
+    if (st != CBW_OK) return st;
+    if (!dY || !W || !dX || (masked && !x_mask)) return CBW_ERR_INVALID_ARG;
+    if (!aligned16(dY) || !aligned16(W) || !aligned16(dX) || (masked && !aligned16(x_mask)))
+        return CBW_ERR_UNSUPPORTED;
+    if ((st = check_ws(ws, ws_bytes, plan.total)) != CBW_OK) return st;
+    if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    const bool gather = data_gathers(plan, masked, flags);
+    const int mode = !masked ? MODE_DENSE : (gather ? MODE_GATHER : MODE_SELECT);
+    hipError_t e;
+    void* dX_out = dX;
+    if (desc->act_layout == CBW_NCHW) {
+        // the kernels read an NHWC copy of dY (and an NHWC-order footprint)
+        // and write an NHWC dX, transposed into the caller's dX at the end
+        void* tdy = at<void>(ws, plan.t_dy);
+        if ((e = launch_transpose(desc->dtype, dY, tdy, desc->N, desc->K, desc->P * desc->Q, s)) != hipSuccess)
+            return hip_status(e);
+        dY = tdy;
+        dX = at<void>(ws, plan.t_dx);
+        if (masked) {
+            uint32_t* t = at<uint32_t>(ws, plan.t_mask);
+            if ((e = launch_bits_nchw_to_nhwc(x_mask, t, desc->N, desc->C, desc->H * desc->W, s)) != hipSuccess)
+                return hip_status(e);
+            x_mask = t;
+        }
+    }
+    int* header = at<int>(ws, plan.header);
+    void* wt = at<void>(ws, plan.wt);
+    DataParams p;
+    CompactParams cp;
+    data_gemm_params(desc, plan, dY, wt, x_mask, dX, ws, gather, no_split, &p, &cp);
     e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S, desc->w_layout == CBW_KRSC,
                          header, mode, gather ? &cp : nullptr, s);
     if (e != hipSuccess) return hip_status(e);
@@ -300,6 +333,11 @@ int cbw_workspace_size(const cbw_conv_desc* desc, int op, size_t* bytes)
         *bytes = elementwise_ws(desc);
         return CBW_OK;
     }
+    if (op == CBW_OP_BWD_BOTH) {
+        size_t off;
+        if ((st = both_offset(desc, &off, bytes)) != CBW_OK) return st;
+        return CBW_OK;
+    }
     if (op == CBW_OP_FWD) {
         cbw_conv_desc vd;
         DataPlan p;
@@ -362,6 +400,81 @@ int conv_fwd_relu_mask(const cbw_conv_desc* desc, const void* X, const void* W, 
     return run_fwd(desc, X, W, Y, y_mask, workspace, workspace_bytes, stream);
 }
 
+// Occupancy pass of the weight gradient on NHWC tensors (dY, and the
+// footprints, in NHWC order): dY block occupancy from dy_mask or dY, and
+// with x_skip the X-window liveness from the packed X footprint xbits.
+static OccParams weight_occ_params(const cbw_conv_desc* desc, const WeightPlan& plan, const void* dY,
+                                   const uint32_t* dy_mask, bool x_skip, const uint32_t* xbits, void* workspace)
+{
+    OccParams op{};
+    op.dy = dY;
+    op.bits = dy_mask;
+    op.occ = at<uint8_t>(workspace, plan.occ);
+    op.npq = (int)plan.npq;
+    op.K = desc->K;
+    op.chunk = weight_chunk_px(desc->dtype);
+    op.BNk = plan.bk;
+    op.ktiles = plan.ktiles;
+    op.nchunks = plan.nchunks;
+    // chunks per workgroup: about four (pixel, k tile) pairs per thread
+    // (one with X-window liveness, whose test loops over taps), within the
+    // per-chunk flag arrays (1024 entries each)
+    const int ncombo = x_skip ? plan.tgroups * plan.ctiles : 1;
+    const int per_chunk = weight_chunk_px(desc->dtype) * plan.ktiles;
+    op.cpw = std::max(1, std::min((x_skip ? 256 : 1024) / per_chunk, 1024 / std::max(plan.ktiles, ncombo)));
+    op.dtype = desc->dtype;
+    if (x_skip) {
+        op.xbits = xbits;
+        op.xlive = at<uint8_t>(workspace, plan.xlive);
+        op.N = desc->N; op.H = desc->H; op.W = desc->W; op.C = desc->C; op.P = desc->P; op.Q = desc->Q;
+        op.S = desc->S; op.RS = desc->R * desc->S;
+        op.stride_h = desc->stride_h; op.stride_w = desc->stride_w;
+        op.pad_h = desc->pad_h; op.pad_w = desc->pad_w;
+        op.tpg = plan.tpg;
+        op.tgroups = plan.tgroups;
+        op.ctiles = plan.ctiles;
+        op.ctw = plan.tpg > 1 ? desc->C : weight_tile_channels();
+        op.div_q = make_fastdiv((uint32_t)desc->Q);
+        op.div_p = make_fastdiv((uint32_t)desc->P);
+    }
+    return op;
+}
+
+// Kernel parameters of the weight-gradient GEMM on NHWC X and dY.
+static WeightParams weight_gemm_params(const cbw_conv_desc* desc, const WeightPlan& plan, const void* X,
+                                       const void* dY, float* dW, void* workspace, bool skip, bool x_skip,
+                                       uint32_t flags)
+{
+    WeightParams p{};
+    p.x = X;
+    p.dy = dY;
+    p.out = plan.direct ? dW : at<float>(workspace, plan.partials);
+    p.occ = skip ? at<uint8_t>(workspace, plan.occ) : nullptr;
+    p.xlive = skip && x_skip ? at<uint8_t>(workspace, plan.xlive) : nullptr;
+    p.work_slots = at<int32_t>(workspace, plan.work_slots);
+    p.skip_slots = at<int32_t>(workspace, plan.skip_slots);
+    p.header = at<int>(workspace, plan.header);
+    p.N = desc->N; p.H = desc->H; p.W = desc->W; p.C = desc->C; p.K = desc->K; p.R = desc->R; p.S = desc->S;
+    p.P = desc->P; p.Q = desc->Q;
+    p.stride_h = desc->stride_h; p.stride_w = desc->stride_w; p.pad_h = desc->pad_h; p.pad_w = desc->pad_w;
+    p.npq = (int)plan.npq;
+    p.nchunks = plan.nchunks;
+    p.chunks_per_split = plan.chunks_per_split;
+    p.ctiles = plan.ctiles;
+    p.ktiles = plan.ktiles;
+    p.nsplit = plan.nsplit;
+    p.bk = plan.bk;
+    p.tpg = plan.tpg;
+    p.tgroups = plan.tgroups;
+    p.cg = plan.cg;
+    p.mode_flags = (int)flags;
+    p.div_q = make_fastdiv((uint32_t)desc->Q);
+    p.div_p = make_fastdiv((uint32_t)desc->P);
+    p.x_bytes = (uint32_t)((int64_t)desc->N * desc->H * desc->W * desc->C * elem_bytes(desc->dtype));
+    p.dy_bytes = (uint32_t)(plan.npq * desc->K * elem_bytes(desc->dtype));
+    return p;
+}
+
 // Weight gradient; x_skip also skips blocks whose X operand is all zero.
 static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, const uint32_t* x_mask,
                const uint32_t* dy_mask, bool x_skip, float* dW, void* workspace, size_t workspace_bytes,
@@ -401,77 +514,21 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
             x_mask = t;
         }
     }
-    uint8_t* occ = at<uint8_t>(workspace, plan.occ);
     if (skip) {
-        OccParams op{};
-        op.dy = dY;
-        op.bits = dy_mask;
-        op.occ = occ;
-        op.npq = (int)plan.npq;
-        op.K = desc->K;
-        op.chunk = weight_chunk_px(desc->dtype);
-        op.BNk = plan.bk;
-        op.ktiles = plan.ktiles;
-        op.nchunks = plan.nchunks;
-        // chunks per workgroup: about one (pixel, k tile) pair per thread,
-        // within the per-chunk flag arrays (1024 entries each)
-        const int ncombo = x_skip ? plan.tgroups * plan.ctiles : 1;
-        const int per_chunk = weight_chunk_px(desc->dtype) * plan.ktiles;
-        op.cpw = std::max(1, std::min(256 / per_chunk, 1024 / std::max(plan.ktiles, ncombo)));
-        op.dtype = desc->dtype;
-        if (x_skip) {
+        const uint32_t* xbits = x_mask;
+        if (x_skip && !xbits) {
             // the X-window liveness is read from a packed footprint of X: the
             // caller's, or one packed here from X's non-zeros
-            const uint32_t* xbits = x_mask;
-            if (!xbits) {
-                uint32_t* packed = at<uint32_t>(workspace, plan.xbits);
-                const int64_t count = (int64_t)desc->N * desc->H * desc->W * desc->C;
-                if ((e = launch_relu_mask_pack(desc->dtype, count, X, packed, 0, s)) != hipSuccess)
-                    return hip_status(e);
-                xbits = packed;
-            }
-            op.xbits = xbits;
-            op.xlive = at<uint8_t>(workspace, plan.xlive);
-            op.N = desc->N; op.H = desc->H; op.W = desc->W; op.C = desc->C; op.P = desc->P; op.Q = desc->Q;
-            op.S = desc->S; op.RS = desc->R * desc->S;
-            op.stride_h = desc->stride_h; op.stride_w = desc->stride_w;
-            op.pad_h = desc->pad_h; op.pad_w = desc->pad_w;
-            op.tpg = plan.tpg;
-            op.tgroups = plan.tgroups;
-            op.ctiles = plan.ctiles;
-            op.ctw = plan.tpg > 1 ? desc->C : weight_tile_channels();
-            op.div_q = make_fastdiv((uint32_t)desc->Q);
-            op.div_p = make_fastdiv((uint32_t)desc->P);
+            uint32_t* packed = at<uint32_t>(workspace, plan.xbits);
+            const int64_t count = (int64_t)desc->N * desc->H * desc->W * desc->C;
+            if ((e = launch_relu_mask_pack(desc->dtype, count, X, packed, 0, s)) != hipSuccess)
+                return hip_status(e);
+            xbits = packed;
         }
+        const OccParams op = weight_occ_params(desc, plan, dY, dy_mask, x_skip, xbits, workspace);
         if ((e = launch_occupancy(op, s)) != hipSuccess) return hip_status(e);
     }
-    WeightParams p{};
-    p.x = X;
-    p.dy = dY;
-    p.out = plan.direct ? dW : at<float>(workspace, plan.partials);
-    p.occ = skip ? occ : nullptr;
-    p.xlive = skip && x_skip ? at<uint8_t>(workspace, plan.xlive) : nullptr;
-    p.work_slots = at<int32_t>(workspace, plan.work_slots);
-    p.skip_slots = at<int32_t>(workspace, plan.skip_slots);
-    p.header = at<int>(workspace, plan.header);
-    p.N = desc->N; p.H = desc->H; p.W = desc->W; p.C = desc->C; p.K = desc->K; p.R = desc->R; p.S = desc->S;
-    p.P = desc->P; p.Q = desc->Q;
-    p.stride_h = desc->stride_h; p.stride_w = desc->stride_w; p.pad_h = desc->pad_h; p.pad_w = desc->pad_w;
-    p.npq = (int)plan.npq;
-    p.nchunks = plan.nchunks;
-    p.chunks_per_split = plan.chunks_per_split;
-    p.ctiles = plan.ctiles;
-    p.ktiles = plan.ktiles;
-    p.nsplit = plan.nsplit;
-    p.bk = plan.bk;
-    p.tpg = plan.tpg;
-    p.tgroups = plan.tgroups;
-    p.cg = plan.cg;
-    p.mode_flags = (int)flags;
-    p.div_q = make_fastdiv((uint32_t)desc->Q);
-    p.div_p = make_fastdiv((uint32_t)desc->P);
-    p.x_bytes = (uint32_t)((int64_t)desc->N * desc->H * desc->W * desc->C * elem_bytes(desc->dtype));
-    p.dy_bytes = (uint32_t)(plan.npq * desc->K * elem_bytes(desc->dtype));
+    const WeightParams p = weight_gemm_params(desc, plan, X, dY, dW, workspace, skip, x_skip, flags);
     if ((e = launch_bwd_weight(desc->dtype, p, s, prof_events(1))) != hipSuccess) return hip_status(e);
     if (!plan.direct) {
         e = launch_splitk_reduce(p.out, dW, plan.nsplit, desc->K, desc->R * desc->S, desc->C,
@@ -479,6 +536,78 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
         if (e != hipSuccess) return hip_status(e);
     }
     return CBW_OK;
+}
+
+// Both gradients of one layer.  NHWC: four launches whatever is skipped --
+// one preparation (filter transform, compaction counts, dY occupancy), the
+// two GEMMs, one reduction (both split reductions).  NCHW: the two
+// separate calls on the two parts of the workspace.
+static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY, const void* W,
+                        const uint32_t* x_mask, const uint32_t* dy_mask, void* dX, float* dW, void* ws,
+                        size_t ws_bytes, uint32_t flags, void* stream)
+{
+    if (flags & ~(CBW_FLAG_NO_SKIP | CBW_FLAG_SKIP_X_BLOCKS)) return CBW_ERR_INVALID_ARG;
+    size_t off = 0, total = 0;
+    int st = both_offset(desc, &off, &total);
+    if (st != CBW_OK) return st;
+    const bool masked = x_mask != nullptr;
+    DataPlan dplan;
+    WeightPlan wplan;
+    if ((st = plan_data(desc, masked, &dplan)) != CBW_OK) return st;
+    if ((st = plan_weight(desc, &wplan)) != CBW_OK) return st;
+    const bool want_dx = dX != nullptr;   // NULL: the weight gradient alone (a first layer's input has no gradient)
+    if (!X || !dY || !dW || (want_dx && !W)) return CBW_ERR_INVALID_ARG;
+    if (!aligned16(X) || !aligned16(dY) || !aligned16(W) || !aligned16(dX) || !aligned16(dW) ||
+        !aligned16(x_mask) || !aligned16(dy_mask))
+        return CBW_ERR_UNSUPPORTED;
+    if ((st = check_ws(ws, ws_bytes, total)) != CBW_OK) return st;
+    if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;
+    const bool skip = !(flags & CBW_FLAG_NO_SKIP);
+    const bool x_skip = skip && masked && (flags & CBW_FLAG_SKIP_X_BLOCKS);
+    if (x_skip && wplan.tgroups * wplan.ctiles > 1024) return CBW_ERR_UNSUPPORTED;   // liveness flags per chunk
+    void* wws = static_cast<char*>(ws) + off;
+    if (!want_dx)
+        return run_weight(desc, X, dY, x_skip ? x_mask : nullptr, dy_mask, x_skip, dW, wws, total - off,
+                          flags & CBW_FLAG_NO_SKIP, stream);
+    if (desc->act_layout == CBW_NCHW) {
+        st = run_bwd_data(desc, dY, W, x_mask, dX, ws, off, flags & CBW_FLAG_NO_SKIP, stream, masked);
+        if (st != CBW_OK) return st;
+        return run_weight(desc, X, dY, x_skip ? x_mask : nullptr, dy_mask, x_skip, dW, wws, total - off,
+                          flags & CBW_FLAG_NO_SKIP, stream);
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool gather = data_gathers(dplan, masked, flags);
+    const int mode = !masked ? MODE_DENSE : (gather ? MODE_GATHER : MODE_SELECT);
+    int* header = at<int>(ws, dplan.header);
+    void* wt = at<void>(ws, dplan.wt);
+    DataParams dp;
+    CompactParams cp;
+    data_gemm_params(desc, dplan, dY, wt, x_mask, dX, ws, gather, false, &dp, &cp);
+    OccParams op{};
+    if (skip) op = weight_occ_params(desc, wplan, dY, dy_mask, x_skip, x_mask, wws);
+    hipError_t e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S,
+                                    desc->w_layout == CBW_KRSC, header, mode, gather ? &cp : nullptr, s,
+                                    skip ? &op : nullptr);
+    if (e != hipSuccess) return hip_status(e);
+    if ((e = launch_bwd_data(desc->dtype, mode, dp, s, prof_events(0), false)) != hipSuccess) return hip_status(e);
+    const WeightParams wp = weight_gemm_params(desc, wplan, X, dY, dW, wws, skip, x_skip,
+                                               flags & CBW_FLAG_NO_SKIP);
+    if ((e = launch_bwd_weight(desc->dtype, wp, s, prof_events(1))) != hipSuccess) return hip_status(e);
+    ReduceParams rp{};
+    if (!wplan.direct) {
+        const int64_t n4 = (int64_t)desc->K * desc->R * desc->S * desc->C / 4;
+        rp.part = wp.out;
+        rp.dw = dW;
+        rp.nsplit = wplan.nsplit;
+        rp.K = desc->K;
+        rp.RS = desc->R * desc->S;
+        rp.C = desc->C;
+        rp.krsc = desc->w_layout == CBW_KRSC;
+        rp.G = splitk_reduce_group(wplan.nsplit, n4);
+        rp.blocks = (int)((n4 * rp.G + 255) / 256);
+    }
+    const bool dx_reduce = mode == MODE_GATHER || dplan.split > 1;
+    return hip_status(launch_bwd_reduce(desc->dtype, mode, dp, dx_reduce, rp, s));
 }
 
 int conv_bwd_data_elementwise(const cbw_conv_desc* desc, const void* dY, const void* W, const uint32_t* x_mask,
@@ -544,6 +673,13 @@ int conv_bwd_weight_sparse_x(const cbw_conv_desc* desc, const void* X, const voi
     return run_weight(desc, X, dY, x_mask, dy_mask, true, dW, workspace, workspace_bytes, flags, stream);
 }
 
+int conv_bwd_sparse(const cbw_conv_desc* desc, const void* X, const void* dY, const void* W, const uint32_t* x_mask,
+                    const uint32_t* dy_mask, void* dX, float* dW, void* workspace, size_t workspace_bytes,
+                    uint32_t flags, void* stream)
+{
+    return run_bwd_both(desc, X, dY, W, x_mask, dy_mask, dX, dW, workspace, workspace_bytes, flags, stream);
+}
+
 int cbw_read_weight_work(const cbw_conv_desc* desc, const void* workspace, size_t workspace_bytes, int32_t* work,
                          int32_t* nsplit, int32_t* ntiles, void* stream)
 {
@@ -569,6 +705,23 @@ int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, siz
     hipStream_t s = static_cast<hipStream_t>(stream);
     cbw_stats r{};
     int st;
+    if (op == CBW_OP_BWD_BOTH) {
+        // data-gradient rows from the first part, weight-gradient blocks from the second
+        size_t off, total;
+        if ((st = both_offset(desc, &off, &total)) != CBW_OK) return st;
+        if (workspace_bytes < total) return CBW_ERR_WORKSPACE;
+        cbw_stats d{}, w{};
+        if ((st = cbw_read_stats(desc, CBW_OP_BWD_DATA_MASKED, workspace, off, &d, stream)) != CBW_OK) return st;
+        if ((st = cbw_read_stats(desc, CBW_OP_BWD_WEIGHT, static_cast<const char*>(workspace) + off, total - off, &w,
+                                 stream)) != CBW_OK)
+            return st;
+        r.rows_total = d.rows_total;
+        r.rows_live = d.rows_live;
+        r.blocks_total = w.blocks_total;
+        r.blocks_skipped = w.blocks_skipped;
+        *out = r;
+        return CBW_OK;
+    }
     if (op == CBW_OP_BWD_DATA || op == CBW_OP_BWD_DATA_MASKED) {
         DataPlan plan;
         if ((st = plan_data(desc, op == CBW_OP_BWD_DATA_MASKED, &plan)) != CBW_OK) return st;

@@ -34,6 +34,8 @@
 #include "kernels.hpp"
 #include "footprint.hpp"
 #include "tiles.hpp"
+#include "occupancy.hpp"
+#include "reduce.hpp"
 
 
 namespace cbw {
@@ -735,14 +737,16 @@ __device__ __forceinline__ void transform_filters(const T* __restrict__ w, T* __
     }
 }
 
-// One launch for the data gradient's preparation: blocks [0, ntb) transform
-// the filters (block 0 also stamps the workspace header), the remaining
-// blocks (gather mode) count the live pixels of one compaction block each
-// and clear the dX rows of its dead pixels.
+// One launch for the preparation of the data gradient (and, in the call
+// that computes both gradients, of the weight gradient): blocks [0, ntb)
+// transform the filters (block 0 also stamps the workspace header), the next
+// ncb blocks (gather mode) count the live pixels of one compaction block each
+// and clear the dX rows of its dead pixels, and the rest compute the dY
+// block occupancy of the weight gradient.
 template <typename T>
 __global__ __launch_bounds__(256) void data_prep_kernel(const T* __restrict__ w, T* __restrict__ wt, int K, int C,
                                                         int RS, int krsc, int* header, int mode, int ntb,
-                                                        CompactParams cp)
+                                                        CompactParams cp, int ncb, OccParams op)
 {
     if ((int)blockIdx.x < ntb) {
         if (blockIdx.x == 0 && threadIdx.x == 0) header[0] = mode;
@@ -750,7 +754,11 @@ __global__ __launch_bounds__(256) void data_prep_kernel(const T* __restrict__ w,
         return;
     }
     const int b = blockIdx.x - ntb;
-    compact_count_block(cp, b % cp.nblk, b / cp.nblk);
+    if (b < ncb) {
+        compact_count_block(cp, b % cp.nblk, b / cp.nblk);
+        return;
+    }
+    occupancy_block(op, b - ncb);
 }
 
 // Forward preparation (launch_fwd_prep).  Blocks [0, ntb) build the GEMM
@@ -801,17 +809,23 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const T* __restrict__ w, 
 constexpr int kMaxDataSplit = 16;   // the planner's kDataMaxSplit (checked at dispatch)
 
 template <typename T, int MODE, int TI>
-__global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
+__device__ __forceinline__ void data_reduce_block(const DataParams& p, int block, int nblocks)
 {
     constexpr int BM = Tile<TI>::BM, BN = Tile<TI>::BN;
     constexpr int E = Elem<T>::E;
     const int kchunks = (p.K + CH * E - 1) / (CH * E);
     const int nsteps = p.R * p.S * kchunks;
     int ntiles, nsplit;
+    bool dense_map = MODE != MODE_GATHER;   // gather mode with every pixel live tiles like the dense mode
     if (MODE == MODE_GATHER) {
         ntiles = 0;
-        for (int g = 0; g < p.ctiles; ++g) ntiles += (p.counts[g] + BN - 1) / BN;
+        bool all = true;
+        for (int g = 0; g < p.ctiles; ++g) {
+            ntiles += (p.counts[g] + BN - 1) / BN;
+            all &= p.counts[g] == p.npix;
+        }
         nsplit = data_split(ntiles, nsteps, p.nslots, p.smax);
+        dense_map = all;
     } else {
         ntiles = p.ptiles * p.ctiles;
         nsplit = p.split;
@@ -821,23 +835,23 @@ __global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
     if (nsplit <= 1) return;
     const int64_t nvec = (int64_t)ntiles * BN * (BM / 4);
     T* __restrict__ dx = reinterpret_cast<T*>(p.dx);
-    for (int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; v < nvec; v += (int64_t)gridDim.x * blockDim.x) {
+    for (int64_t v = (int64_t)block * 256 + threadIdx.x; v < nvec; v += (int64_t)nblocks * 256) {
         const int tile = (int)(v / (BN * (BM / 4)));
         const int rem = (int)(v - (int64_t)tile * BN * (BM / 4));
         const int pr = rem / (BM / 4), cl = (rem - pr * (BM / 4)) * 4;
         int ctile, ptile;
-        if (MODE == MODE_GATHER) {
+        if (!dense_map) {
             gather_tile(p.counts, p.ctiles, BN, tile, ctile, ptile);
         } else {
             ptile = tile / p.ctiles;
             ctile = tile - ptile * p.ctiles;
         }
         const int r = ptile * BN + pr;
-        const int nrows = MODE == MODE_GATHER ? p.counts[ctile] : p.npix;
+        const int nrows = dense_map ? p.npix : p.counts[ctile];
         const int c = ctile * BM + cl;
         if (r >= nrows || c >= p.C) continue;
         // (a fully live group's list is 0, 1, 2, ... and is not stored)
-        const int pix = MODE == MODE_GATHER && nrows < p.npix ? p.lists[(int64_t)ctile * p.npix + r] : r;
+        const int pix = nrows < p.npix ? p.lists[(int64_t)ctile * p.npix + r] : r;
         // every split's partial is loaded before any is added (latency, not
         // bandwidth, bounds a serial chain of loads); the sum runs in split order
         const float* __restrict__ base = p.partial + ((int64_t)tile * nsplit * BN + pr) * BM + cl;
@@ -889,6 +903,47 @@ __global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
     }
 }
 
+template <typename T, int MODE, int TI>
+__global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
+{
+    data_reduce_block<T, MODE, TI>(p, blockIdx.x, gridDim.x);
+}
+
+// The split reductions of both gradients in one launch (the call that
+// computes both): blocks [0, dw_blocks) sum the weight gradient's split-K
+// partials (G threads per output), the next dx_blocks blocks the data
+// gradient's split tiles (when its reduction was split; they exit at once
+// otherwise).
+template <typename T>
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(DataParams dp, int dx_mode, int dx_blocks, ReduceParams rp)
+{
+    const int b = blockIdx.x;
+    if (b < rp.blocks) {
+        switch (rp.G) {
+        case 1: splitk_reduce_block<1>(rp.part, rp.dw, rp.nsplit, rp.K, rp.RS, rp.C, rp.krsc, b); break;
+        case 2: splitk_reduce_block<2>(rp.part, rp.dw, rp.nsplit, rp.K, rp.RS, rp.C, rp.krsc, b); break;
+        case 4: splitk_reduce_block<4>(rp.part, rp.dw, rp.nsplit, rp.K, rp.RS, rp.C, rp.krsc, b); break;
+        case 8: splitk_reduce_block<8>(rp.part, rp.dw, rp.nsplit, rp.K, rp.RS, rp.C, rp.krsc, b); break;
+        default: splitk_reduce_block<16>(rp.part, rp.dw, rp.nsplit, rp.K, rp.RS, rp.C, rp.krsc, b); break;
+        }
+        return;
+    }
+    const int db = b - rp.blocks;
+    if (dx_mode == MODE_GATHER) {
+        if (dp.tile == 0) data_reduce_block<T, MODE_GATHER, 0>(dp, db, dx_blocks);
+        else if (dp.tile == 1) data_reduce_block<T, MODE_GATHER, 1>(dp, db, dx_blocks);
+        else data_reduce_block<T, MODE_GATHER, 2>(dp, db, dx_blocks);
+    } else if (dx_mode == MODE_SELECT) {
+        if (dp.tile == 0) data_reduce_block<T, MODE_SELECT, 0>(dp, db, dx_blocks);
+        else if (dp.tile == 1) data_reduce_block<T, MODE_SELECT, 1>(dp, db, dx_blocks);
+        else data_reduce_block<T, MODE_SELECT, 2>(dp, db, dx_blocks);
+    } else {
+        if (dp.tile == 0) data_reduce_block<T, MODE_DENSE, 0>(dp, db, dx_blocks);
+        else if (dp.tile == 1) data_reduce_block<T, MODE_DENSE, 1>(dp, db, dx_blocks);
+        else data_reduce_block<T, MODE_DENSE, 2>(dp, db, dx_blocks);
+    }
+}
+
 }  // namespace
 
 int data_tile_channels(int tile)
@@ -901,7 +956,7 @@ int data_tile_pixels(int tile)
 }
 
 hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, int RS, int krsc, int* header,
-                            int mode, const CompactParams* cp, hipStream_t stream)
+                            int mode, const CompactParams* cp, hipStream_t stream, const OccParams* op)
 {
     const int E = dtype == 1 ? 8 : 4;
     const int64_t nthreads = krsc ? (int64_t)K * RS * (C / E) : (int64_t)K * C;
@@ -912,12 +967,32 @@ hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, in
         c = *cp;
         ncb = c.nblk * c.groups;
     }
+    OccParams o{};
+    int nob = 0;
+    if (op) {
+        o = *op;
+        if (o.cpw < 1 || o.cpw * o.ktiles > 1024 || (o.xlive && o.cpw * o.tgroups * o.ctiles > 1024))
+            return hipErrorInvalidValue;
+        nob = (o.nchunks + o.cpw - 1) / o.cpw;
+    }
     if (dtype == 1)
-        data_prep_kernel<uint16_t><<<ntb + ncb, 256, 0, stream>>>((const uint16_t*)w, (uint16_t*)wt, K, C, RS, krsc,
-                                                                  header, mode, ntb, c);
+        data_prep_kernel<uint16_t><<<ntb + ncb + nob, 256, 0, stream>>>((const uint16_t*)w, (uint16_t*)wt, K, C, RS,
+                                                                        krsc, header, mode, ntb, c, ncb, o);
     else
-        data_prep_kernel<float><<<ntb + ncb, 256, 0, stream>>>((const float*)w, (float*)wt, K, C, RS, krsc, header,
-                                                               mode, ntb, c);
+        data_prep_kernel<float><<<ntb + ncb + nob, 256, 0, stream>>>((const float*)w, (float*)wt, K, C, RS, krsc,
+                                                                     header, mode, ntb, c, ncb, o);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_reduce(int dtype, int dx_mode, const DataParams& dp, bool dx_reduce, const ReduceParams& rp,
+                             hipStream_t stream)
+{
+    const int dx_blocks = dx_reduce ? dp.nslots : 0;
+    const int nb = rp.blocks + dx_blocks;
+    if (nb == 0) return hipSuccess;
+    if (dx_reduce && (dp.tile < 0 || dp.tile >= kDataTileCount || dp.smax > kMaxDataSplit)) return hipErrorInvalidValue;
+    if (dtype == 1) bwd_reduce_kernel<uint16_t><<<nb, 256, 0, stream>>>(dp, dx_mode, dx_blocks, rp);
+    else bwd_reduce_kernel<float><<<nb, 256, 0, stream>>>(dp, dx_mode, dx_blocks, rp);
     return hipGetLastError();
 }
 
@@ -943,7 +1018,7 @@ namespace {
 // GEMM (and, when the reduction may be split, the partial-tile reduction) of
 // one element type, mode and tile shape.
 template <typename T, int MODE, int TI>
-hipError_t launch_shape(const DataParams& p, int nb, hipStream_t stream, const ProfEvents& ev)
+hipError_t launch_shape(const DataParams& p, int nb, hipStream_t stream, const ProfEvents& ev, bool with_reduce)
 {
     if (p.stride_h == 1 && p.stride_w == 1)
         hipExtLaunchKernelGGL(bwd_data_kernel<T, MODE, true, TI>, dim3(nb), dim3(Tile<TI>::NT), 0, stream, ev.start,
@@ -954,7 +1029,7 @@ hipError_t launch_shape(const DataParams& p, int nb, hipStream_t stream, const P
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     // in gather mode the split is only known on the device
-    if (MODE == MODE_GATHER || p.split > 1) {
+    if (with_reduce && (MODE == MODE_GATHER || p.split > 1)) {
         splitk_data_reduce_kernel<T, MODE, TI><<<p.nslots, 256, 0, stream>>>(p);
         e = hipGetLastError();
     }
@@ -962,33 +1037,34 @@ hipError_t launch_shape(const DataParams& p, int nb, hipStream_t stream, const P
 }
 
 template <typename T, int MODE>
-hipError_t launch_mode(const DataParams& p, int nb, hipStream_t stream, const ProfEvents& ev)
+hipError_t launch_mode(const DataParams& p, int nb, hipStream_t stream, const ProfEvents& ev, bool wr)
 {
-    if (p.tile == 0) return launch_shape<T, MODE, 0>(p, nb, stream, ev);
-    if (p.tile == 1) return launch_shape<T, MODE, 1>(p, nb, stream, ev);
-    return launch_shape<T, MODE, 2>(p, nb, stream, ev);
+    if (p.tile == 0) return launch_shape<T, MODE, 0>(p, nb, stream, ev, wr);
+    if (p.tile == 1) return launch_shape<T, MODE, 1>(p, nb, stream, ev, wr);
+    return launch_shape<T, MODE, 2>(p, nb, stream, ev, wr);
 }
 
 template <typename T>
-hipError_t launch_type(int mode, const DataParams& p, int nb, hipStream_t stream, const ProfEvents& ev)
+hipError_t launch_type(int mode, const DataParams& p, int nb, hipStream_t stream, const ProfEvents& ev, bool wr)
 {
-    if (mode == MODE_DENSE) return launch_mode<T, MODE_DENSE>(p, nb, stream, ev);
-    if (mode == MODE_SELECT) return launch_mode<T, MODE_SELECT>(p, nb, stream, ev);
-    if (mode == MODE_FWD) return launch_mode<T, MODE_FWD>(p, nb, stream, ev);
-    return launch_mode<T, MODE_GATHER>(p, nb, stream, ev);
+    if (mode == MODE_DENSE) return launch_mode<T, MODE_DENSE>(p, nb, stream, ev, wr);
+    if (mode == MODE_SELECT) return launch_mode<T, MODE_SELECT>(p, nb, stream, ev, wr);
+    if (mode == MODE_FWD) return launch_mode<T, MODE_FWD>(p, nb, stream, ev, wr);
+    return launch_mode<T, MODE_GATHER>(p, nb, stream, ev, wr);
 }
 
 }  // namespace
 
-hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream, const ProfEvents& ev)
+hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream, const ProfEvents& ev,
+                           bool with_reduce)
 {
     // enough workgroups for every tile unsplit (gather mode: at the smallest
     // row choice), or for nslots split items
     const int nb = max(mode == MODE_GATHER ? p.maxtiles : p.ptiles * p.ctiles, p.nslots);
     if (nb <= 0) return hipSuccess;
     if (p.tile < 0 || p.tile >= kDataTileCount || p.smax > kMaxDataSplit) return hipErrorInvalidValue;
-    return dtype == 1 ? launch_type<uint16_t>(mode, p, nb, stream, ev)
-                      : launch_type<float>(mode, p, nb, stream, ev);
+    return dtype == 1 ? launch_type<uint16_t>(mode, p, nb, stream, ev, with_reduce)
+                      : launch_type<float>(mode, p, nb, stream, ev, with_reduce);
 }
 
 }  // namespace cbw

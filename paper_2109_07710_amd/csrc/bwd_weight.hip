@@ -53,11 +53,11 @@ constexpr int OCC_WIN = 1024;   // occupancy bytes cached per workgroup
 // and when every chunk is live they are the unskipped ranges, which keeps
 // the two results bitwise equal.
 //
-// Tiles of up to TILE_LIVE_CAP chunks stage their liveness in LDS in one
-// coalesced pass (four loads in flight per thread) that also decides the
-// all-live case; each thread then counts a contiguous segment of it from LDS
-// (a bit mask for segments of up to 32 chunks).  Larger tiles read their
-// segments from global memory.  The ranks come from a wave-level shuffle
+// One coalesced pass over the tile's liveness (eight loads in flight per
+// thread) decides the all-live case; tiles of up to TILE_LIVE_CAP chunks also
+// stage their liveness in LDS in it.  Otherwise each thread then counts a
+// contiguous segment of it, from LDS when staged, else from global memory (a
+// bit mask for segments of up to 32 chunks).  The ranks come from a wave-level shuffle
 // scan and one exchange of wave totals.  Called by the whole workgroup before
 // any operand copy; scratch is SPLIT_SCRATCH_BYTES of LDS, free until the
 // function returns.
@@ -83,6 +83,32 @@ __device__ bool split_range(const WeightParams& p, int kt, int combo, int z, int
         if (p.xlive) v &= p.xlive[(int64_t)c * ncombo + combo];
         return v != 0;
     };
+    // Fast test first: every byte of the occupancy map (and of the X-window
+    // liveness) is 1, read 16 bytes at a time with eight loads in flight --
+    // the usual case for element-wise footprints, decided with a few loads
+    // per thread even for tiles of tens of thousands of chunks.
+    auto all_ones = [&](const uint8_t* m, int64_t n) -> bool {
+        const uint4* v = reinterpret_cast<const uint4*>(m);
+        const int64_t nv = n / 16;
+        bool ok = true;
+        for (int64_t i0 = tid; i0 < nv; i0 += 8 * T) {
+            uint4 a[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                a[u] = i0 + u * T < nv ? v[i0 + u * T] : make_uint4(0x01010101u, 0x01010101u, 0x01010101u, 0x01010101u);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) ok &= (a[u].x & a[u].y & a[u].z & a[u].w) == 0x01010101u;
+        }
+        for (int64_t i = nv * 16 + tid; i < n; i += T) ok &= m[i] == 1;
+        return ok;
+    };
+    bool every = all_ones(p.occ, (int64_t)nch * p.ktiles);
+    if (p.xlive) every &= all_ones(p.xlive, (int64_t)nch * ncombo);
+    if (__syncthreads_and(every)) {
+        begin = min(nch, z * p.chunks_per_split);
+        end = min(nch, begin + p.chunks_per_split);
+        return true;
+    }
     int* wsum = reinterpret_cast<int*>(scratch);         // [0, 16): wave totals
     int* pos = wsum + 32;                                // [32, 34): chunk of ranks r0, r1
     uint8_t* tl = scratch + 256;                         // tile liveness when staged
@@ -91,25 +117,18 @@ __device__ bool split_range(const WeightParams& p, int kt, int combo, int z, int
     const int s0 = min(nch, tid * per), s1 = min(nch, s0 + per);
     int cnt = 0;
     uint32_t bits = 0;   // bit i: chunk s0 + i is live (segments of up to 32 chunks)
+    // one coalesced pass over the tile's liveness, eight loads in flight per
+    // thread, decides the all-live case (and stages the liveness when it fits)
     bool all = true;
-    if (staged) {
-        for (int cb = tid; cb < nch; cb += 4 * T) {
-            int v[4];
+    for (int cb = tid; cb < nch; cb += 8 * T) {
+        int v[8];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) v[u] = cb + u * T < nch ? live(cb + u * T) : 1;
+        for (int u = 0; u < 8; ++u) v[u] = cb + u * T < nch ? live(cb + u * T) : 1;
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                if (cb + u * T < nch) tl[cb + u * T] = (uint8_t)v[u];
-                all &= v[u] != 0;
-            }
+        for (int u = 0; u < 8; ++u) {
+            if (staged && cb + u * T < nch) tl[cb + u * T] = (uint8_t)v[u];
+            all &= v[u] != 0;
         }
-    } else {
-        for (int c = s0; c < s1; ++c) {
-            const int v = live(c);
-            cnt += v;
-            bits |= (uint32_t)v << ((c - s0) & 31);
-        }
-        all = cnt == s1 - s0;
     }
     // every chunk live (the usual case for element-wise footprints): the
     // ranges are the unskipped ones and nothing needs ranking
@@ -118,12 +137,10 @@ __device__ bool split_range(const WeightParams& p, int kt, int combo, int z, int
         end = min(nch, begin + p.chunks_per_split);
         return true;
     }
-    if (staged) {
-        for (int c = s0; c < s1; ++c) {
-            const int v = tl[c];
-            cnt += v;
-            bits |= (uint32_t)v << ((c - s0) & 31);
-        }
+    for (int c = s0; c < s1; ++c) {
+        const int v = staged ? (int)tl[c] : live(c);
+        cnt += v;
+        bits |= (uint32_t)v << ((c - s0) & 31);
     }
     // otherwise an inclusive scan of the counts over the threads: within
     // each wave by shuffles, then across the waves' totals

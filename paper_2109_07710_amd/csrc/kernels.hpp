@@ -110,15 +110,30 @@ int weight_chunk(int dtype);
 int compact_block_pixels();
 
 // Filter transform (and, when cp is given, the compaction counts and the
-// dead-row zero fill) in one launch.
+// dead-row zero fill; when op is given, the weight gradient's dY block
+// occupancy) in one launch.
 hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, int RS, int krsc, int* header,
-                            int mode, const CompactParams* cp, hipStream_t stream);
+                            int mode, const CompactParams* cp, hipStream_t stream, const OccParams* op = nullptr);
 // Optional timing events attached to the dispatch of a GEMM kernel (both
 // may be null): they record the kernel's own begin and end.
 struct ProfEvents {
     hipEvent_t start = nullptr, stop = nullptr;
 };
-hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream, const ProfEvents& ev);
+// with_reduce = false leaves a split reduction to launch_bwd_reduce.
+hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream, const ProfEvents& ev,
+                           bool with_reduce = true);
+// The weight gradient's split-K reduction (rp.blocks workgroups, none when
+// dW was written directly) and, when dx_reduce, the data gradient's split
+// tiles, in one launch.
+struct ReduceParams {
+    const float* part;       // [nsplit][K][RS][C] weight-gradient partials
+    float* dw;
+    int nsplit, K, RS, C, krsc;
+    int G;                   // threads per output (splitk_reduce_group)
+    int blocks;              // workgroups of the weight-gradient part
+};
+hipError_t launch_bwd_reduce(int dtype, int dx_mode, const DataParams& dp, bool dx_reduce, const ReduceParams& rp,
+                             hipStream_t stream);
 // Forward preparation: Wf[tap'][k][c] = W[k][tap][c] with tap' the flipped tap
 // (R-1-r, S-1-s), the workspace header stamped, and `zero_words` words of
 // `zero` cleared (footprint words filled by atomic OR), in one launch.

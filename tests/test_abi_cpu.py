@@ -277,3 +277,34 @@ def test_peaks_library_exports_its_header():
     assert pk.mfma_flops(pk.MFMA_32X32X16, 1, 1) == 2 * 32 * 32 * 16 * 4 * 4
     assert PL.cbw_peak_mfma(7, 1, 1, None, None, None) == -1
     assert PL.cbw_peak_hbm_copy(None, None, 16, None) == -1
+
+
+def test_both_gradients_workspace_and_validation(L):
+    """conv_bwd_sparse: its workspace holds the masked data gradient's, then
+    (from the next 256-byte boundary) the weight gradient's; every argument
+    error is reported before anything is launched."""
+    d = cb.ConvDesc.make(32, 256, 56, 56, 256, 3, 3, 1, 1)
+    both = cb.cbw_workspace_size(d, cb.CBW_OP_BWD_BOTH)
+    masked = cb.cbw_workspace_size(d, cb.CBW_OP_BWD_DATA_MASKED)
+    wgt = cb.cbw_workspace_size(d, cb.CBW_OP_BWD_WEIGHT)
+    off = cb.both_weight_offset(d)
+    assert off % 256 == 0 and masked <= off < masked + 256
+    assert both == off + wgt
+    fake = ctypes.c_void_p(1 << 20)
+    call = L.conv_bwd_sparse
+    # null tensors, then unknown flags, then misaligned pointers, then the workspace
+    assert call(ctypes.byref(d), None, fake, fake, None, None, fake, fake, None, 0, 0, None) == \
+        cb.CBW_ERR_INVALID_ARG
+    assert call(ctypes.byref(d), fake, fake, fake, None, None, fake, fake, None, 0, 4, None) == \
+        cb.CBW_ERR_INVALID_ARG
+    misaligned = ctypes.c_void_p((1 << 20) + 4)
+    assert call(ctypes.byref(d), fake, fake, fake, misaligned, None, fake, fake, None, 0, 0, None) == \
+        cb.CBW_ERR_UNSUPPORTED
+    assert call(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, None, 0, 0, None) == \
+        cb.CBW_ERR_WORKSPACE
+    assert call(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, both - 1, 0, None) == \
+        cb.CBW_ERR_WORKSPACE
+    bad = cb.ConvDesc.make(32, 256, 56, 56, 256, 3, 3, 1, 1)
+    bad.P += 1
+    assert call(ctypes.byref(bad), fake, fake, fake, None, None, fake, fake, fake, both, 0, None) == \
+        cb.CBW_ERR_INVALID_ARG
