@@ -127,12 +127,32 @@ bool data_gathers(const DataPlan& plan, bool masked, uint32_t flags)
 int both_offset(const cbw_conv_desc* desc, size_t* off, size_t* total)
 {
     DataPlan dp;
-    WeightPlan wp;
+    size_t wbytes = 0;
     int st = plan_data(desc, true, &dp);
     if (st != CBW_OK) return st;
-    if ((st = plan_weight(desc, &wp)) != CBW_OK) return st;
+    if ((st = weight_ws_bytes(desc, &wbytes)) != CBW_OK) return st;
     *off = (dp.total + 255) & ~(size_t)255;
-    *total = *off + wp.total;
+    *total = *off + wbytes;
+    return CBW_OK;
+}
+
+// The weight-gradient plan the last call on `workspace` ran (its kernel
+// stamps which one into the header), for the readers.
+int last_weight_plan(const cbw_conv_desc* desc, const void* workspace, size_t workspace_bytes, WeightPlan* plan,
+                     hipStream_t s)
+{
+    WeightPlan p;
+    int st = plan_weight(desc, &p, false);
+    if (st != CBW_OK) return st;
+    if (!workspace) return CBW_ERR_INVALID_ARG;
+    if (workspace_bytes < 256) return CBW_ERR_WORKSPACE;
+    int hdr[2] = {0, 0};
+    hipError_t e = hipMemcpyAsync(hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_status(e);
+    if ((st = plan_weight(desc, &p, hdr[1] == 1)) != CBW_OK) return st;
+    if (workspace_bytes < p.total) return CBW_ERR_WORKSPACE;
+    *plan = p;
     return CBW_OK;
 }
 
@@ -322,12 +342,7 @@ int cbw_workspace_size(const cbw_conv_desc* desc, int op, size_t* bytes)
         *bytes = p.total;
         return CBW_OK;
     }
-    if (op == CBW_OP_BWD_WEIGHT) {
-        WeightPlan p;
-        if ((st = plan_weight(desc, &p)) != CBW_OK) return st;
-        *bytes = p.total;
-        return CBW_OK;
-    }
+    if (op == CBW_OP_BWD_WEIGHT) return weight_ws_bytes(desc, bytes);
     if (op == CBW_OP_BWD_DATA_ELEMENTWISE) {
         if ((st = validate_elementwise(desc)) != CBW_OK) return st;
         *bytes = elementwise_ws(desc);
@@ -412,7 +427,7 @@ static OccParams weight_occ_params(const cbw_conv_desc* desc, const WeightPlan& 
     op.occ = at<uint8_t>(workspace, plan.occ);
     op.npq = (int)plan.npq;
     op.K = desc->K;
-    op.chunk = weight_chunk_px(desc->dtype);
+    op.chunk = plan.chunk;
     op.BNk = plan.bk;
     op.ktiles = plan.ktiles;
     op.nchunks = plan.nchunks;
@@ -420,7 +435,7 @@ static OccParams weight_occ_params(const cbw_conv_desc* desc, const WeightPlan& 
     // (one with X-window liveness, whose test loops over taps), within the
     // per-chunk flag arrays (1024 entries each)
     const int ncombo = x_skip ? plan.tgroups * plan.ctiles : 1;
-    const int per_chunk = weight_chunk_px(desc->dtype) * plan.ktiles;
+    const int per_chunk = plan.chunk * plan.ktiles;
     op.cpw = std::max(1, std::min((x_skip ? 256 : 1024) / per_chunk, 1024 / std::max(plan.ktiles, ncombo)));
     op.dtype = desc->dtype;
     if (x_skip) {
@@ -467,6 +482,7 @@ static WeightParams weight_gemm_params(const cbw_conv_desc* desc, const WeightPl
     p.tpg = plan.tpg;
     p.tgroups = plan.tgroups;
     p.cg = plan.cg;
+    p.rows = plan.rows ? 1 : 0;
     p.mode_flags = (int)flags;
     p.div_q = make_fastdiv((uint32_t)desc->Q);
     p.div_p = make_fastdiv((uint32_t)desc->P);
@@ -481,7 +497,7 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
                uint32_t flags, void* stream)
 {
     WeightPlan plan;
-    int st = plan_weight(desc, &plan);
+    int st = plan_weight(desc, &plan, !x_skip);   // X-block skipping runs the chunked kernel
     if (st != CBW_OK) return st;
     if (!X || !dY || !dW) return CBW_ERR_INVALID_ARG;
     if (!aligned16(X) || !aligned16(dY) || !aligned16(dW) || !aligned16(dy_mask) || !aligned16(x_mask))
@@ -531,7 +547,7 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
     const WeightParams p = weight_gemm_params(desc, plan, X, dY, dW, workspace, skip, x_skip, flags);
     if ((e = launch_bwd_weight(desc->dtype, p, s, prof_events(1))) != hipSuccess) return hip_status(e);
     if (!plan.direct) {
-        e = launch_splitk_reduce(p.out, dW, plan.nsplit, desc->K, desc->R * desc->S, desc->C,
+        e = launch_splitk_reduce(p.out, dW, plan.nparts, desc->K, desc->R * desc->S, desc->C,
                                  desc->w_layout == CBW_KRSC, s);
         if (e != hipSuccess) return hip_status(e);
     }
@@ -551,10 +567,12 @@ static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY
     int st = both_offset(desc, &off, &total);
     if (st != CBW_OK) return st;
     const bool masked = x_mask != nullptr;
+    const bool skip = !(flags & CBW_FLAG_NO_SKIP);
+    const bool x_skip = skip && masked && (flags & CBW_FLAG_SKIP_X_BLOCKS);
     DataPlan dplan;
     WeightPlan wplan;
     if ((st = plan_data(desc, masked, &dplan)) != CBW_OK) return st;
-    if ((st = plan_weight(desc, &wplan)) != CBW_OK) return st;
+    if ((st = plan_weight(desc, &wplan, !x_skip)) != CBW_OK) return st;
     const bool want_dx = dX != nullptr;   // NULL: the weight gradient alone (a first layer's input has no gradient)
     if (!X || !dY || !dW || (want_dx && !W)) return CBW_ERR_INVALID_ARG;
     if (!aligned16(X) || !aligned16(dY) || !aligned16(W) || !aligned16(dX) || !aligned16(dW) ||
@@ -562,8 +580,6 @@ static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY
         return CBW_ERR_UNSUPPORTED;
     if ((st = check_ws(ws, ws_bytes, total)) != CBW_OK) return st;
     if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;
-    const bool skip = !(flags & CBW_FLAG_NO_SKIP);
-    const bool x_skip = skip && masked && (flags & CBW_FLAG_SKIP_X_BLOCKS);
     if (x_skip && wplan.tgroups * wplan.ctiles > 1024) return CBW_ERR_UNSUPPORTED;   // liveness flags per chunk
     void* wws = static_cast<char*>(ws) + off;
     if (!want_dx)
@@ -598,12 +614,12 @@ static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY
         const int64_t n4 = (int64_t)desc->K * desc->R * desc->S * desc->C / 4;
         rp.part = wp.out;
         rp.dw = dW;
-        rp.nsplit = wplan.nsplit;
+        rp.nsplit = wplan.nparts;
         rp.K = desc->K;
         rp.RS = desc->R * desc->S;
         rp.C = desc->C;
         rp.krsc = desc->w_layout == CBW_KRSC;
-        rp.G = splitk_reduce_group(wplan.nsplit, n4);
+        rp.G = splitk_reduce_group(wplan.nparts, n4);
         rp.blocks = (int)((n4 * rp.G + 255) / 256);
     }
     const bool dx_reduce = mode == MODE_GATHER || dplan.split > 1;
@@ -684,10 +700,9 @@ int cbw_read_weight_work(const cbw_conv_desc* desc, const void* workspace, size_
                          int32_t* nsplit, int32_t* ntiles, void* stream)
 {
     WeightPlan plan;
-    int st = plan_weight(desc, &plan);
-    if (st != CBW_OK) return st;
     if (!workspace || !nsplit || !ntiles) return CBW_ERR_INVALID_ARG;
-    if (workspace_bytes < plan.total) return CBW_ERR_WORKSPACE;
+    int st = last_weight_plan(desc, workspace, workspace_bytes, &plan, static_cast<hipStream_t>(stream));
+    if (st != CBW_OK) return st;
     *nsplit = plan.nsplit;
     *ntiles = plan.grid / plan.nsplit;
     if (!work) return CBW_OK;
@@ -748,8 +763,7 @@ int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, siz
         }
     } else if (op == CBW_OP_BWD_WEIGHT) {
         WeightPlan plan;
-        if ((st = plan_weight(desc, &plan)) != CBW_OK) return st;
-        if (workspace_bytes < plan.total) return CBW_ERR_WORKSPACE;
+        if ((st = last_weight_plan(desc, workspace, workspace_bytes, &plan, s)) != CBW_OK) return st;
         r.blocks_total = (int64_t)plan.nchunks * plan.ktiles * plan.tgroups * plan.ctiles;
         int64_t skipped = 0;
         int32_t buf[256];
@@ -817,13 +831,12 @@ int cbw_read_occupancy(const cbw_conv_desc* desc, const void* workspace, size_t 
                        void* stream)
 {
     WeightPlan plan;
-    int st = plan_weight(desc, &plan);
-    if (st != CBW_OK) return st;
     if (!workspace || !nchunks || !ktiles || !chunk_pixels || !ktile_width) return CBW_ERR_INVALID_ARG;
-    if (workspace_bytes < plan.total) return CBW_ERR_WORKSPACE;
+    int st = last_weight_plan(desc, workspace, workspace_bytes, &plan, static_cast<hipStream_t>(stream));
+    if (st != CBW_OK) return st;
     *nchunks = plan.nchunks;
     *ktiles = plan.ktiles;
-    *chunk_pixels = weight_chunk_px(desc->dtype);
+    *chunk_pixels = plan.chunk;
     *ktile_width = plan.bk;
     if (occ) {
         hipStream_t s = static_cast<hipStream_t>(stream);

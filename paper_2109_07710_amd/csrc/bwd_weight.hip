@@ -302,8 +302,10 @@ __global__ __launch_bounds__(NT) void bwd_weight_kernel(WeightParams p)
     const int r = tap / p.S, s = tap - r * p.S;
     const int c0 = ct * BM, k0 = kt * BN;
 
-    if (blockIdx.x == 0 && tid == 0) p.header[0] = p.mode_flags;
-
+    if (blockIdx.x == 0 && tid == 0) {
+        p.header[0] = p.mode_flags;
+        p.header[1] = 0;   // the readers' plan: 64-pixel chunks
+    }
 
     floatx4 acc[FM][FN];
 #pragma unroll
@@ -533,8 +535,10 @@ __global__ __launch_bounds__(WTile<BKT>::NT) void bwd_weight_tr_kernel(WeightPar
     // fragment reads and matrix instructions (it still copies and waits).
     const int used_cols = p.tpg > 1 ? min(p.tpg, RS - tg * p.tpg) * cg : min(BM, p.C - c0);
 
-    if (blockIdx.x == 0 && tid == 0) p.header[0] = p.mode_flags;
-
+    if (blockIdx.x == 0 && tid == 0) {
+        p.header[0] = p.mode_flags;
+        p.header[1] = 0;   // the readers' plan: 64-pixel chunks
+    }
 
     const u32x4_t rs_x = make_rsrc_words(p.x, p.x_bytes);
     const u32x4_t rs_dy = make_rsrc_words(p.dy, p.dy_bytes);
@@ -691,6 +695,323 @@ __global__ __launch_bounds__(WTile<BKT>::NT) void bwd_weight_tr_kernel(WeightPar
     }
 }
 
+// Row-window weight gradient for narrow stride-1 layers (64 or 128 input and
+// output channels, filters of at most 3 x 3).  A workgroup owns a 64-wide
+// output-channel tile, a 64-wide channel tile and a segment of up to 128
+// output columns q, and accumulates all R*S taps of dW over a range of
+// output rows (n, p) -- one row per step:
+//
+//   dW[k, r, s, c] += sum_q  X[n, p - ph + r, q - pw + s, c] * dY[n, p, q, k]
+//
+// The X rows a step needs are the R input rows p - ph .. p - ph + R - 1, each
+// read into LDS once with its halo columns (zeros outside the image) and
+// shared by the S taps of its filter row: the tap shift s is an offset of
+// the row index at which the matrix fragments are read.  Consecutive output
+// rows of one image share R - 1 of those input rows, so X rows sit in a ring
+// of four and a step copies one new input row and one dY row segment while
+// the previous step computes.  Per output pixel that is 2 x 128 bytes of
+// copies for 2 * 64 * R*S * 64 multiply-adds (the chunked kernel copies the
+// X row once per tap).
+//
+// GEMM view per step: M = (tap, c) columns (A = shifted X rows), N = k
+// (B = dY), reduction = q in 32-column chunks; both operands sit in LDS in
+// their natural [column][channel] order and the fragments are read with
+// ds_read_b64_tr_b16 (as in the chunked kernel).  Input sparsity: the
+// "chunks" of the skip machinery are whole output rows (occupancy per row
+// and k tile), ranked into balanced splits exactly as above.
+constexpr int RW_NT = 512;               // 8 waves: 2 along k (32 each) x 4 column quarters
+constexpr int RW_QT = 128;               // output columns per segment (multiple of 32)
+constexpr int RW_XROWS = 136;            // X row slots: RW_QT + S - 1 halo columns, in groups of 8
+constexpr int RW_SLOTS = 5;              // X ring: R rows in use plus the next two steps' new rows
+constexpr int RW_YBUF = 3;               // dY segments: this step and the next two
+constexpr int RW_NB = 9;                 // column blocks (16 columns) per wave at most: 36 / 4
+static_assert(RW_QT % 32 == 0 && RW_XROWS >= RW_QT + 2 && RW_XROWS % 8 == 0, "row-window shape");
+
+// LDS chunk swizzle of the 128-byte rows (8 chunks).  The LDS serves 256
+// bytes (64 banks) per cycle, a row of even index the lower half of the
+// banks and one of odd index the upper half, and a transpose read takes 32
+// lanes per cycle: rows b .. b+3 and b+8 .. b+11, 32 bytes (one chunk pair)
+// each.  The pair is moved by bits 1 and 3 of the row, which differ among
+// the four rows of either parity for every b (tap shifts included), so the
+// eight chunk pairs of a cycle never share a bank.  (Moving the pair by the
+// row's two low bits, as first tried, left the rows 8 apart on the same
+// banks: bank-conflict cycles were half of the LDS's active cycles.)
+__device__ __forceinline__ int trswz8(int row) { return 2 * (((row >> 1) & 1) | (((row >> 3) & 1) << 1)); }
+
+// Ring slot of input row h (h >= -16): (h + 20) mod 5 by a multiply and shift
+// (x / 5 = (x * 52429) >> 18 for 0 <= x < 2^16).
+__device__ __forceinline__ int ring_slot(int h)
+{
+    static_assert(RW_SLOTS == 5, "the slot formula divides by 5");
+    const uint32_t x = (uint32_t)(h + 20);
+    return (int)(x - ((x * 52429u) >> 18) * 5u);
+}
+
+// NB: column blocks per wave, R*S (every wave holds R*S of the 4 R*S blocks).
+template <int NB>
+__global__ __launch_bounds__(RW_NT) void bwd_weight_rows_kernel(WeightParams p)
+{
+    static_assert(NB >= 1 && NB <= RW_NB, "at most 3 x 3 taps");
+    constexpr uint32_t ESZ = 2;
+    constexpr int NW = RW_NT / 64;
+    __shared__ uint4 Ys[RW_YBUF][RW_QT * 8];         // dY segments of output rows, [q][k]
+    __shared__ uint4 Xs[RW_SLOTS][RW_XROWS * 8];     // input rows with halo, [w][c]
+    __shared__ uint8_t live_s[OCC_WIN];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const int wk = wave_u & 1, wq = wave_u >> 1;     // k half, column quarter
+    const int RS = p.R * p.S;
+
+    // work item: split z of tile (q segment, channel tile, k tile)
+    const int tiles = p.tgroups * p.ctiles * p.ktiles;   // tgroups = q segments here
+    const int t = xcd_remap(blockIdx.x, gridDim.x);
+    const int z = t / tiles;
+    int rem = t - z * tiles;
+    const int kt = rem % p.ktiles;
+    rem /= p.ktiles;
+    const int ct = rem % p.ctiles;
+    const int qt = rem / p.ctiles;
+    const int k0 = kt * 64, c0 = ct * 64, q0 = qt * RW_QT;
+    const int qn = min(RW_QT, p.Q - q0);             // valid columns of the segment
+    const int nqc = (qn + 31) >> 5;                  // 32-column reduction chunks
+    const int xn = qn + p.S - 1;                     // X columns the segment reads
+    if (blockIdx.x == 0 && tid == 0) {
+        p.header[0] = p.mode_flags;
+        p.header[1] = 1;   // the readers' plan: row-window chunks
+    }
+
+    const u32x4_t rs_x = make_rsrc_words(p.x, p.x_bytes);
+    const u32x4_t rs_dy = make_rsrc_words(p.dy, p.dy_bytes);
+
+    // this wave's column blocks: [cb0, cb0 + nbw) of the R*S*4 blocks
+    // (block b = tap b / 4, channels 16 (b % 4) .. + 15 of the tile)
+    const int ncb = RS * 4;
+    const int nbq = (ncb + 3) >> 2;
+    const int cb0 = wq * nbq;
+    constexpr int nbw = NB;
+    (void)nbq;
+
+    floatx4 acc[NB][2];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) acc[j][0] = acc[j][1] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    // copies: lane l of a wave serves row 8g + l/8 at physical chunk l%8,
+    // i.e. logical chunk (l%8) ^ trswz8(row)
+    const int lrow8 = lane >> 3, pch = lane & 7;
+    // Each copy helper returns how many copy instructions this wave issued
+    // (the waits below count them).  A lane's byte offset is a scalar row
+    // base plus a per-lane part computed once here (kOOB where the column
+    // lies outside the segment or the image).
+    constexpr int YG = (RW_QT / 8 + NW - 1) / NW, XG = (RW_XROWS / 8 + NW - 1) / NW;
+    uint32_t ylane[YG], xlane[XG];
+#pragma unroll
+    for (int u = 0; u < YG; ++u) {
+        const int i = 8 * (wave_u + NW * u) + lrow8;
+        const int lc = pch ^ trswz8(i);
+        ylane[u] = i < qn ? (uint32_t)(((q0 + i) * p.K + k0 + lc * 8) * ESZ) : kOOB;
+    }
+#pragma unroll
+    for (int u = 0; u < XG; ++u) {
+        const int i = 8 * (wave_u + NW * u) + lrow8;
+        const int lc = pch ^ trswz8(i);
+        const int w = q0 - p.pad_w + i;
+        xlane[u] = (i < xn && w >= 0 && w < p.W) ? (uint32_t)((w * p.C + c0 + lc * 8) * ESZ) : kOOB;
+    }
+    auto copy_y = [&](int buf, int row) -> int {   // dY segment of output row `row` = n*P + p
+        const uint32_t base = (uint32_t)row * (uint32_t)(p.Q * p.K * ESZ);
+        int issued = 0;
+#pragma unroll
+        for (int u = 0; u < YG; ++u) {
+            const int g = wave_u + NW * u;
+            if (g < RW_QT / 8) {
+                buf_load16_lds(rs_dy, ylane[u] == kOOB ? kOOB : base + ylane[u], lds_addr(&Ys[buf][g * 64]));
+                ++issued;
+            }
+        }
+        return issued;
+    };
+    auto copy_x = [&](int n, int h) -> int {   // input row h of image n into its ring slot
+        const int slot = ring_slot(h);
+        const bool hin = h >= 0 && h < p.H;
+        const uint32_t base = hin ? (uint32_t)(n * p.H + h) * (uint32_t)(p.W * p.C * ESZ) : 0u;
+        int issued = 0;
+#pragma unroll
+        for (int u = 0; u < XG; ++u) {
+            const int g = wave_u + NW * u;
+            if (g < RW_XROWS / 8) {
+                buf_load16_lds(rs_x, (!hin || xlane[u] == kOOB) ? kOOB : base + xlane[u],
+                               lds_addr(&Xs[slot][g * 64]));
+                ++issued;
+            }
+        }
+        return issued;
+    };
+
+    // fragment addresses (bytes in a buffer of 128-byte rows), as tr_addr
+    const int kg = lane >> 4, q4 = lane & 3, m4 = (lane >> 2) & 3;
+    auto tr8 = [&](int row, int cb) {
+        const int col = cb + 4 * q4;
+        return row * 128 + (((col >> 3) ^ trswz8(row)) << 4) + ((col & 7) << 1);
+    };
+    // per column block of this wave: filter row, column shift and channel base
+    int b_r[NB], b_s[NB], b_c[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        const int b = cb0 + j, tap = b >> 2;
+        b_r[j] = tap / p.S;
+        b_s[j] = tap - b_r[j] * p.S;
+        b_c[j] = (b & 3) * 16;
+    }
+
+    // Fragment addresses.  Within a buffer the address of a fragment read is
+    // a per-lane part fixed for the whole kernel (row 8 kg + m, plus the
+    // column shift s, and the swizzled column) plus 4096 bytes per 32-row
+    // chunk (the swizzle does not depend on bits 5 and up), which the
+    // unrolled chunk loop folds into the instructions' offset fields; only
+    // the ring slot of each X block changes from step to step.  So the inner
+    // loop issues reads and matrix instructions with no address arithmetic.
+    int xl[NB][2], yl[2][2];
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) xl[j][h] = tr8(8 * kg + m4 + 4 * h + b_s[j], b_c[j]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) yl[i][h] = tr8(8 * kg + m4 + 4 * h, wk * 32 + i * 16);
+    const char* X0 = reinterpret_cast<const char*>(Xs);
+    auto compute = [&](int ybuf, int pp) {
+        const char* Yb = reinterpret_cast<const char*>(Ys[ybuf]);
+        const char* Xb[NB];
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            const int h = pp - p.pad_h + b_r[j];
+            Xb[j] = X0 + ring_slot(h) * (int)sizeof(Xs[0]) + xl[j][0];
+        }
+        // per 32-column chunk: the chunk's eleven fragment pairs are read,
+        // then its 18 matrix instructions; the other wave on the SIMD
+        // overlaps its reads with them
+#pragma unroll
+        for (int kc = 0; kc < RW_QT / 32; ++kc) {
+            if (kc < nqc) {   // uniform
+                uint4 fb[2], fa[NB];
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    const uint2 lo = ds_read_tr16(Yb + yl[i][0] + kc * 4096);
+                    const uint2 hi = ds_read_tr16(Yb + yl[i][1] + kc * 4096);
+                    fb[i] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                }
+#pragma unroll
+                for (int j = 0; j < NB; ++j) {
+                    if (j < nbw) {   // uniform; every index stays a compile-time constant
+                        const uint2 lo = ds_read_tr16(Xb[j] + kc * 4096);
+                        const uint2 hi = ds_read_tr16(Xb[j] + (xl[j][1] - xl[j][0]) + kc * 4096);
+                        fa[j] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < NB; ++j) {
+                    if (j < nbw) {
+                        acc[j][0] = mfma_chunk(acc[j][0], fa[j], fb[0], uint16_t{});
+                        acc[j][1] = mfma_chunk(acc[j][1], fa[j], fb[1], uint16_t{});
+                    }
+                }
+            }
+        }
+    };
+
+    // this split's row range, balanced over the live rows when skipping
+    const int combo = qt * p.ctiles + ct;
+    int ch_begin, ch_end;
+    static_assert(sizeof(Xs) >= SPLIT_SCRATCH_BYTES, "ranking scratch fits the X ring");
+    const bool all_live = split_range(p, kt, combo, z, ch_begin, ch_end, live_s, reinterpret_cast<uint8_t*>(Xs));
+    int skipped = 0;
+    auto next_live = [&](int row) {
+        return all_live ? row : next_live_chunk(p, live_s, ch_begin, ch_end, kt, combo, row, skipped);
+    };
+
+    // Pipeline over the live output rows ra (this step), rb and rc (the next
+    // two): the copies of step i + 2 are issued at step i (its dY
+    // segment, and its one new input row when steps i .. i + 2 are
+    // consecutive rows of one image), so every copy has two steps' matrix
+    // work to land; the wait at the end of step i leaves exactly the copies
+    // just issued in flight.  A step that does not follow its predecessor
+    // (next image, or dead rows skipped) has its R input rows loaded after
+    // the step before it, with the next step's new row if that one follows.
+    auto follows = [&](int a, int b) {   // output row b comes right after a in the same image
+        return b == a + 1 && fdiv((uint32_t)b, p.div_p) == fdiv((uint32_t)a, p.div_p);
+    };
+    int ra = next_live(ch_begin);
+    int rb = ra < ch_end ? next_live(ra + 1) : ch_end;
+    int rc = rb < ch_end ? next_live(rb + 1) : ch_end;
+    auto new_row = [&](int c) {          // the input row a following output row adds to the window
+        const int n = (int)fdiv((uint32_t)c, p.div_p), pp = c - n * p.P;
+        return copy_x(n, pp - p.pad_h + p.R - 1);
+    };
+    auto all_rows = [&](int c) {
+        const int n = (int)fdiv((uint32_t)c, p.div_p), pp = c - n * p.P;
+        for (int r = 0; r < p.R; ++r) copy_x(n, pp - p.pad_h + r);
+    };
+    if (ra < ch_end) {
+        copy_y(0, ra);
+        all_rows(ra);
+        if (rb < ch_end) {
+            copy_y(1, rb);
+            if (follows(ra, rb)) new_row(rb);
+        }
+    }
+    wait_vmem();
+    __syncthreads();
+    int ybuf = 0;
+    while (ra < ch_end) {
+        int issued = 0;   // this wave's copies for step i + 2
+        if (rc < ch_end) {
+            issued += copy_y(ybuf == 0 ? 2 : ybuf - 1, rc);
+            if (follows(ra, rb) && follows(rb, rc)) issued += new_row(rc);
+        }
+        compute(ybuf, ra - (int)fdiv((uint32_t)ra, p.div_p) * p.P);
+        wait_vmem_upto(issued);
+        __syncthreads();
+        if (rb < ch_end && !follows(ra, rb)) {
+            // step i + 1 starts a new window
+            all_rows(rb);
+            if (rc < ch_end && follows(rb, rc)) new_row(rc);
+            wait_vmem();
+            __syncthreads();
+        }
+        ybuf = ybuf == 2 ? 0 : ybuf + 1;
+        ra = rb;
+        rb = rc;
+        rc = rc < ch_end ? next_live(rc + 1) : ch_end;
+    }
+
+    if (tid == 0) {
+        p.skip_slots[blockIdx.x] = skipped;
+        p.work_slots[t] = ch_end - ch_begin - skipped;
+    }
+
+    // Partial [qt * nsplit + z][K][RS][C]: lane holds columns 4 (lane/16) .. +3
+    // of column block j (4 channels of one tap) for output channel
+    // k0 + 32 wk + 16 i + lane%16.
+    const uint32_t part_bytes = (uint32_t)p.K * RS * p.C * 4u;
+    const __amdgpu_buffer_rsrc_t rs_out =
+        make_rsrc(p.out + (int64_t)(qt * p.nsplit + z) * p.K * RS * p.C, part_bytes);
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        if (j < nbw) {   // uniform
+            const int b = cb0 + j, tap = b >> 2;
+            const int c = c0 + (b & 3) * 16 + 4 * (lane >> 4);
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int k = k0 + wk * 32 + i * 16 + (lane & 15);
+                const uint32_t off = (uint32_t)((k * RS + tap) * p.C + c) * 4u;
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[j][i]), rs_out, off, 0, 0);
+            }
+        }
+    }
+}
+
 }  // namespace
 
 int weight_tile_channels() { return BM; }
@@ -700,6 +1021,19 @@ int weight_chunk(int dtype) { return CH * (dtype == 1 ? 8 : 4); }
 hipError_t launch_bwd_weight(int dtype, const WeightParams& p, hipStream_t stream, const ProfEvents& ev)
 {
     const int nb = p.tgroups * p.ctiles * p.ktiles * p.nsplit;
+    if (p.rows) {
+        if (dtype != 1 || p.R > 3 || p.S > 3 || p.bk != 64 || p.cg != 64) return hipErrorInvalidValue;
+        switch (p.R * p.S) {
+        case 1: hipExtLaunchKernelGGL(bwd_weight_rows_kernel<1>, dim3(nb), dim3(RW_NT), 0, stream, ev.start, ev.stop, 0, p); break;
+        case 2: hipExtLaunchKernelGGL(bwd_weight_rows_kernel<2>, dim3(nb), dim3(RW_NT), 0, stream, ev.start, ev.stop, 0, p); break;
+        case 3: hipExtLaunchKernelGGL(bwd_weight_rows_kernel<3>, dim3(nb), dim3(RW_NT), 0, stream, ev.start, ev.stop, 0, p); break;
+        case 4: hipExtLaunchKernelGGL(bwd_weight_rows_kernel<4>, dim3(nb), dim3(RW_NT), 0, stream, ev.start, ev.stop, 0, p); break;
+        case 6: hipExtLaunchKernelGGL(bwd_weight_rows_kernel<6>, dim3(nb), dim3(RW_NT), 0, stream, ev.start, ev.stop, 0, p); break;
+        case 9: hipExtLaunchKernelGGL(bwd_weight_rows_kernel<9>, dim3(nb), dim3(RW_NT), 0, stream, ev.start, ev.stop, 0, p); break;
+        default: return hipErrorInvalidValue;
+        }
+        return hipGetLastError();
+    }
     const dim3 grid(nb), block(dtype != 1 ? NT : p.bk == 64 ? WTile<64>::NT : WTile<256>::NT);
     if (dtype == 1) {
         if (p.bk == 64) hipExtLaunchKernelGGL(bwd_weight_tr_kernel<64>, grid, block, 0, stream, ev.start, ev.stop, 0, p);

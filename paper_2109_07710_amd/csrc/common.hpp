@@ -144,6 +144,21 @@ __device__ __forceinline__ void buf_load16_lds(const u32x4_t& rsrc, uint32_t off
 
 // Wait until all of this wave's vector memory operations have completed.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+// Wait until at most n (0..7) of this wave's vector memory operations are
+// outstanding: the oldest ones (copies complete in issue order) have landed.
+__device__ __forceinline__ void wait_vmem_upto(int n)
+{
+    switch (n) {
+    case 0: __builtin_amdgcn_s_waitcnt(0x0f70); break;
+    case 1: __builtin_amdgcn_s_waitcnt(0x0f71); break;
+    case 2: __builtin_amdgcn_s_waitcnt(0x0f72); break;
+    case 3: __builtin_amdgcn_s_waitcnt(0x0f73); break;
+    case 4: __builtin_amdgcn_s_waitcnt(0x0f74); break;
+    case 5: __builtin_amdgcn_s_waitcnt(0x0f75); break;
+    case 6: __builtin_amdgcn_s_waitcnt(0x0f76); break;
+    default: __builtin_amdgcn_s_waitcnt(0x0f77); break;
+    }
+}
 // vmcnt(0) and lgkmcnt(0): this wave's copies have landed and its LDS reads are done.
 __device__ __forceinline__ void wait_vmem_lds() { __builtin_amdgcn_s_waitcnt(0x0070); }
 

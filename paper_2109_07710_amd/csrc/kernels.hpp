@@ -66,6 +66,7 @@ struct WeightParams {
     int bk;                  // output channels per tile (64, 128, 256)
     int tpg, tgroups;        // filter taps per 256-column channel tile, and tap groups
     int cg;                  // channel columns per packed tap (C when packed, else 256)
+    int rows;                // row-window kernel: chunks are output rows, tgroups are 128-column segments
     int mode_flags;
     uint32_t x_bytes, dy_bytes;
     FastDiv div_q, div_p;    // pixel -> (n, p, q)

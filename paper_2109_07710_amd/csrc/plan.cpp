@@ -150,19 +150,38 @@ int weight_taps_per_group(const cbw_conv_desc* d)
     return (rs + groups - 1) / groups;
 }
 
-int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
+bool weight_rows_eligible(const cbw_conv_desc* d)
+{
+    return d->dtype == CBW_BF16 && d->stride_h == 1 && d->stride_w == 1 && d->R <= 3 && d->S <= 3 &&
+           d->C % 64 == 0 && d->K % 64 == 0 && d->C <= 128 && d->K <= 128;
+}
+
+int plan_weight(const cbw_conv_desc* d, WeightPlan* out, bool allow_rows)
 {
     int st = validate_desc(d);
     if (st != CBW_OK) return st;
     WeightPlan p;
     p.npq = (int64_t)d->N * d->P * d->Q;
-    const int chunk = weight_chunk_px(d->dtype);
-    p.nchunks = (int)((p.npq + chunk - 1) / chunk);
-    p.bk = weight_tile_k_for(d);
-    p.tpg = weight_taps_per_group(d);
-    p.cg = p.tpg > 1 ? d->C : kWeightTileC;
-    p.tgroups = (d->R * d->S + p.tpg - 1) / p.tpg;
-    p.ctiles = p.tpg > 1 ? 1 : (d->C + kWeightTileC - 1) / kWeightTileC;
+    p.rows = allow_rows && weight_rows_eligible(d);
+    if (p.rows) {
+        // row-window kernel: 64 x 64 (k, c) tiles, output rows in segments
+        // of up to 128 columns; the skip chunks are whole output rows
+        p.chunk = d->Q;
+        p.nchunks = d->N * d->P;
+        p.bk = 64;
+        p.tpg = 1;
+        p.cg = 64;
+        p.tgroups = (d->Q + kRowSegment - 1) / kRowSegment;
+        p.ctiles = d->C / 64;
+    } else {
+        p.chunk = weight_chunk_px(d->dtype);
+        p.nchunks = (int)((p.npq + p.chunk - 1) / p.chunk);
+        p.bk = weight_tile_k_for(d);
+        p.tpg = weight_taps_per_group(d);
+        p.cg = p.tpg > 1 ? d->C : kWeightTileC;
+        p.tgroups = (d->R * d->S + p.tpg - 1) / p.tpg;
+        p.ctiles = p.tpg > 1 ? 1 : (d->C + kWeightTileC - 1) / kWeightTileC;
+    }
     p.ktiles = (d->K + p.bk - 1) / p.bk;
     const int tiles = p.tgroups * p.ctiles * p.ktiles;
     // as many splits as fit in one round of resident workgroups
@@ -174,7 +193,10 @@ int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
     p.chunks_per_split = (p.nchunks + nsplit - 1) / nsplit;
     p.nsplit = (p.nchunks + p.chunks_per_split - 1) / p.chunks_per_split;
     p.grid = tiles * p.nsplit;
-    p.direct = (p.nsplit == 1 && d->w_layout == CBW_KRSC);
+    // partial weight gradients to sum: one per split (and per column segment
+    // for the row-window kernel)
+    p.nparts = p.rows ? p.nsplit * p.tgroups : p.nsplit;
+    p.direct = (p.nparts == 1 && d->w_layout == CBW_KRSC);
     size_t cur = 0;
     p.header = take(&cur, 256);
     p.occ = take(&cur, (size_t)p.nchunks * p.ktiles);
@@ -182,7 +204,7 @@ int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
     p.xbits = take(&cur, ((size_t)d->N * d->H * d->W * d->C + 31) / 32 * 4);
     p.skip_slots = take(&cur, (size_t)p.grid * 4);
     p.work_slots = take(&cur, (size_t)p.grid * 4);
-    if (!p.direct) p.partials = take(&cur, (size_t)p.nsplit * d->K * d->R * d->S * d->C * 4);
+    if (!p.direct) p.partials = take(&cur, (size_t)p.nparts * d->K * d->R * d->S * d->C * 4);
     if (d->act_layout == CBW_NCHW) {
         p.t_x = take(&cur, (size_t)d->N * d->H * d->W * d->C * elem_bytes(d->dtype));
         p.t_dy = take(&cur, (size_t)p.npq * d->K * elem_bytes(d->dtype));
@@ -190,6 +212,20 @@ int plan_weight(const cbw_conv_desc* d, WeightPlan* out)
     }
     p.total = cur;
     *out = p;
+    return CBW_OK;
+}
+
+}  // namespace cbw
+
+namespace cbw {
+
+int weight_ws_bytes(const cbw_conv_desc* d, size_t* bytes)
+{
+    WeightPlan a, b;
+    int st = plan_weight(d, &a, true);
+    if (st != CBW_OK) return st;
+    if ((st = plan_weight(d, &b, false)) != CBW_OK) return st;
+    *bytes = a.total > b.total ? a.total : b.total;
     return CBW_OK;
 }
 

@@ -14,6 +14,7 @@ namespace cbw {
 constexpr int kWeightTileC = CBW_DW_BM; // channels c per weight-gradient tile
 constexpr int kWeightTileK = CBW_DW_BN; // output channels k per weight-gradient tile
 constexpr int kCompactBlock = 256;      // pixels per compaction block
+constexpr int kRowSegment = 128;        // output columns per segment of the row-window weight gradient
 // Resident weight-gradient workgroups the split-K factor aims to fill exactly.
 constexpr int kWeightSlots = CBW_NUM_CUS * CBW_DW_OCC;
 
@@ -64,10 +65,13 @@ int weight_tile_k_for(const cbw_conv_desc* d);
 int weight_taps_per_group(const cbw_conv_desc* d);
 
 struct WeightPlan {
+    bool rows = false;      // row-window kernel (narrow stride-1 layers): chunks are output rows
+    int chunk = 0;          // pixels per occupancy chunk (64, or Q for the row-window kernel)
     int64_t npq = 0;
     int bk = 0, tpg = 1, tgroups = 0;   // output-channel tile width, taps per group, tap groups
     int cg = 0;                         // channel columns per packed tap (C, or 256 without packing)
     int nchunks = 0, ctiles = 0, ktiles = 0, nsplit = 0, chunks_per_split = 0, grid = 0;
+    int nparts = 0;         // partials the reduction sums
     bool direct = false;  // partial of the single split is dW itself
     Region header, occ, xlive, xbits, skip_slots, work_slots, partials;
     // NCHW callers: NHWC copies of X and dY and the NHWC-order dY footprint
@@ -84,7 +88,13 @@ int require_nhwc(const cbw_conv_desc* d);
 // no_split: the reduction is never split (no partial-tile region; the
 // kernels get a split bound of 1), for callers with a bounded scratch.
 int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out, bool no_split = false);
-int plan_weight(const cbw_conv_desc* d, WeightPlan* out);
+// allow_rows: narrow stride-1 layers (C and K multiples of 64, at most 128,
+// filters of at most 3 x 3, bf16) get the row-window kernel; callers that
+// need the chunked kernel (X-block skipping) pass false.
+int plan_weight(const cbw_conv_desc* d, WeightPlan* out, bool allow_rows = true);
+bool weight_rows_eligible(const cbw_conv_desc* d);
+// Workspace bytes of the weight gradient: enough for either kernel.
+int weight_ws_bytes(const cbw_conv_desc* d, size_t* bytes);
 // The forward convolution as a data-gradient GEMM: for stride 1, Y = conv(X, W)
 // is the backward-data operation with the roles of C and K, of (H, W) and
 // (P, Q) interchanged, the filter taps flipped and padding R-1-pad.  Writes that
