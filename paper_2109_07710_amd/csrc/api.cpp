@@ -99,6 +99,7 @@ void data_gemm_params(const cbw_conv_desc* desc, const DataPlan& plan, const voi
     if (gather) {
         cp.mask = x_mask;
         cp.blk_counts = at<int32_t>(ws, plan.blk_counts);
+        cp.dead_flags = at<int32_t>(ws, plan.dead_flags);
         cp.dx = dX;
         cp.npix = (int)plan.npix;
         cp.C = desc->C;
@@ -110,6 +111,7 @@ void data_gemm_params(const cbw_conv_desc* desc, const DataPlan& plan, const voi
         p.nblk = plan.nblk;
         p.lists = at<int32_t>(ws, plan.lists);
         p.counts = at<int32_t>(ws, plan.counts);
+        p.dead_flags = cp.dead_flags;
     }
     *out = p;
     *cpo = cp;

@@ -255,9 +255,8 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     // Gather mode speculates: it first takes the dense mode's tiles, which
     // are exactly its own when every pixel of every group is live (the usual
     // case for element-wise footprints), and issues their first copies at
-    // once.  The groups' live totals, summed from the preparation launch's
-    // block counts while those copies fly, confirm it; otherwise the copies
-    // are dropped and the tiles are rebuilt over the live lists.
+    // once; when the preparation launch flagged a dead pixel, the copies are
+    // dropped and the tiles are rebuilt over the live lists.
     const int kchunks = (p.K + (CH * Elem<T>::E) - 1) / (CH * Elem<T>::E);
     const int nsteps = p.R * p.S * kchunks;
     constexpr int GG = MODE == MODE_GATHER ? kGatherMaxGroups : 1;
@@ -492,13 +491,21 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
         if (mask_lds) fetch_mask();
     };
 
+    // Gather mode: whether some group has a dead pixel, a flag per group that
+    // the preparation launch raised (the reduction launch lowers it again):
+    // scalar loads issued before the first copies, complete by the time the
+    // copies have landed, so the usual case (every pixel live) pays nothing.
+    int anydead = 0;
+    if (MODE == MODE_GATHER)
+        for (int g = 0; g < p.ctiles; ++g) anydead |= p.dead_flags[g];
     map_item(true);
     if (active) start_item();
-    bool published = false;   // step 0's copies have landed and a barrier has published them
-    if (MODE == MODE_GATHER) {
-        // every group's live-pixel total; the block counts' loads complete
-        // with the copies above, and the barrier that publishes those copies
-        // also publishes the per-wave sums
+    wait_vmem();
+    __syncthreads();
+    if (MODE == MODE_GATHER && anydead != 0) {
+        // speculation failed (the copies have landed): every group's live
+        // total from the block counts (workgroup 0 also stores them for the
+        // reduction kernel and the readers), then the tiles over the live lists
         for (int g = 0; g < p.ctiles; ++g) {
             const int32_t* bc = p.blk_counts + (int64_t)g * p.nblk;
             int v = 0;
@@ -512,33 +519,23 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
             v = wave_sum(v);
             if (lane == 0) gsum_s[g * NW + wave] = v;
         }
-        wait_vmem();
         __syncthreads();
-        bool all_live = true;
-        for (int g = 0; g < p.ctiles; ++g) {
+        if (tid < p.ctiles) {
             int tot = 0;
 #pragma unroll
-            for (int w = 0; w < NW; ++w) tot += gsum_s[g * NW + w];
-            all_live &= tot == p.npix;
-            if (tid == 0) gtot_s[g] = tot;
-            // workgroup 0 also stores them for the reduction kernel and the readers
-            if (blockIdx.x == 0 && tid == 0) p.counts[g] = tot;
+            for (int w = 0; w < NW; ++w) tot += gsum_s[tid * NW + w];
+            gtot_s[tid] = tot;
+            if (blockIdx.x == 0) p.counts[tid] = tot;
         }
-        if (!all_live) {
-            // speculation failed: the copies have landed; start over on the
-            // live lists
-            __syncthreads();   // gtot_s
-            map_item(false);
-            if (active) start_item();
-        } else {
-            published = true;
-        }
-    }
-    if (!active) return;   // uniform across the workgroup
-    if (!published) {
+        __syncthreads();
+        map_item(false);
+        if (active) start_item();
         wait_vmem();
         __syncthreads();
+    } else if (MODE == MODE_GATHER && blockIdx.x == 0 && tid < p.ctiles) {
+        p.counts[tid] = p.npix;   // every pixel live
     }
+    if (!active) return;   // uniform across the workgroup
     auto main_loop = [&](auto nb_tag) {
         for (int step = 0; step < nloc; ++step) {
             const int buf = step & 1;
@@ -815,6 +812,8 @@ __device__ __forceinline__ void data_reduce_block(const DataParams& p, int block
     constexpr int E = Elem<T>::E;
     const int kchunks = (p.K + CH * E - 1) / (CH * E);
     const int nsteps = p.R * p.S * kchunks;
+    // the GEMM has read the dead-pixel flags: lower them for the next call
+    if (MODE == MODE_GATHER && block == 0 && (int)threadIdx.x < p.ctiles) p.dead_flags[threadIdx.x] = 0;
     int ntiles, nsplit;
     bool dense_map = MODE != MODE_GATHER;   // gather mode with every pixel live tiles like the dense mode
     if (MODE == MODE_GATHER) {

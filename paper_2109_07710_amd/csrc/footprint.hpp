@@ -77,7 +77,10 @@ __device__ __forceinline__ void compact_count_block(const CompactParams& p, int 
         ndead += wd[w];
         nlive += wc[w];
     }
-    if (tid == 0) p.blk_counts[(int64_t)g * p.nblk + blk] = nlive;
+    if (tid == 0) {
+        p.blk_counts[(int64_t)g * p.nblk + blk] = nlive;
+        if (nlive < min(T, p.npix - blk * T)) p.dead_flags[g] = 1;   // every writer stores 1
+    }
     if (ndead == 0) return;   // uniform
     // dead pixels listed, then their rows cleared by the whole block:
     // consecutive threads write consecutive 16-byte pieces of one row, so a

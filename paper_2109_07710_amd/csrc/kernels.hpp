@@ -25,6 +25,8 @@ struct DataParams {
     int32_t* lists;          // [groups][npix] live pixels, ascending (written by the tiles of
                              // groups with dead pixels; a fully live group's list is 0, 1, 2, ...)
     int32_t* counts;         // [groups] live-pixel counts (written by workgroup 0)
+    int32_t* dead_flags;     // [groups] 1 when the group has a dead pixel (raised by the
+                             // preparation launch, lowered by the reduction launch)
     int N, H, W, C, K, R, S, P, Q;
     int stride_h, stride_w, pad_h, pad_w;
     int npix;                // N*H*W
@@ -44,6 +46,7 @@ struct DataParams {
 struct CompactParams {
     const uint32_t* mask;    // packed footprint, NHWC bit order
     int32_t* blk_counts;     // [groups][nblk] live pixels per 256-pixel block
+    int32_t* dead_flags;     // [groups] set to 1 by a block with a dead pixel
     void* dx;                // zero-filled at (pixel, group) rows dead for the whole group
     int npix, C, G, groups, nblk, elem_bytes;
 };

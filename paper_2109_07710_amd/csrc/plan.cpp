@@ -96,6 +96,7 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out, bool no_split)
     if (masked) {
         p.blk_counts = take(&cur, (size_t)p.groups * p.nblk * 4);
         p.counts = take(&cur, (size_t)p.groups * 4);
+        p.dead_flags = take(&cur, (size_t)p.groups * 4);
         p.lists = take(&cur, (size_t)p.groups * p.npix * 4);
     }
     // Split partial tiles.  Without skipping the host knows the split; with

@@ -36,7 +36,7 @@ struct DataPlan {
     int brows = 0;          // dense / select: pixel rows per tile (data_rows_pick)
     int maxtiles = 0;       // most tiles any row choice can give (the gather mode's grid)
     int split = 1;          // dense / select: host-chosen reduction split
-    Region header, wt, blk_counts, counts, lists, partial;
+    Region header, wt, blk_counts, counts, dead_flags, lists, partial;
     // NCHW callers: NHWC copies of dY and dX and the NHWC-order footprint,
     // after every other region (the other offsets do not depend on layout)
     Region t_dy, t_dx, t_mask;

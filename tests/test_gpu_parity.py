@@ -160,6 +160,43 @@ def test_run_twice_bitwise_deterministic():
     assert torch.equal(a["dw"].view(torch.int32), b["dw"].view(torch.int32))
 
 
+def test_gather_sequence_shared_workspace():
+    """One workspace over calls whose footprints alternate between every
+    pixel live and some pixels dead, starting from a zeroed and from a
+    0xff-filled workspace: each call's data gradient equals the dense
+    kernel's bits at live outputs and zero elsewhere, whatever the previous
+    call left behind (the per-group dead-pixel flags it raised or lowered)."""
+    spec = wl.config4(0.3, "clustered", N=2, H=14)[0]
+    _case("gather sequence " + spec.name)
+    t = wl.draw(spec)
+    desc = desc_of(spec)
+    d = to_dev(t)
+    x_live = d["x"].abs() + 0.125   # every element positive: every pixel live
+    dx_ref = torch.empty_like(d["x"])
+    cb.conv_bwd_data(desc, d["dy"], d["w"], dx_ref, cb.workspace(desc, cb.CBW_OP_BWD_DATA, "cuda"))
+    ref_bits = dx_bits_nchw(dx_ref)
+    dw = torch.empty((spec.K, spec.R, spec.S, spec.C), dtype=torch.float32, device="cuda")
+    for fill in (0, 255):
+        ws = cb.workspace(desc, cb.CBW_OP_BWD_DATA_MASKED, "cuda")
+        ws_b = cb.workspace(desc, cb.CBW_OP_BWD_BOTH, "cuda")
+        ws.fill_(fill)
+        ws_b.fill_(fill)
+        for i, x in enumerate((x_live, d["x"], x_live, d["x"], d["x"], x_live)):
+            xm = torch.zeros(max(cb.cbw_mask_words(desc), 1), dtype=torch.int32, device="cuda")
+            cb.cbw_relu_mask_pack(desc, x, xm)
+            mask = oracle.relu_mask(oracle.nhwc_to_nchw(x.float().cpu().numpy()))
+            for both in (False, True):
+                dx = torch.full_like(d["x"], float("nan"))
+                if both:
+                    cb.conv_bwd_sparse(desc, x, d["dy"], d["w"], xm, None, dx, dw, ws_b, 0)
+                else:
+                    cb.conv_bwd_data_masked(desc, d["dy"], d["w"], xm, dx, ws, 0)
+                torch.cuda.synchronize()
+                bits = dx_bits_nchw(dx)
+                assert np.array_equal(bits[mask], ref_bits[mask]), (fill, i, both)
+                assert np.all(bits[~mask] == 0), (fill, i, both)
+
+
 def test_relu_mask_pack_exact():
     _case("mask pack special values")
     vals = [0.0, -0.0, 1.0, -1.0, float("nan"), float("inf"), -float("inf"), 1e-40, -1e-40, 3e-38]
