@@ -45,6 +45,7 @@ bool tiles_consistent()
     if (data_split(1, 1 << 20, kDataSlots, kDataMaxSplit) != host_data_split(1, 1 << 20)) return false;
     for (int t = 0; t < kDataTileCount; ++t)
         if (data_tile_channels(t) != kDataTiles[t].bm || data_tile_pixels(t) != kDataTiles[t].bn) return false;
+    if (data_rows_segment() != kDataRowSegment) return false;
     return weight_tile_channels() == kWeightTileC && weight_tile_k() == kWeightTileK &&
            compact_block_pixels() == kCompactBlock && weight_chunk(CBW_BF16) == weight_chunk_px(CBW_BF16) &&
            weight_chunk(CBW_F32) == weight_chunk_px(CBW_F32);
@@ -115,6 +116,31 @@ void data_gemm_params(const cbw_conv_desc* desc, const DataPlan& plan, const voi
     }
     *out = p;
     *cpo = cp;
+}
+
+// Kernel parameters of the row-window data gradient (NHWC tensors).
+DataRowsParams data_rows_params(const cbw_conv_desc* d, const DataPlan& plan, const void* dY, const void* wt,
+                                const uint32_t* x_mask, void* dX, void* ws, bool skip)
+{
+    DataRowsParams p{};
+    p.dy = dY;
+    p.wt = wt;
+    p.dx = dX;
+    p.mask = x_mask;
+    p.row_counts = at<int32_t>(ws, plan.row_counts);
+    p.N = d->N; p.H = d->H; p.W = d->W; p.P = d->P; p.Q = d->Q;
+    p.pad_h = d->pad_h; p.pad_w = d->pad_w;
+    p.nseg = plan.rows_nseg;
+    p.rows_per_strip = plan.rows_per_strip;
+    p.nrows = d->N * d->H;
+    p.skip = x_mask && skip ? 1 : 0;
+    const int64_t esz = elem_bytes(d->dtype);
+    p.dy_bytes = (uint32_t)((int64_t)d->N * d->P * d->Q * d->K * esz);
+    p.dx_bytes = (uint32_t)(plan.npix * d->C * esz);
+    p.mask_bytes = (uint32_t)((plan.npix * d->C + 31) / 32 * 4);
+    p.wt_bytes = (uint32_t)((int64_t)d->R * d->S * d->C * d->K * esz);
+    p.div_h = make_fastdiv((uint32_t)d->H);
+    return p;
 }
 
 // compaction needs at most kGatherMaxGroups channel groups; wider layers
@@ -192,13 +218,23 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
     }
     int* header = at<int>(ws, plan.header);
     void* wt = at<void>(ws, plan.wt);
-    DataParams p;
-    CompactParams cp;
-    data_gemm_params(desc, plan, dY, wt, x_mask, dX, ws, gather, no_split, &p, &cp);
-    e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S, desc->w_layout == CBW_KRSC,
-                         header, mode, gather ? &cp : nullptr, s);
-    if (e != hipSuccess) return hip_status(e);
-    if ((e = launch_bwd_data(desc->dtype, mode, p, s, prof_events(0))) != hipSuccess) return hip_status(e);
+    if (plan.rows) {
+        e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S, desc->w_layout == CBW_KRSC,
+                             header, MODE_ROWS, nullptr, s);
+        if (e != hipSuccess) return hip_status(e);
+        const DataRowsParams rp = data_rows_params(desc, plan, dY, wt, masked ? x_mask : nullptr, dX, ws,
+                                                   !(flags & CBW_FLAG_NO_SKIP));
+        if ((e = launch_bwd_data_rows(rp, plan.rows_grid, plan.rows_nbw, s, prof_events(0))) != hipSuccess)
+            return hip_status(e);
+    } else {
+        DataParams p;
+        CompactParams cp;
+        data_gemm_params(desc, plan, dY, wt, x_mask, dX, ws, gather, no_split, &p, &cp);
+        e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S, desc->w_layout == CBW_KRSC,
+                             header, mode, gather ? &cp : nullptr, s);
+        if (e != hipSuccess) return hip_status(e);
+        if ((e = launch_bwd_data(desc->dtype, mode, p, s, prof_events(0))) != hipSuccess) return hip_status(e);
+    }
     if (dX != dX_out)
         e = launch_transpose(desc->dtype, dX, dX_out, desc->N, desc->H * desc->W, desc->C, s);
     return hip_status(e);
@@ -211,7 +247,7 @@ int run_fwd(const cbw_conv_desc* desc, const void* X, const void* W, void* Y, ui
     int st = fwd_as_data_desc(desc, &vd);
     if (st != CBW_OK) return st;
     DataPlan plan;
-    if ((st = plan_data(&vd, false, &plan)) != CBW_OK) return st;
+    if ((st = plan_data(&vd, false, &plan, false, false)) != CBW_OK) return st;
     if (!X || !W || !Y) return CBW_ERR_INVALID_ARG;
     if (!aligned16(X) || !aligned16(W) || !aligned16(Y) || (y_mask && !aligned16(y_mask)))
         return CBW_ERR_UNSUPPORTED;
@@ -326,7 +362,7 @@ static size_t elementwise_ws(const cbw_conv_desc* d)
 int cbw_data_tiling(const cbw_conv_desc* desc, int32_t* channels, int32_t* capacity, int32_t* rows)
 {
     DataPlan p;
-    const int st = plan_data(desc, false, &p);
+    const int st = plan_data(desc, false, &p, false, false);
     if (st != CBW_OK) return st;
     if (channels) *channels = p.bm;
     if (capacity) *capacity = p.bn;
@@ -359,7 +395,7 @@ int cbw_workspace_size(const cbw_conv_desc* desc, int op, size_t* bytes)
         cbw_conv_desc vd;
         DataPlan p;
         if ((st = fwd_as_data_desc(desc, &vd)) != CBW_OK) return st;
-        if ((st = plan_data(&vd, false, &p)) != CBW_OK) return st;
+        if ((st = plan_data(&vd, false, &p, false, false)) != CBW_OK) return st;
         *bytes = p.total;
         return CBW_OK;
     }
@@ -594,20 +630,26 @@ static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY
                           flags & CBW_FLAG_NO_SKIP, stream);
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const bool gather = data_gathers(dplan, masked, flags);
-    const int mode = !masked ? MODE_DENSE : (gather ? MODE_GATHER : MODE_SELECT);
+    const bool gather = !dplan.rows && data_gathers(dplan, masked, flags);
+    const int mode = dplan.rows ? MODE_ROWS : !masked ? MODE_DENSE : (gather ? MODE_GATHER : MODE_SELECT);
     int* header = at<int>(ws, dplan.header);
     void* wt = at<void>(ws, dplan.wt);
-    DataParams dp;
+    DataParams dp{};
     CompactParams cp;
-    data_gemm_params(desc, dplan, dY, wt, x_mask, dX, ws, gather, false, &dp, &cp);
+    if (!dplan.rows) data_gemm_params(desc, dplan, dY, wt, x_mask, dX, ws, gather, false, &dp, &cp);
     OccParams op{};
     if (skip) op = weight_occ_params(desc, wplan, dY, dy_mask, x_skip, x_mask, wws);
     hipError_t e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S,
                                     desc->w_layout == CBW_KRSC, header, mode, gather ? &cp : nullptr, s,
                                     skip ? &op : nullptr);
     if (e != hipSuccess) return hip_status(e);
-    if ((e = launch_bwd_data(desc->dtype, mode, dp, s, prof_events(0), false)) != hipSuccess) return hip_status(e);
+    if (dplan.rows) {
+        const DataRowsParams rp = data_rows_params(desc, dplan, dY, wt, x_mask, dX, ws, skip);
+        e = launch_bwd_data_rows(rp, dplan.rows_grid, dplan.rows_nbw, s, prof_events(0));
+    } else {
+        e = launch_bwd_data(desc->dtype, mode, dp, s, prof_events(0), false);
+    }
+    if (e != hipSuccess) return hip_status(e);
     const WeightParams wp = weight_gemm_params(desc, wplan, X, dY, dW, wws, skip, x_skip,
                                                flags & CBW_FLAG_NO_SKIP);
     if ((e = launch_bwd_weight(desc->dtype, wp, s, prof_events(1))) != hipSuccess) return hip_status(e);
@@ -624,7 +666,7 @@ static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY
         rp.G = splitk_reduce_group(wplan.nparts, n4);
         rp.blocks = (int)((n4 * rp.G + 255) / 256);
     }
-    const bool dx_reduce = mode == MODE_GATHER || dplan.split > 1;
+    const bool dx_reduce = !dplan.rows && (mode == MODE_GATHER || dplan.split > 1);
     return hip_status(launch_bwd_reduce(desc->dtype, mode, dp, dx_reduce, rp, s));
 }
 
@@ -750,7 +792,20 @@ int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, siz
         if (e != hipSuccess) return hip_status(e);
         r.rows_total = (int64_t)plan.groups * plan.npix;
         r.rows_live = r.rows_total;
-        if (op == CBW_OP_BWD_DATA_MASKED && header == MODE_GATHER) {
+        if (plan.rows && header == MODE_ROWS) {
+            // pixels of the rows each workgroup computed (dead rows skipped)
+            int32_t buf[256];
+            int64_t live = 0;
+            const int32_t* slots = at<int32_t>(const_cast<void*>(workspace), plan.row_counts);
+            for (int i0 = 0; i0 < plan.rows_grid; i0 += 256) {
+                const int n = plan.rows_grid - i0 < 256 ? plan.rows_grid - i0 : 256;
+                e = hipMemcpyAsync(buf, slots + i0, n * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+                if (e == hipSuccess) e = hipStreamSynchronize(s);
+                if (e != hipSuccess) return hip_status(e);
+                for (int i = 0; i < n; ++i) live += buf[i];
+            }
+            r.rows_live = live * plan.groups;
+        } else if (op == CBW_OP_BWD_DATA_MASKED && header == MODE_GATHER) {
             int32_t counts[64];
             int64_t live = 0;
             for (int g0 = 0; g0 < plan.groups; g0 += 64) {
@@ -808,6 +863,7 @@ int cbw_read_live_lists(const cbw_conv_desc* desc, const void* workspace, size_t
     if (workspace_bytes < plan.total) return CBW_ERR_WORKSPACE;
     hipStream_t s = static_cast<hipStream_t>(stream);
     void* ws = const_cast<void*>(workspace);
+    if (plan.rows) return CBW_ERR_UNSUPPORTED;   // the row-window kernel lists nothing
     int32_t n = 0;
     hipError_t e = hipMemcpyAsync(&n, at<int32_t>(ws, plan.counts) + group, sizeof(int32_t),
                                   hipMemcpyDeviceToHost, s);

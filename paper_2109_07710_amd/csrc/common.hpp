@@ -142,6 +142,21 @@ __device__ __forceinline__ void buf_load16_lds(const u32x4_t& rsrc, uint32_t off
         : "v"(off), "s"(rsrc), "s"(lds_base));
 }
 
+// The same for 4 bytes per lane: lane l's word lands at lds_base + 4*l.
+__device__ __forceinline__ void buf_load4_lds(const u32x4_t& rsrc, uint32_t off, uint32_t lds_base)
+{
+    lds_base = __builtin_amdgcn_readfirstlane(lds_base);  // wave-uniform by contract
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dword %1, %2, 0 offen lds\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(off), "s"(rsrc), "s"(lds_base));
+}
+
 // Wait until all of this wave's vector memory operations have completed.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 // Wait until at most n (0..7) of this wave's vector memory operations are

@@ -12,6 +12,15 @@ namespace cbw {
 // convolution (flipped filters, padding R-1-pad, stride 1) with a ReLU
 // epilogue that also emits the output's footprint bits.
 enum { MODE_DENSE = 0, MODE_SELECT = 1, MODE_GATHER = 2, MODE_FWD = 3 };
+// Workspace header stamp of a data-gradient call served by the row-window
+// kernel (bwd_data_rows.hip) instead of the tiled GEMM.
+constexpr int MODE_ROWS = 4;
+
+// Optional timing events attached to the dispatch of a GEMM kernel (both
+// may be null): they record the kernel's own begin and end.
+struct ProfEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
 
 struct DataParams {
     const void* dy;          // [N*P*Q][K]
@@ -42,6 +51,23 @@ struct DataParams {
     int tile;                // kDataTiles entry the plan chose
     FastDiv div_w, div_h;    // pixel -> (n, h, w)
 };
+
+// Row-window data gradient (3 x 3, stride 1, C = K = 64, bf16, NHWC): a
+// workgroup per (column segment, strip of rows_per_strip output rows).
+struct DataRowsParams {
+    const void* dy;          // [N*P*Q][64]
+    const void* wt;          // [9][64][64]: filters by tap, input channel c, then k
+    void* dx;                // [N*H*W][64]
+    const uint32_t* mask;    // packed footprint of X, or null (dense)
+    int32_t* row_counts;     // [grid] pixels of the rows each workgroup computed
+    int N, H, W, P, Q, pad_h, pad_w;
+    int nseg, rows_per_strip, nrows;   // nrows = N*H
+    int skip;                // masked: rows whose footprint is empty skip the matrix work
+    uint32_t dy_bytes, dx_bytes, mask_bytes, wt_bytes;
+    FastDiv div_h;           // output row -> image
+};
+int data_rows_segment();
+hipError_t launch_bwd_data_rows(const DataRowsParams& p, int grid, int nbw, hipStream_t stream, const ProfEvents& ev);
 
 struct CompactParams {
     const uint32_t* mask;    // packed footprint, NHWC bit order
@@ -118,11 +144,6 @@ int compact_block_pixels();
 // occupancy) in one launch.
 hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, int RS, int krsc, int* header,
                             int mode, const CompactParams* cp, hipStream_t stream, const OccParams* op = nullptr);
-// Optional timing events attached to the dispatch of a GEMM kernel (both
-// may be null): they record the kernel's own begin and end.
-struct ProfEvents {
-    hipEvent_t start = nullptr, stop = nullptr;
-};
 // with_reduce = false leaves a split reduction to launch_bwd_reduce.
 hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream, const ProfEvents& ev,
                            bool with_reduce = true);

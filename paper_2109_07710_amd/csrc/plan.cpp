@@ -68,11 +68,47 @@ int data_tile_index(int C)
     return best;
 }
 
-int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out, bool no_split)
+bool data_rows_eligible(const cbw_conv_desc* d)
+{
+    return d->dtype == CBW_BF16 && d->R == 3 && d->S == 3 && d->stride_h == 1 && d->stride_w == 1 && d->C == 64 &&
+           d->K == 64;
+}
+
+int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out, bool no_split, bool allow_rows)
 {
     int st = validate_desc(d);
     if (st != CBW_OK) return st;
     DataPlan p;
+    if (allow_rows && data_rows_eligible(d)) {
+        // one workgroup per CU: strips of consecutive output rows, as many
+        // as make the segments times the strips fill the CUs once
+        p.tile = data_tile_index(d->C);
+        p.bm = kDataTiles[p.tile].bm;
+        p.bn = kDataTiles[p.tile].bn;
+        p.npix = (int64_t)d->N * d->H * d->W;
+        p.groups = (d->C + p.bm - 1) / p.bm;
+        p.rows = true;
+        p.rows_nseg = (d->W + kDataRowSegment - 1) / kDataRowSegment;
+        const int nrows = d->N * d->H;
+        int strips = CBW_NUM_CUS / p.rows_nseg;
+        if (strips < 1) strips = 1;
+        p.rows_per_strip = (nrows + strips - 1) / strips;
+        p.rows_grid = (nrows + p.rows_per_strip - 1) / p.rows_per_strip * p.rows_nseg;
+        const int wseg = d->W < kDataRowSegment ? d->W : kDataRowSegment;
+        p.rows_nbw = ((wseg + 15) / 16 + 3) / 4;
+        size_t cur = 0;
+        p.header = take(&cur, 256);
+        p.wt = take(&cur, (size_t)d->K * d->C * d->R * d->S * elem_bytes(d->dtype));
+        p.row_counts = take(&cur, (size_t)p.rows_grid * 4);
+        if (d->act_layout == CBW_NCHW) {
+            p.t_dy = take(&cur, (size_t)d->N * d->P * d->Q * d->K * elem_bytes(d->dtype));
+            p.t_dx = take(&cur, (size_t)p.npix * d->C * elem_bytes(d->dtype));
+            if (masked) p.t_mask = take(&cur, ((size_t)p.npix * d->C + 31) / 32 * 4);
+        }
+        p.total = cur;
+        *out = p;
+        return CBW_OK;
+    }
     p.tile = data_tile_index(d->C);
     p.bm = kDataTiles[p.tile].bm;
     p.bn = kDataTiles[p.tile].bn;

@@ -15,6 +15,7 @@ constexpr int kWeightTileC = CBW_DW_BM; // channels c per weight-gradient tile
 constexpr int kWeightTileK = CBW_DW_BN; // output channels k per weight-gradient tile
 constexpr int kCompactBlock = 256;      // pixels per compaction block
 constexpr int kRowSegment = 128;        // output columns per segment of the row-window weight gradient
+constexpr int kDataRowSegment = 224;    // output columns per segment of the row-window data gradient
 // Resident weight-gradient workgroups the split-K factor aims to fill exactly.
 constexpr int kWeightSlots = CBW_NUM_CUS * CBW_DW_OCC;
 
@@ -36,7 +37,12 @@ struct DataPlan {
     int brows = 0;          // dense / select: pixel rows per tile (data_rows_pick)
     int maxtiles = 0;       // most tiles any row choice can give (the gather mode's grid)
     int split = 1;          // dense / select: host-chosen reduction split
-    Region header, wt, blk_counts, counts, dead_flags, lists, partial;
+    // Row-window kernel (data_rows_eligible): a workgroup per (column
+    // segment, strip of rows_per_strip output rows), nbw 16-column blocks
+    // per wave at most; it replaces the tiled GEMM and its compaction.
+    bool rows = false;
+    int rows_grid = 0, rows_per_strip = 0, rows_nseg = 0, rows_nbw = 0;
+    Region header, wt, blk_counts, counts, dead_flags, lists, partial, row_counts;
     // NCHW callers: NHWC copies of dY and dX and the NHWC-order footprint,
     // after every other region (the other offsets do not depend on layout)
     Region t_dy, t_dx, t_mask;
@@ -44,6 +50,11 @@ struct DataPlan {
 };
 
 constexpr int kDataSlots = CBW_NUM_CUS * CBW_DX_OCC;  // resident data-gradient workgroups
+
+// Layers the row-window data gradient serves: bf16, 3 x 3 filters, stride
+// 1, 64 input and 64 output channels (any padding, any layout: NCHW calls
+// run it on their NHWC copies).
+bool data_rows_eligible(const cbw_conv_desc* d);
 constexpr int kDataMaxSplit = 16;
 
 // Same rule as the kernels' data_split (see common.hpp).
@@ -87,7 +98,9 @@ int validate_desc(const cbw_conv_desc* d);
 int require_nhwc(const cbw_conv_desc* d);
 // no_split: the reduction is never split (no partial-tile region; the
 // kernels get a split bound of 1), for callers with a bounded scratch.
-int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out, bool no_split = false);
+// allow_rows = false plans the tiled GEMM even for layers the row-window
+// kernel serves (the forward convolution, the tiling inspection).
+int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out, bool no_split = false, bool allow_rows = true);
 // allow_rows: narrow stride-1 layers (C and K multiples of 64, at most 128,
 // filters of at most 3 x 3, bf16) get the row-window kernel; callers that
 // need the chunked kernel (X-block skipping) pass false.

@@ -10,7 +10,9 @@ at sampled outputs (random ones plus image borders, tile-boundary rows
 included through the random draw) are compared with the fp64 oracle with the
 normwise and per-element bounds of the other parity tests; over the whole
 tensor, killed outputs must be +0.0 and the masked calls must equal the dense
-call bit for bit at live outputs.
+call bit for bit at live outputs.  (With C = K = 64 the data gradient runs
+the row-window kernel instead of the GEMM; the forward of those cases still
+runs the 64-channel tile at its row choices.)
 """
 import numpy as np
 import pytest
