@@ -45,7 +45,7 @@ bool tiles_consistent()
     if (data_split(1, 1 << 20, kDataSlots, kDataMaxSplit) != host_data_split(1, 1 << 20)) return false;
     for (int t = 0; t < kDataTileCount; ++t)
         if (data_tile_channels(t) != kDataTiles[t].bm || data_tile_pixels(t) != kDataTiles[t].bn) return false;
-    if (data_rows_segment() != kDataRowSegment) return false;
+    if (data_rows_segment() != kDataRowsSegment) return false;
     return weight_tile_channels() == kWeightTileC && weight_tile_k() == kWeightTileK &&
            compact_block_pixels() == kCompactBlock && weight_chunk(CBW_BF16) == weight_chunk_px(CBW_BF16) &&
            weight_chunk(CBW_F32) == weight_chunk_px(CBW_F32);
@@ -140,6 +140,13 @@ DataRowsParams data_rows_params(const cbw_conv_desc* d, const DataPlan& plan, co
     p.mask_bytes = (uint32_t)((plan.npix * d->C + 31) / 32 * 4);
     p.wt_bytes = (uint32_t)((int64_t)d->R * d->S * d->C * d->K * esz);
     p.div_h = make_fastdiv((uint32_t)d->H);
+    p.depth = plan.rows_depth;
+    p.nslot = plan.rows_depth + 3;
+    p.slot_bytes = plan.rows_slot;
+    p.mslot_bytes = plan.rows_mslot;
+    p.mask_off = p.nslot * p.slot_bytes;
+    p.div_nslot = make_fastdiv((uint32_t)p.nslot);
+    p.div_nmslot = make_fastdiv((uint32_t)(p.depth + 1));
     return p;
 }
 

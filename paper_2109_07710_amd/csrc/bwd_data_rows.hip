@@ -25,39 +25,47 @@
 // outputs +0.0; counted as not computed).
 #include <hip/hip_ext.h>
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
+#include "tiles.hpp"
 
 namespace cbw {
 namespace {
 
 constexpr int DR_NT = 512;                 // 8 waves: 2 channel halves x 4 column groups
-constexpr int DR_WT = 224;                 // output columns per segment
-constexpr int DR_ROWS = 240;               // LDS rows (dY columns) per plane: DR_WT + 2 halo, whole copy groups
-constexpr int DR_PLANE = DR_ROWS * 64;     // one plane: 32 output channels k of every column
-constexpr int DR_SLOT = 2 * DR_PLANE;      // one dY row segment (both k halves)
-constexpr int DR_SLOTS = 5;                // ring: the 3 rows in use and the next two steps' new rows
-constexpr int DR_MSLOT = 2048;             // footprint of one output row segment: 8 bytes per pixel
-constexpr int DR_MSLOTS = 3;               // this step's and the next two
-constexpr int DR_MW = DR_WT * 8 / 256;     // word copies (256 bytes each) per footprint row
-constexpr int DR_NU = 2 * DR_ROWS / 16;    // copy instructions per dY row (16 LDS rows of 64 bytes each)
-constexpr int DR_UPW = (DR_NU + 7) / 8;    // per wave
-static_assert(DR_ROWS % 16 == 0 && DR_ROWS >= DR_WT + 2 && DR_PLANE < 65536, "row-window shape");
-static_assert(DR_WT * 8 <= DR_MSLOT && DR_WT * 8 % 256 == 0 && DR_MW <= 8, "footprint slot");
+constexpr int DR_WT = kDataRowsSegment;    // output columns per segment (at most)
+constexpr int DR_NU_MAX = ((DR_WT + 15) / 16 * 16 + 2 + 7) / 8;   // copy instructions per dY row (8 rows each)
+constexpr int DR_UPW = (DR_NU_MAX + 7) / 8;      // per wave
+static_assert(DR_WT * 8 % 256 == 0 && DR_WT * 8 / 256 <= 8, "footprint copies: one per wave at most");
 
-// Planes of 64-byte rows: a 16-byte chunk j of row i sits at physical chunk
-// (j + i / 4) mod 4.  A fragment read takes 16 lanes per cycle, sixteen
-// consecutive rows at one logical chunk: rows i and i + 4m land in the same
-// quarter of the banks (64 bytes = 16 banks per row) and the four of them
-// at four different chunks, so the cycle covers all 64 banks.
-__device__ __forceinline__ int dr_chunk(int row, int j) { return (j + (row >> 2)) & 3; }
+// 128-byte rows (one dY column, all 64 k): the 16-byte chunk j of row i sits
+// at physical chunk j ^ (i mod 8).  A fragment read covers sixteen
+// consecutive rows at one logical chunk, starting at any row (the tap shift
+// s moves the start by 0, 1 or 2).  Measured with the bank-conflict counter
+// on single-wave reads of this shape: chunk ^ (i mod 8) is conflict-free for
+// every start; the tiled GEMM's chunk ^ ((i / 2) mod 8) is conflict-free
+// only for starts that are multiples of 16 (4 conflict cycles per read
+// otherwise), and rows of 64 bytes in two k planes conflict for every start.
+__device__ __forceinline__ int dr_swz(int row) { return row & 7; }
 
 // Ring slot of dY row p (p >= -16): (p + 20) mod 5 by a multiply and shift.
-__device__ __forceinline__ int dr_slot(int p)
+// Wait until at most n (0 .. 63) of this wave's vector memory operations
+// are outstanding (s_waitcnt takes the count as an immediate).
+__device__ __forceinline__ void wait_vmem_le(int n)
 {
-    static_assert(DR_SLOTS == 5, "the slot formula divides by 5");
-    const uint32_t x = (uint32_t)(p + 20);
-    return (int)(x - ((x * 52429u) >> 18) * 5u);
+    switch (n) {
+#define CBW_VMCNT_CASE(k) \
+    case k: __builtin_amdgcn_s_waitcnt(0x0f70 | ((k) & 15) | ((((k) >> 4) & 3) << 14)); break;
+#define CBW_VMCNT_8(k) CBW_VMCNT_CASE(k) CBW_VMCNT_CASE(k + 1) CBW_VMCNT_CASE(k + 2) CBW_VMCNT_CASE(k + 3) \
+    CBW_VMCNT_CASE(k + 4) CBW_VMCNT_CASE(k + 5) CBW_VMCNT_CASE(k + 6) CBW_VMCNT_CASE(k + 7)
+        CBW_VMCNT_8(0) CBW_VMCNT_8(8) CBW_VMCNT_8(16) CBW_VMCNT_8(24)
+        CBW_VMCNT_8(32) CBW_VMCNT_8(40) CBW_VMCNT_8(48) CBW_VMCNT_8(56)
+#undef CBW_VMCNT_8
+#undef CBW_VMCNT_CASE
+    default: __builtin_amdgcn_s_waitcnt(0x0f70); break;   // vmcnt(0)
+    }
 }
 
 // NBW: 16-column blocks per wave at most; MASKED: x_mask applied.
@@ -65,8 +73,10 @@ template <int NBW, bool MASKED>
 __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
 {
     static_assert(NBW >= 1 && NBW <= 4, "column blocks per wave");
-    __shared__ __attribute__((aligned(1024))) char Ys[DR_SLOTS * DR_SLOT];
-    __shared__ __attribute__((aligned(1024))) char Ms[MASKED ? DR_MSLOTS * DR_MSLOT : 16];
+    // The ring of dY rows (p.nslot slots of p.slot_bytes) and, masked, the
+    // ring of footprint rows (p.depth + 1 slots of p.mslot_bytes) after it.
+    __shared__ __attribute__((aligned(1024))) char Ys[kDataRowsLds];
+    char* const Ms = Ys + p.mask_off;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -77,6 +87,7 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
     const int seg = t % p.nseg, strip = t / p.nseg;
     const int w0 = seg * DR_WT;
     const int wn = min(DR_WT, p.W - w0);               // valid columns of the segment
+    const int nu = p.slot_bytes >> 10;                 // copy instructions per dY row
     const int row_begin = strip * p.rows_per_strip;
     const int row_end = min(row_begin + p.rows_per_strip, p.nrows);
 
@@ -103,66 +114,65 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
                 }
     }
 
-    // B fragment offsets in a ring slot: output column block j, tap column
-    // s; LDS row i = 16 (b0 + j) + col + 2 - s holds dY column
-    // w0 + pw - 2 + i.  The k half adds DR_PLANE (an instruction offset).
-    int boff[3][NBW];
+    // B fragment offsets in a ring slot: output column block b0, tap column
+    // s, k half kc; LDS row i = 16 b0 + col + 2 - s holds dY column
+    // w0 + pw - 2 + i.  Block b0 + j adds 16 rows (2048 bytes, an
+    // instruction offset: the swizzle repeats every 16 rows).
+    int boff[3][2];
 #pragma unroll
     for (int s = 0; s < 3; ++s)
 #pragma unroll
-        for (int j = 0; j < NBW; ++j) {
-            const int i = 16 * (b0 + j) + col + 2 - s;
-            boff[s][j] = i * 64 + 16 * dr_chunk(i, g);
+        for (int kc = 0; kc < 2; ++kc) {
+            const int i = 16 * b0 + col + 2 - s;
+            boff[s][kc] = i * 128 + 16 * ((4 * kc + g) ^ dr_swz(i));
         }
 
     // Copies of a dY row segment: instruction u writes LDS bytes
-    // [1024 u, 1024 u + 1024) of the slot, i.e. plane u / 15, rows
-    // 16 (u % 15) + l / 4 at physical chunk l % 4 for lane l.
+    // [1024 u, 1024 u + 1024) of the slot, i.e. rows 8 u + l / 8 at physical
+    // chunk l % 8 for lane l.
+    // Ring slots: dY row p in slot (p + 16) mod nslot, the footprint of
+    // output row `row` in slot row mod (depth + 1).  The pipeline below
+    // advances both by one per step instead of dividing.
+    auto dr_slot = [&](int pp) { const uint32_t x = (uint32_t)(pp + 16); return (int)(x - fdiv(x, p.div_nslot) * p.nslot); };
+    auto mslot = [&](int row) { return (int)((uint32_t)row - fdiv((uint32_t)row, p.div_nmslot) * (p.depth + 1)); };
+    auto wrap = [](int x, int n) { return x >= n ? x - n : (x < 0 ? x + n : x); };   // |x| < 2n
     const u32x4_t rs_dy = make_rsrc_words(p.dy, p.dy_bytes);
     uint32_t ylane[DR_UPW];
 #pragma unroll
     for (int m = 0; m < DR_UPW; ++m) {
         const int u = wave + 8 * m;
-        const int kc = u / (DR_ROWS / 16), tg = u - kc * (DR_ROWS / 16);
-        const int i = 16 * tg + (lane >> 2), pc = lane & 3;
-        const int j = (pc - (i >> 2)) & 3;             // logical chunk stored at physical chunk pc
+        const int i = 8 * u + (lane >> 3);
+        const int j = (lane & 7) ^ dr_swz(i);          // logical chunk stored at physical chunk lane % 8
         const int q = w0 + p.pad_w - 2 + i;
-        ylane[m] = (u < DR_NU && q >= 0 && q < p.Q) ? (uint32_t)((q * 64 + kc * 32 + j * 8) * 2) : kOOB;
+        ylane[m] = (u < nu && q >= 0 && q < p.Q) ? (uint32_t)((q * 64 + j * 8) * 2) : kOOB;
     }
-    auto copy_y = [&](int n, int pp) -> int {          // dY row (n, pp) into its ring slot
-        if (pp < 0 || pp >= p.P) return 0;             // rows outside the image are never read
-        const uint32_t base = (uint32_t)(n * p.P + pp) * (uint32_t)(p.Q * 128);
-        const uint32_t lds = lds_addr(Ys) + (uint32_t)(dr_slot(pp) * DR_SLOT);
+    // dY row (n, pp) into ring slot `slot`; a row outside the image (the
+    // padding above and below) is written as zeros, so that the matrix loop
+    // reads every tap's row without a branch
+    auto copy_y = [&](int n, int pp, int slot) -> int {
+        const bool in = pp >= 0 && pp < p.P;
+        const uint32_t base = in ? (uint32_t)(n * p.P + pp) * (uint32_t)(p.Q * 128) : 0u;
+        const uint32_t lds = lds_addr(Ys) + (uint32_t)(slot * p.slot_bytes);
         int issued = 0;
 #pragma unroll
         for (int m = 0; m < DR_UPW; ++m) {
             const int u = wave + 8 * m;
-            if (u < DR_NU) {
-                buf_load16_lds(rs_dy, ylane[m] == kOOB ? kOOB : base + ylane[m], lds + 1024u * u);
+            if (u < nu) {
+                buf_load16_lds(rs_dy, (!in || ylane[m] == kOOB) ? kOOB : base + ylane[m], lds + 1024u * u);
                 ++issued;
             }
         }
         return issued;
     };
     const u32x4_t rs_m = make_rsrc_words(p.mask, p.mask_bytes);
-    auto copy_m = [&](int row) -> int {                // footprint of output row `row`: 4 bytes per lane
-        if (!MASKED || wave >= DR_MW) return 0;        // (waves 0 .. DR_MW - 1, one word copy each)
+    auto copy_m = [&](int row, int slot) -> int {      // footprint of output row `row`: 4 bytes per lane
+        if (!MASKED || wave >= (p.mslot_bytes >> 8)) return 0;   // one word copy per wave
         const uint32_t byte = 256u * wave + 4u * lane;
         const uint32_t off = byte < (uint32_t)(wn * 8) ? (uint32_t)(row * p.W + w0) * 8u + byte : kOOB;
-        buf_load4_lds(rs_m, off, lds_addr(Ms) + (uint32_t)((row % DR_MSLOTS) * DR_MSLOT) + 256u * wave);
+        buf_load4_lds(rs_m, off, lds_addr(Ms) + (uint32_t)(slot * p.mslot_bytes) + 256u * wave);
         return 1;
     };
     auto image = [&](int row) { return (int)fdiv((uint32_t)row, p.div_h); };
-    auto follows = [&](int a, int b) { return b == a + 1 && image(a) == image(b); };
-    auto all_rows = [&](int row) {                     // the three dY rows of output row `row`
-        const int n = image(row), h = row - n * p.H;
-#pragma unroll
-        for (int r = 0; r < 3; ++r) copy_y(n, h + p.pad_h - r);
-    };
-    auto new_row = [&](int row) -> int {               // the dY row the window gains at `row`
-        const int n = image(row), h = row - n * p.H;
-        return copy_y(n, h + p.pad_h);
-    };
 
     floatx4 acc[2][NBW];
 #pragma unroll
@@ -170,47 +180,54 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
     uint2 outv[2][NBW];                                // the previous row's outputs, stored one step later
     int computed = 0;                                  // pixels of the rows whose matrix work ran
 
-    auto compute = [&](int row) {
-        const int n = image(row), h = row - n * p.H;
+    // The wave's NB column blocks (NB = cnt, a compile-time constant in each
+    // copy of the pipeline below, so the block loops carry no branches and
+    // the fragment reads of a (tap, k half) are issued ahead of its MFMAs).
+    auto compute = [&](int h, int sl0, auto nb_tag) {   // output row h of its image; slot of dY row h + ph
+        constexpr int NB = decltype(nb_tag)::value;
+        (void)h;
+        const char* yb[3];
 #pragma unroll
-        for (int r = 0; r < 3; ++r) {
-            const int pp = h + p.pad_h - r;
-            if (pp >= 0 && pp < p.P) {                 // uniform
-                const char* yb = Ys + dr_slot(pp) * DR_SLOT;
+        for (int r = 0; r < 3; ++r) yb[r] = Ys + wrap(sl0 - r, p.nslot) * p.slot_bytes;
+        // straight-line code over the 9 taps and both k halves: the fragment
+        // reads of later taps can be issued ahead of earlier MFMAs
 #pragma unroll
-                for (int s = 0; s < 3; ++s)
+        for (int r = 0; r < 3; ++r)
 #pragma unroll
-                    for (int kc = 0; kc < 2; ++kc)
+            for (int s = 0; s < 3; ++s)
 #pragma unroll
-                        for (int j = 0; j < NBW; ++j) {
-                            if (j < cnt) {             // uniform; indices stay compile-time constants
-                                const uint4 fb = *reinterpret_cast<const uint4*>(yb + boff[s][j] + kc * DR_PLANE);
-                                acc[0][j] = mfma_chunk(acc[0][j], afr[3 * r + s][0][kc], fb, uint16_t{});
-                                acc[1][j] = mfma_chunk(acc[1][j], afr[3 * r + s][1][kc], fb, uint16_t{});
-                            }
-                        }
-            }
-        }
+                for (int kc = 0; kc < 2; ++kc) {
+                    uint4 fb[NB > 0 ? NB : 1];
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+                        fb[j] = *reinterpret_cast<const uint4*>(yb[r] + boff[s][kc] + 2048 * j);
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) {
+                        acc[0][j] = mfma_chunk(acc[0][j], afr[3 * r + s][0][kc], fb[j], uint16_t{});
+                        acc[1][j] = mfma_chunk(acc[1][j], afr[3 * r + s][1][kc], fb[j], uint16_t{});
+                    }
+                }
     };
 
     // One output row: footprint words, the matrix work unless the row is
     // dead, then the outputs rounded, masked and held for the next step.
-    auto step = [&](int row) {
-        uint32_t mw[NBW];
+    auto step = [&](int h, int sl0, int ms, auto nb_tag) {
+        constexpr int NB = decltype(nb_tag)::value;
+        uint32_t mw[NB > 0 ? NB : 1];
         bool live = true;
         if (MASKED) {
-            const char* mrow = Ms + (row % DR_MSLOTS) * DR_MSLOT;
+            const char* mrow = Ms + ms * p.mslot_bytes;
 #pragma unroll
-            for (int j = 0; j < NBW; ++j) {
+            for (int j = 0; j < NB; ++j) {
                 const int px = 16 * (b0 + j) + col;
-                mw[j] = (j < cnt && px < wn) ? *reinterpret_cast<const uint32_t*>(mrow + px * 8 + cw * 4) : 0u;
+                mw[j] = px < wn ? *reinterpret_cast<const uint32_t*>(mrow + px * 8 + cw * 4) : 0u;
             }
             if (p.skip) {
                 // the whole segment's footprint, read by every wave alike
                 const uint4* mv = reinterpret_cast<const uint4*>(mrow);
                 uint32_t any = 0;
 #pragma unroll
-                for (int v = 0; v < DR_MSLOT / 16 / 64; ++v) {
+                for (int v = 0; v < (DR_WT * 8 + 1023) / 1024; ++v) {
                     const int idx = lane + 64 * v;   // pixels 2 idx and 2 idx + 1
                     if (2 * idx < wn) {
                         const uint4 x = mv[idx];
@@ -222,11 +239,11 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
             }
         }
         if (live) {
-            compute(row);
+            compute(h, sl0, nb_tag);
             computed += wn;
         }
 #pragma unroll
-        for (int j = 0; j < NBW; ++j) {
+        for (int j = 0; j < NB; ++j) {
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb) {
                 const floatx4 v = acc[cb][j];
@@ -242,58 +259,88 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
         }
     };
     const __amdgpu_buffer_rsrc_t rs_dx = make_rsrc(p.dx, p.dx_bytes);
-    auto store = [&](int row) {                        // outputs of `row`: 4 channels of one pixel per lane
+    auto store = [&](int row, auto nb_tag) {           // outputs of `row`: 4 channels of one pixel per lane
+        constexpr int NB = decltype(nb_tag)::value;
 #pragma unroll
-        for (int j = 0; j < NBW; ++j) {
-            if (j < cnt) {
-                const int w = 16 * (b0 + j) + col;
-                const uint32_t base = (uint32_t)(((row * p.W + w0 + w) * 64 + 32 * cw + 4 * g) * 2);
+        for (int j = 0; j < NB; ++j) {
+            const int w = 16 * (b0 + j) + col;
+            const uint32_t base = (uint32_t)(((row * p.W + w0 + w) * 64 + 32 * cw + 4 * g) * 2);
 #pragma unroll
-                for (int cb = 0; cb < 2; ++cb) {
-                    const uint32_t off = w < wn ? base + 32u * cb : kOOB;
-                    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, outv[cb][j]), rs_dx, off, 0, 0);
-                }
+            for (int cb = 0; cb < 2; ++cb) {
+                const uint32_t off = w < wn ? base + 32u * cb : kOOB;
+                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, outv[cb][j]), rs_dx, off, 0, 0);
             }
         }
     };
 
-    // Pipeline over the strip's rows: at step i the copies of step i + 2 are
-    // issued (its new dY row when rows i .. i + 2 are consecutive rows of one
-    // image, and its footprint) and the outputs of step i - 1 are stored
-    // before them; the wait at the end of step i leaves only the copies just
-    // issued in flight (stores issued before them have completed by then, as
-    // have the older copies, which land in issue order).  A row that starts a
-    // new image has its three dY rows loaded after the step before it.
-    int ra = row_begin;
-    if (ra < row_end) {
-        all_rows(ra);
-        copy_m(ra);
-        if (ra + 1 < row_end) {
-            if (follows(ra, ra + 1)) new_row(ra + 1);
-            copy_m(ra + 1);
+    // Pipeline over the strip's rows, D = p.depth steps ahead: at step i the
+    // copies of step i + D are issued (its new dY row when it lies in the
+    // same image as row i, and its footprint) after the outputs of step i - 1
+    // are stored; the wait at the end of step i leaves only the copies of
+    // steps i + 2 .. i + D in flight (stores issued before them have
+    // completed by then, as have the older copies, which land in issue
+    // order).  A window starts at the strip's first row and at every first
+    // row of an image: its three dY rows and the new rows of the next D - 1
+    // steps are loaded after the step before it, and waited for.  Every
+    // wave runs the same steps and barriers, in the copy of this loop for
+    // its own block count.
+    auto pipeline = [&](auto nb_tag) {
+        const int D = p.depth, nm = p.depth + 1;
+        // state of step row ra: image n, row h, ring slot sl0 of dY row
+        // h + ph, footprint slot ms; allowed = copies issued at the last
+        // D - 1 steps, hist = the issue counts of the last steps, a byte each
+        int n = 0, h = 0, sl0 = 0, ms = 0, allowed = 0;
+        uint64_t hist = 0;
+        auto open_window = [&](int rs) {
+            n = image(rs);
+            h = rs - n * p.H;
+            sl0 = dr_slot(h + p.pad_h);
+#pragma unroll
+            for (int r = 0; r < 3; ++r) copy_y(n, h + p.pad_h - r, wrap(sl0 - r, p.nslot));
+            for (int d = 1; d < D && rs + d < row_end && h + d < p.H; ++d)
+                copy_y(n, h + p.pad_h + d, wrap(sl0 + d, p.nslot));
+            hist = 0;
+            allowed = 0;
+        };
+        int ra = row_begin;
+        if (ra < row_end) {
+            open_window(ra);
+            ms = mslot(ra);
+            for (int d = 0; d < D && ra + d < row_end; ++d) copy_m(ra + d, wrap(ms + d, nm));
         }
-    }
-    wait_vmem();
-    __syncthreads();
-    for (; ra < row_end; ++ra) {
-        const int rb = ra + 1, rc = ra + 2;
-        if (ra > row_begin) store(ra - 1);
-        int issued = 0;
-        if (rc < row_end) {
-            if (follows(ra, rb) && follows(rb, rc)) issued += new_row(rc);
-            issued += copy_m(rc);
-        }
-        step(ra);
-        wait_vmem_upto(issued);
+        wait_vmem();
         __syncthreads();
-        if (rb < row_end && !follows(ra, rb)) {
-            all_rows(rb);
-            if (rc < row_end && follows(rb, rc)) new_row(rc);
-            wait_vmem();
+        for (; ra < row_end; ++ra) {
+            if (ra > row_begin) store(ra - 1, nb_tag);
+            int issued = 0;
+            if (ra + D < row_end) {
+                if (h + D < p.H) issued += copy_y(n, h + p.pad_h + D, wrap(sl0 + D, p.nslot));
+                issued += copy_m(ra + D, wrap(ms + D, nm));
+            }
+            hist = (hist << 8) | (uint64_t)issued;
+            allowed += issued - (int)((hist >> (8 * (D - 1))) & 0xffu);
+            step(h, sl0, ms, nb_tag);
+            wait_vmem_le(allowed);
             __syncthreads();
+            // advance to row ra + 1
+            ms = wrap(ms + 1, nm);
+            if (h + 1 < p.H) {
+                ++h;
+                sl0 = wrap(sl0 + 1, p.nslot);
+            } else if (ra + 1 < row_end) {
+                open_window(ra + 1);   // the next image
+                wait_vmem();
+                __syncthreads();
+            }
         }
-    }
-    if (row_end > row_begin) store(row_end - 1);
+        if (row_end > row_begin) store(row_end - 1, nb_tag);
+    };
+    // cnt <= NBW (checked by the host for the first segment, which is the widest)
+    if (cnt >= NBW) pipeline(std::integral_constant<int, NBW>{});
+    else if (NBW >= 2 && cnt == NBW - 1) pipeline(std::integral_constant<int, (NBW >= 2 ? NBW - 1 : 0)>{});
+    else if (NBW >= 3 && cnt == NBW - 2) pipeline(std::integral_constant<int, (NBW >= 3 ? NBW - 2 : 0)>{});
+    else if (NBW >= 4 && cnt == NBW - 3) pipeline(std::integral_constant<int, (NBW >= 4 ? NBW - 3 : 0)>{});
+    else pipeline(std::integral_constant<int, 0>{});
     if (tid == 0) p.row_counts[blockIdx.x] = computed;
 }
 
@@ -318,6 +365,13 @@ hipError_t launch_bwd_data_rows(const DataRowsParams& p, int grid, int nbw, hipS
     // the grid must cover every (segment, strip) pair exactly as planned
     const int nstrips = (p.nrows + p.rows_per_strip - 1) / p.rows_per_strip;
     if (p.nseg != (p.W + DR_WT - 1) / DR_WT || grid != nstrips * p.nseg || p.nrows != p.N * p.H)
+        return hipErrorInvalidValue;
+    // the rings as the planner laid them out
+    const int wseg = p.W < DR_WT ? p.W : DR_WT;
+    if (p.depth < 1 || p.depth > 8 || p.nslot != p.depth + 3 || p.slot_bytes != ((wseg + 15) / 16 * 16 + 2 + 7) / 8 * 1024 ||
+        p.mslot_bytes != (wseg * 8 + 255) / 256 * 256 || p.mask_off != p.nslot * p.slot_bytes ||
+        p.mask_off + (p.depth + 1) * p.mslot_bytes > kDataRowsLds || p.div_nslot.d != (uint32_t)p.nslot ||
+        p.div_nmslot.d != (uint32_t)(p.depth + 1))
         return hipErrorInvalidValue;
     if (nbw < (((p.W < DR_WT ? p.W : DR_WT) + 15) / 16 + 3) / 4) return hipErrorInvalidValue;
     switch (nbw) {

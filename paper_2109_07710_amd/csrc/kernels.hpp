@@ -65,6 +65,10 @@ struct DataRowsParams {
     int skip;                // masked: rows whose footprint is empty skip the matrix work
     uint32_t dy_bytes, dx_bytes, mask_bytes, wt_bytes;
     FastDiv div_h;           // output row -> image
+    // rings in LDS: depth steps of prefetch, nslot = depth + 3 dY rows of
+    // slot_bytes, then (from mask_off) depth + 1 footprint rows of mslot_bytes
+    int depth, nslot, slot_bytes, mslot_bytes, mask_off;
+    FastDiv div_nslot, div_nmslot;
 };
 int data_rows_segment();
 hipError_t launch_bwd_data_rows(const DataRowsParams& p, int grid, int nbw, hipStream_t stream, const ProfEvents& ev);

@@ -88,14 +88,23 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out, bool no_split,
         p.npix = (int64_t)d->N * d->H * d->W;
         p.groups = (d->C + p.bm - 1) / p.bm;
         p.rows = true;
-        p.rows_nseg = (d->W + kDataRowSegment - 1) / kDataRowSegment;
+        p.rows_nseg = (d->W + kDataRowsSegment - 1) / kDataRowsSegment;
         const int nrows = d->N * d->H;
         int strips = CBW_NUM_CUS / p.rows_nseg;
         if (strips < 1) strips = 1;
         p.rows_per_strip = (nrows + strips - 1) / strips;
         p.rows_grid = (nrows + p.rows_per_strip - 1) / p.rows_per_strip * p.rows_nseg;
-        const int wseg = d->W < kDataRowSegment ? d->W : kDataRowSegment;
+        const int wseg = d->W < kDataRowsSegment ? d->W : kDataRowsSegment;
         p.rows_nbw = ((wseg + 15) / 16 + 3) / 4;
+        // the deepest prefetch (at most 8 steps) whose rings fit the LDS:
+        // depth + 3 dY rows and depth + 1 footprint rows
+        // a slot holds the 16-column blocks' rows and the two halo columns
+        p.rows_slot = ((wseg + 15) / 16 * 16 + 2 + 7) / 8 * 1024;
+        p.rows_mslot = (wseg * 8 + 255) / 256 * 256;
+        p.rows_depth = 8;
+        while (p.rows_depth > 1 &&
+               (p.rows_depth + 3) * p.rows_slot + (p.rows_depth + 1) * p.rows_mslot > kDataRowsLds)
+            --p.rows_depth;
         size_t cur = 0;
         p.header = take(&cur, 256);
         p.wt = take(&cur, (size_t)d->K * d->C * d->R * d->S * elem_bytes(d->dtype));

@@ -15,7 +15,6 @@ constexpr int kWeightTileC = CBW_DW_BM; // channels c per weight-gradient tile
 constexpr int kWeightTileK = CBW_DW_BN; // output channels k per weight-gradient tile
 constexpr int kCompactBlock = 256;      // pixels per compaction block
 constexpr int kRowSegment = 128;        // output columns per segment of the row-window weight gradient
-constexpr int kDataRowSegment = 224;    // output columns per segment of the row-window data gradient
 // Resident weight-gradient workgroups the split-K factor aims to fill exactly.
 constexpr int kWeightSlots = CBW_NUM_CUS * CBW_DW_OCC;
 
@@ -42,6 +41,7 @@ struct DataPlan {
     // per wave at most; it replaces the tiled GEMM and its compaction.
     bool rows = false;
     int rows_grid = 0, rows_per_strip = 0, rows_nseg = 0, rows_nbw = 0;
+    int rows_depth = 0, rows_slot = 0, rows_mslot = 0;   // prefetch depth, ring slot bytes
     Region header, wt, blk_counts, counts, dead_flags, lists, partial, row_counts;
     // NCHW callers: NHWC copies of dY and dX and the NHWC-order footprint,
     // after every other region (the other offsets do not depend on layout)

@@ -38,6 +38,12 @@ constexpr int kDataTileCount = 3;
 constexpr int kGatherMaxGroups = 16;
 constexpr DataTile kDataTiles[kDataTileCount] = {{256, 224, 8, 2}, {128, 448, 4, 4}, {64, 512, 2, 8}};
 
+// Row-window data gradient (3 x 3, stride 1, 64 channels in and out): output
+// columns per segment at most, and the LDS its two rings share (dY rows of
+// 128 bytes per column plus halo, footprint rows of 8 bytes per pixel).
+constexpr int kDataRowsSegment = 224;
+constexpr int kDataRowsLds = 159744;
+
 // Pixel rows a data-gradient tile actually covers: its capacity BN, or 16 or
 // 32 rows less.  With `slots` resident workgroups the busiest CU runs
 // ceil(tiles / slots) tiles one after another, so the rows that make

@@ -86,6 +86,8 @@ SHAPES = [
     (2, 11, 37, (0, 0)),     # no padding: P = H - 2, Q = W - 2
     (2, 8, 40, (2, 2)),      # pad 2: P = H + 2
     (1, 10, 24, (2, 0)),     # unequal pads
+    (100, 13, 12, (1, 1)),   # strips of 6 rows across 13-row images, prefetch 8 rows deep
+    (6, 90, 150, (1, 1)),    # strips of 3 rows, prefetch 4 rows deep (150-column rings)
 ]
 
 
