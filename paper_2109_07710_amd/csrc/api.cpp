@@ -146,7 +146,7 @@ DataRowsParams data_rows_params(const cbw_conv_desc* d, const DataPlan& plan, co
     p.mslot_bytes = plan.rows_mslot;
     p.mask_off = p.nslot * p.slot_bytes;
     p.div_nslot = make_fastdiv((uint32_t)p.nslot);
-    p.div_nmslot = make_fastdiv((uint32_t)(p.depth + 1));
+    p.div_nmslot = make_fastdiv((uint32_t)(p.depth + 2));
     return p;
 }
 
@@ -811,7 +811,7 @@ int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, siz
                 if (e != hipSuccess) return hip_status(e);
                 for (int i = 0; i < n; ++i) live += buf[i];
             }
-            r.rows_live = live * plan.groups;
+            r.rows_live = live / 2 * plan.groups;   // each pixel is counted by its two channel-half waves
         } else if (op == CBW_OP_BWD_DATA_MASKED && header == MODE_GATHER) {
             int32_t counts[64];
             int64_t live = 0;

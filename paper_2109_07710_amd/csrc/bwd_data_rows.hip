@@ -20,9 +20,10 @@
 //
 // GEMM view per step: M = c (A = filters, registers), N = output columns w
 // (B = shifted dY rows, LDS), reduction = (r, s, k).  Masked calls stage the
-// row's footprint words next to its dY copies, zero the dead outputs in the
-// epilogue and skip the matrix work of a row whose footprint is empty (all
-// outputs +0.0; counted as not computed).
+// row's footprint words next to its dY copies, zero the dead outputs when
+// they are stored, and a wave skips the matrix work of a row when every one
+// of its outputs there (its channel half of its columns) is dead: those
+// outputs are +0.0 and are counted as not computed.
 #include <hip/hip_ext.h>
 
 #include <type_traits>
@@ -38,7 +39,7 @@ constexpr int DR_NT = 512;                 // 8 waves: 2 channel halves x 4 colu
 constexpr int DR_WT = kDataRowsSegment;    // output columns per segment (at most)
 constexpr int DR_NU_MAX = ((DR_WT + 15) / 16 * 16 + 2 + 7) / 8;   // copy instructions per dY row (8 rows each)
 constexpr int DR_UPW = (DR_NU_MAX + 7) / 8;      // per wave
-static_assert(DR_WT * 8 % 256 == 0 && DR_WT * 8 / 256 <= 8, "footprint copies: one per wave at most");
+static_assert(DR_WT * 8 <= 256 * 8, "footprint copies: one per wave at most");
 
 // 128-byte rows (one dY column, all 64 k): the 16-byte chunk j of row i sits
 // at physical chunk j ^ (i mod 8).  A fragment read covers sixteen
@@ -74,7 +75,8 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
 {
     static_assert(NBW >= 1 && NBW <= 4, "column blocks per wave");
     // The ring of dY rows (p.nslot slots of p.slot_bytes) and, masked, the
-    // ring of footprint rows (p.depth + 1 slots of p.mslot_bytes) after it.
+    // ring of footprint rows (p.depth + 2 slots of p.mslot_bytes) after it:
+    // this step's, the previous one's (stored now) and the next depth.
     __shared__ __attribute__((aligned(1024))) char Ys[kDataRowsLds];
     char* const Ms = Ys + p.mask_off;
 
@@ -131,10 +133,10 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
     // [1024 u, 1024 u + 1024) of the slot, i.e. rows 8 u + l / 8 at physical
     // chunk l % 8 for lane l.
     // Ring slots: dY row p in slot (p + 16) mod nslot, the footprint of
-    // output row `row` in slot row mod (depth + 1).  The pipeline below
+    // output row `row` in slot row mod (depth + 2).  The pipeline below
     // advances both by one per step instead of dividing.
     auto dr_slot = [&](int pp) { const uint32_t x = (uint32_t)(pp + 16); return (int)(x - fdiv(x, p.div_nslot) * p.nslot); };
-    auto mslot = [&](int row) { return (int)((uint32_t)row - fdiv((uint32_t)row, p.div_nmslot) * (p.depth + 1)); };
+    auto mslot = [&](int row) { return (int)((uint32_t)row - fdiv((uint32_t)row, p.div_nmslot) * (p.depth + 2)); };
     auto wrap = [](int x, int n) { return x >= n ? x - n : (x < 0 ? x + n : x); };   // |x| < 2n
     const u32x4_t rs_dy = make_rsrc_words(p.dy, p.dy_bytes);
     uint32_t ylane[DR_UPW];
@@ -165,11 +167,23 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
         return issued;
     };
     const u32x4_t rs_m = make_rsrc_words(p.mask, p.mask_bytes);
-    auto copy_m = [&](int row, int slot) -> int {      // footprint of output row `row`: 4 bytes per lane
-        if (!MASKED || wave >= (p.mslot_bytes >> 8)) return 0;   // one word copy per wave
-        const uint32_t byte = 256u * wave + 4u * lane;
-        const uint32_t off = byte < (uint32_t)(wn * 8) ? (uint32_t)(row * p.W + w0) * 8u + byte : kOOB;
-        buf_load4_lds(rs_m, off, lds_addr(Ms) + (uint32_t)(slot * p.mslot_bytes) + 256u * wave);
+    // footprint of output row `row` (8 bytes per pixel, wn pixels): 16 bytes
+    // per lane when the row is a whole number of 16-byte pieces (wn even),
+    // else 4 bytes per lane; one copy per wave of the first waves
+    auto copy_m = [&](int row, int slot) -> int {
+        if (!MASKED) return 0;
+        const uint32_t rowb = (uint32_t)(wn * 8);
+        const uint32_t src = (uint32_t)(row * p.W + w0) * 8u;
+        const uint32_t dst = lds_addr(Ms) + (uint32_t)(slot * p.mslot_bytes);
+        if ((wn & 1) == 0) {
+            if (wave * 1024 >= wn * 8) return 0;
+            const uint32_t byte = 1024u * wave + 16u * lane;
+            buf_load16_lds(rs_m, byte < rowb ? src + byte : kOOB, dst + 1024u * wave);
+        } else {
+            if (wave * 256 >= wn * 8) return 0;
+            const uint32_t byte = 256u * wave + 4u * lane;
+            buf_load4_lds(rs_m, byte < rowb ? src + byte : kOOB, dst + 256u * wave);
+        }
         return 1;
     };
     auto image = [&](int row) { return (int)fdiv((uint32_t)row, p.div_h); };
@@ -209,66 +223,70 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
                 }
     };
 
-    // One output row: footprint words, the matrix work unless the row is
-    // dead, then the outputs rounded, masked and held for the next step.
+    // The wave's footprint words of row slot `ms`: channels 32 cw .. + 31 of
+    // pixel 16 (b0 + j) + col (0 past the segment).
+    auto mask_words = [&](int ms, uint32_t* mw, auto nb_tag) {
+        constexpr int NB = decltype(nb_tag)::value;
+        const char* mrow = Ms + ms * p.mslot_bytes;
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            const int px = 16 * (b0 + j) + col;
+            mw[j] = px < wn ? *reinterpret_cast<const uint32_t*>(mrow + px * 8 + cw * 4) : 0u;
+        }
+    };
+    // pixels of this wave's columns (each pixel belongs to two waves, one
+    // per channel half)
+    const int wave_px = max(0, min(16 * (b0 + cnt), wn) - 16 * b0);
+
+    // One output row: the matrix work unless every output of this wave is
+    // dead (its channel half of its columns), then the sums rounded and held
+    // for the next step, which applies the footprint and stores them.
     auto step = [&](int h, int sl0, int ms, auto nb_tag) {
         constexpr int NB = decltype(nb_tag)::value;
-        uint32_t mw[NB > 0 ? NB : 1];
         bool live = true;
-        if (MASKED) {
-            const char* mrow = Ms + ms * p.mslot_bytes;
+        if (MASKED && p.skip) {
+            uint32_t mw[NB > 0 ? NB : 1];
+            mask_words(ms, mw, nb_tag);
+            uint32_t any = 0;
 #pragma unroll
-            for (int j = 0; j < NB; ++j) {
-                const int px = 16 * (b0 + j) + col;
-                mw[j] = px < wn ? *reinterpret_cast<const uint32_t*>(mrow + px * 8 + cw * 4) : 0u;
-            }
-            if (p.skip) {
-                // the whole segment's footprint, read by every wave alike
-                const uint4* mv = reinterpret_cast<const uint4*>(mrow);
-                uint32_t any = 0;
-#pragma unroll
-                for (int v = 0; v < (DR_WT * 8 + 1023) / 1024; ++v) {
-                    const int idx = lane + 64 * v;   // pixels 2 idx and 2 idx + 1
-                    if (2 * idx < wn) {
-                        const uint4 x = mv[idx];
-                        any |= x.x | x.y;
-                        if (2 * idx + 1 < wn) any |= x.z | x.w;
-                    }
-                }
-                live = __ballot(any != 0u) != 0ull;
-            }
+            for (int j = 0; j < NB; ++j) any |= mw[j];
+            live = __ballot(any != 0u) != 0ull;
         }
         if (live) {
             compute(h, sl0, nb_tag);
-            computed += wn;
+            computed += wave_px;
         }
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb) {
                 const floatx4 v = acc[cb][j];
-                uint32_t lo = pack_bf16x2(v.x, v.y), hi = pack_bf16x2(v.z, v.w);
-                if (MASKED) {
-                    const uint32_t keep = mw[j] >> (16 * cb + 4 * g);
-                    lo &= ((0u - (keep & 1u)) & 0xffffu) | ((0u - ((keep >> 1) & 1u)) & 0xffff0000u);
-                    hi &= ((0u - ((keep >> 2) & 1u)) & 0xffffu) | ((0u - ((keep >> 3) & 1u)) & 0xffff0000u);
-                }
-                outv[cb][j] = make_uint2(lo, hi);
+                outv[cb][j] = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
                 acc[cb][j] = floatx4{0.f, 0.f, 0.f, 0.f};
             }
         }
     };
     const __amdgpu_buffer_rsrc_t rs_dx = make_rsrc(p.dx, p.dx_bytes);
-    auto store = [&](int row, auto nb_tag) {           // outputs of `row`: 4 channels of one pixel per lane
+    // outputs of `row` (footprint slot ms): 4 channels of one pixel per lane;
+    // a dead output is stored as +0.0 (the bit pattern 0)
+    auto store = [&](int row, int ms, auto nb_tag) {
         constexpr int NB = decltype(nb_tag)::value;
+        uint32_t mw[NB > 0 ? NB : 1];
+        if (MASKED) mask_words(ms, mw, nb_tag);
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             const int w = 16 * (b0 + j) + col;
             const uint32_t base = (uint32_t)(((row * p.W + w0 + w) * 64 + 32 * cw + 4 * g) * 2);
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb) {
+                uint2 v = outv[cb][j];
+                if (MASKED) {
+                    const uint32_t keep = mw[j] >> (16 * cb + 4 * g);
+                    v.x &= ((0u - (keep & 1u)) & 0xffffu) | ((0u - ((keep >> 1) & 1u)) & 0xffff0000u);
+                    v.y &= ((0u - ((keep >> 2) & 1u)) & 0xffffu) | ((0u - ((keep >> 3) & 1u)) & 0xffff0000u);
+                }
                 const uint32_t off = w < wn ? base + 32u * cb : kOOB;
-                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, outv[cb][j]), rs_dx, off, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), rs_dx, off, 0, 0);
             }
         }
     };
@@ -285,7 +303,7 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
     // wave runs the same steps and barriers, in the copy of this loop for
     // its own block count.
     auto pipeline = [&](auto nb_tag) {
-        const int D = p.depth, nm = p.depth + 1;
+        const int D = p.depth, nm = p.depth + 2;
         // state of step row ra: image n, row h, ring slot sl0 of dY row
         // h + ph, footprint slot ms; allowed = copies issued at the last
         // D - 1 steps, hist = the issue counts of the last steps, a byte each
@@ -311,7 +329,7 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
         wait_vmem();
         __syncthreads();
         for (; ra < row_end; ++ra) {
-            if (ra > row_begin) store(ra - 1, nb_tag);
+            if (ra > row_begin) store(ra - 1, wrap(ms - 1, nm), nb_tag);
             int issued = 0;
             if (ra + D < row_end) {
                 if (h + D < p.H) issued += copy_y(n, h + p.pad_h + D, wrap(sl0 + D, p.nslot));
@@ -333,7 +351,7 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
                 __syncthreads();
             }
         }
-        if (row_end > row_begin) store(row_end - 1, nb_tag);
+        if (row_end > row_begin) store(row_end - 1, wrap(ms - 1, nm), nb_tag);
     };
     // cnt <= NBW (checked by the host for the first segment, which is the widest)
     if (cnt >= NBW) pipeline(std::integral_constant<int, NBW>{});
@@ -341,7 +359,16 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
     else if (NBW >= 3 && cnt == NBW - 2) pipeline(std::integral_constant<int, (NBW >= 3 ? NBW - 2 : 0)>{});
     else if (NBW >= 4 && cnt == NBW - 3) pipeline(std::integral_constant<int, (NBW >= 4 ? NBW - 3 : 0)>{});
     else pipeline(std::integral_constant<int, 0>{});
-    if (tid == 0) p.row_counts[blockIdx.x] = computed;
+    // the workgroup's count: the sum over its waves
+    __shared__ int wave_counts[DR_NT / 64];
+    if (lane == 0) wave_counts[wave] = computed;
+    __syncthreads();
+    if (tid == 0) {
+        int total = 0;
+#pragma unroll
+        for (int w = 0; w < DR_NT / 64; ++w) total += wave_counts[w];
+        p.row_counts[blockIdx.x] = total;
+    }
 }
 
 template <int NBW>
@@ -369,9 +396,9 @@ hipError_t launch_bwd_data_rows(const DataRowsParams& p, int grid, int nbw, hipS
     // the rings as the planner laid them out
     const int wseg = p.W < DR_WT ? p.W : DR_WT;
     if (p.depth < 1 || p.depth > 8 || p.nslot != p.depth + 3 || p.slot_bytes != ((wseg + 15) / 16 * 16 + 2 + 7) / 8 * 1024 ||
-        p.mslot_bytes != (wseg * 8 + 255) / 256 * 256 || p.mask_off != p.nslot * p.slot_bytes ||
-        p.mask_off + (p.depth + 1) * p.mslot_bytes > kDataRowsLds || p.div_nslot.d != (uint32_t)p.nslot ||
-        p.div_nmslot.d != (uint32_t)(p.depth + 1))
+        p.mslot_bytes != (wseg * 8 + 1023) / 1024 * 1024 || p.mask_off != p.nslot * p.slot_bytes ||
+        p.mask_off + (p.depth + 2) * p.mslot_bytes > kDataRowsLds || p.div_nslot.d != (uint32_t)p.nslot ||
+        p.div_nmslot.d != (uint32_t)(p.depth + 2))
         return hipErrorInvalidValue;
     if (nbw < (((p.W < DR_WT ? p.W : DR_WT) + 15) / 16 + 3) / 4) return hipErrorInvalidValue;
     switch (nbw) {

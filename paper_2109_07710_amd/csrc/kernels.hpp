@@ -59,14 +59,14 @@ struct DataRowsParams {
     const void* wt;          // [9][64][64]: filters by tap, input channel c, then k
     void* dx;                // [N*H*W][64]
     const uint32_t* mask;    // packed footprint of X, or null (dense)
-    int32_t* row_counts;     // [grid] pixels of the rows each workgroup computed
+    int32_t* row_counts;     // [grid] pixels computed per workgroup, counted once per channel half
     int N, H, W, P, Q, pad_h, pad_w;
     int nseg, rows_per_strip, nrows;   // nrows = N*H
     int skip;                // masked: rows whose footprint is empty skip the matrix work
     uint32_t dy_bytes, dx_bytes, mask_bytes, wt_bytes;
     FastDiv div_h;           // output row -> image
     // rings in LDS: depth steps of prefetch, nslot = depth + 3 dY rows of
-    // slot_bytes, then (from mask_off) depth + 1 footprint rows of mslot_bytes
+    // slot_bytes, then (from mask_off) depth + 2 footprint rows of mslot_bytes
     int depth, nslot, slot_bytes, mslot_bytes, mask_off;
     FastDiv div_nslot, div_nmslot;
 };

@@ -97,13 +97,13 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out, bool no_split,
         const int wseg = d->W < kDataRowsSegment ? d->W : kDataRowsSegment;
         p.rows_nbw = ((wseg + 15) / 16 + 3) / 4;
         // the deepest prefetch (at most 8 steps) whose rings fit the LDS:
-        // depth + 3 dY rows and depth + 1 footprint rows
+        // depth + 3 dY rows and depth + 2 footprint rows
         // a slot holds the 16-column blocks' rows and the two halo columns
         p.rows_slot = ((wseg + 15) / 16 * 16 + 2 + 7) / 8 * 1024;
-        p.rows_mslot = (wseg * 8 + 255) / 256 * 256;
+        p.rows_mslot = (wseg * 8 + 1023) / 1024 * 1024;   // whole 1 KB copies of 16-byte pieces
         p.rows_depth = 8;
         while (p.rows_depth > 1 &&
-               (p.rows_depth + 3) * p.rows_slot + (p.rows_depth + 1) * p.rows_mslot > kDataRowsLds)
+               (p.rows_depth + 3) * p.rows_slot + (p.rows_depth + 2) * p.rows_mslot > kDataRowsLds)
             --p.rows_depth;
         size_t cur = 0;
         p.header = take(&cur, 256);

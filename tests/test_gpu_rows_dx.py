@@ -116,20 +116,44 @@ def test_rows_dx_strips_cross_images():
     _check(desc, t, dx, True)
 
 
+def _computed_pixels(live, W):
+    """Pixels the row-window kernel computes: per output row, each of its 8
+    waves (2 channel halves x 4 column groups of 16-column blocks) runs its
+    matrix work unless all its outputs are dead; a pixel counts once per
+    channel half, the total is halved.  live: bool [rows, W, 64]."""
+    nwb = (W + 15) // 16
+    base, rem = divmod(nwb, 4)
+    total = 0
+    for wg in range(4):
+        cnt = base + (1 if wg < rem else 0)
+        b0 = wg * base + min(wg, rem)
+        c0, c1 = 16 * b0, min(16 * (b0 + cnt), W)
+        if c1 <= c0:
+            continue
+        for half in range(2):
+            any_live = live[:, c0:c1, 32 * half:32 * half + 32].any(axis=(1, 2))
+            total += int(any_live.sum()) * (c1 - c0)
+    return total // 2
+
+
 def test_rows_dx_dead_rows_skipped():
-    """Output rows whose footprint is empty skip the matrix work and are
-    +0.0; the statistics count only the computed rows; NO_SKIP computes them
-    (same values)."""
+    """A wave whose outputs in a row are all dead skips that row's matrix
+    work (those outputs are +0.0); the statistics count only the computed
+    pixels; NO_SKIP computes everything (same values)."""
     def kill(x):
         x[0, 2:5] = -1.0     # three dead rows of image 0
         x[1, :, :] = -1.0    # image 1 entirely dead
-        x[2, 7, :100] = -1.0 # a row with a live tail: computed
+        x[2, 7, :100] = -1.0 # a row with a live tail: only the waves over columns 80.. compute
+        x[2, 3, :, :32] = -1.0   # one channel half dead along a row
 
     desc, t = _layer(3, 9, 130, (1, 1), seed=11, dead_rows=kill)
     _case("row-window dX dead rows N=3 H=9 W=130")
     dx, st = _run(desc, t, True)
     _check(desc, t, dx, True)
-    assert st.rows_live == (3 * 9 - 3 - 9) * 130
+    live = (t["x"].float().numpy() > 0).reshape(3 * 9, 130, 64)
+    expect = _computed_pixels(live, 130)
+    assert expect < (3 * 9 - 3 - 9) * 130
+    assert st.rows_live == expect
     dx2, st2 = _run(desc, t, True, cb.CBW_FLAG_NO_SKIP)
     assert torch.equal(dx.view(torch.int16), dx2.view(torch.int16))
     assert st2.rows_live == st2.rows_total
