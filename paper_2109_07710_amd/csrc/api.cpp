@@ -476,12 +476,17 @@ static OccParams weight_occ_params(const cbw_conv_desc* desc, const WeightPlan& 
     op.BNk = plan.bk;
     op.ktiles = plan.ktiles;
     op.nchunks = plan.nchunks;
-    // chunks per workgroup: about four (pixel, k tile) pairs per thread
-    // (one with X-window liveness, whose test loops over taps), within the
-    // per-chunk flag arrays (1024 entries each)
+    op.div_chunk = make_fastdiv((uint32_t)plan.chunk);
+    op.div_ktiles = make_fastdiv((uint32_t)plan.ktiles);
+    // chunks per workgroup: enough workgroups for two per CU, at most about
+    // eight (pixel, k tile) pairs per thread (one with X-window liveness,
+    // whose test loops over taps), within the per-chunk flag arrays (1024
+    // entries each)
     const int ncombo = x_skip ? plan.tgroups * plan.ctiles : 1;
     const int per_chunk = plan.chunk * plan.ktiles;
-    op.cpw = std::max(1, std::min((x_skip ? 256 : 1024) / per_chunk, 1024 / std::max(plan.ktiles, ncombo)));
+    const int spread = (plan.nchunks + 2 * CBW_NUM_CUS - 1) / (2 * CBW_NUM_CUS);
+    op.cpw = std::max(1, std::min(std::min((x_skip ? 256 : 2048) / per_chunk, spread),
+                                  1024 / std::max(plan.ktiles, ncombo)));
     op.dtype = desc->dtype;
     if (x_skip) {
         op.xbits = xbits;

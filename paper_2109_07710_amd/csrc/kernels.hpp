@@ -119,6 +119,7 @@ struct OccParams {
     int N, H, W, C, P, Q, S, RS, stride_h, stride_w, pad_h, pad_w;
     int tpg, tgroups, ctiles, ctw;   // taps per group, groups, channel tiles, channels per tile
     FastDiv div_q, div_p;
+    FastDiv div_chunk, div_ktiles;   // pixel -> chunk, pair -> pixel
 };
 
 // Per-element data gradient on the vector ALUs (bf16, NHWC, KRSC filters).

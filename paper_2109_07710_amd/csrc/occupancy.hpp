@@ -37,11 +37,11 @@ __device__ __forceinline__ uint32_t vec_bits(const uint4& v, bool relu)
 // Workgroup `block` of the occupancy pass (256 threads):
 // occ[chunk][kt] = 1 iff dY has a non-zero in pixels of the chunk and
 // channels of k-tile kt (from the packed footprint when given: one (pixel,
-// k-tile) pair per thread and round, four rounds' loads issued together, the
-// tile's words read as vectors when the k-tile is 256 wide and K a multiple
-// of 256).  A workgroup covers p.cpw consecutive chunks, about four pairs
-// per thread, so narrow layers do not launch one nearly idle workgroup per
-// 64-pixel chunk.
+// k-tile) pair per thread and round, eight rounds' loads issued together,
+// the tile's words read as one or two vectors when K is a multiple of the
+// tile width).  A workgroup covers p.cpw consecutive chunks, about four
+// pairs per thread, so narrow layers do not launch one nearly idle workgroup
+// per 64-pixel chunk.
 __device__ __forceinline__ void occupancy_block(const OccParams& p, int block)
 {
     __shared__ int flags[1024];                  // [chunk of the group][k tile]
@@ -52,33 +52,45 @@ __device__ __forceinline__ void occupancy_block(const OccParams& p, int block)
     for (int i = threadIdx.x; i < nloc * p.ktiles; i += blockDim.x) flags[i] = 0;
     __syncthreads();
     if (p.bits) {
-        const bool vec = p.BNk == 256 && (p.K & 255) == 0;
+        // whole 16-, 8- or 32-byte aligned word runs per (pixel, k tile) when
+        // K is a multiple of the tile width (256, 128 or 64 channels)
+        const int vw = (p.K % p.BNk) == 0 ? (p.BNk == 256 ? 8 : p.BNk == 128 ? 4 : p.BNk == 64 ? 2 : 0) : 0;
         const int pairs = npx * p.ktiles;
         auto pair_any = [&](int i) -> bool {
-            const int j = i / p.ktiles, kt = i - j * p.ktiles;   // pixel of the group, k tile
+            const int j = (int)fdiv((uint32_t)i, p.div_ktiles), kt = i - j * p.ktiles;   // pixel of the group, k tile
             const int64_t base = (int64_t)(px0 + j) * p.K;
             const int lo = kt * p.BNk, hi = min(p.K, lo + p.BNk);
-            if (vec) {
-                const uint4* w = reinterpret_cast<const uint4*>(p.bits + ((base + lo) >> 5));
+            const uint32_t* wp = p.bits + ((base + lo) >> 5);
+            if (vw == 8) {
+                const uint4* w = reinterpret_cast<const uint4*>(wp);
                 const uint4 a = w[0], b = w[1];
                 return ((a.x | a.y | a.z | a.w) | (b.x | b.y | b.z | b.w)) != 0;
             }
+            if (vw == 4) {
+                const uint4 a = *reinterpret_cast<const uint4*>(wp);
+                return (a.x | a.y | a.z | a.w) != 0;
+            }
+            if (vw == 2) {
+                const uint2 a = *reinterpret_cast<const uint2*>(wp);
+                return (a.x | a.y) != 0;
+            }
             return any_bits(p.bits, base + lo, base + hi);
         };
-        // four (pixel, k tile) pairs per thread and round, their loads issued together
-        for (int i0 = threadIdx.x; i0 < pairs; i0 += 4 * blockDim.x) {
-            bool any[4];
+        // eight (pixel, k tile) pairs per thread and round, their loads
+        // issued together; consecutive threads read consecutive runs
+        for (int i0 = threadIdx.x; i0 < pairs; i0 += 8 * blockDim.x) {
+            bool any[8];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < 8; ++u) {
                 const int i = i0 + u * blockDim.x;
                 any[u] = i < pairs && pair_any(i);
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < 8; ++u) {
                 const int i = i0 + u * blockDim.x;
                 if (any[u]) {
-                    const int j = i / p.ktiles, kt = i - j * p.ktiles;
-                    flags[(j / p.chunk) * p.ktiles + kt] = 1;   // every writer stores 1
+                    const int j = (int)fdiv((uint32_t)i, p.div_ktiles), kt = i - j * p.ktiles;
+                    flags[(int)fdiv((uint32_t)j, p.div_chunk) * p.ktiles + kt] = 1;   // every writer stores 1
                 }
             }
         }
@@ -92,7 +104,7 @@ __device__ __forceinline__ void occupancy_block(const OccParams& p, int block)
             const uint4 v = v4[i];
             const uint32_t b = p.dtype == 1 ? vec_bits<uint16_t>(v, false) : vec_bits<float>(v, false);
             const int j = i / vpp;
-            if (b) flags[(j / p.chunk) * p.ktiles + ((i - j * vpp) * E) / p.BNk] = 1;
+            if (b) flags[(int)fdiv((uint32_t)j, p.div_chunk) * p.ktiles + ((i - j * vpp) * E) / p.BNk] = 1;
         }
     }
     __syncthreads();
@@ -136,7 +148,7 @@ __device__ __forceinline__ void occupancy_block(const OccParams& p, int block)
                     any = any_bits(p.xbits, base + lo, base + hi);
                 }
             }
-            if (any) xflags[(j / p.chunk) * ncombo + combo] = 1;   // every writer stores 1
+            if (any) xflags[(int)fdiv((uint32_t)j, p.div_chunk) * ncombo + combo] = 1;   // every writer stores 1
         }
         __syncthreads();
         for (int i = threadIdx.x; i < nloc * ncombo; i += blockDim.x)
