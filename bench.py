@@ -664,8 +664,23 @@ def layer_timing(cb, torch, spec, steps, warmup):
     ws_m = cb.workspace(desc, cb.CBW_OP_BWD_DATA_MASKED, dev)
     ws_d = cb.workspace(desc, cb.CBW_OP_BWD_DATA, dev)
     ws_w = cb.workspace(desc, cb.CBW_OP_BWD_WEIGHT, dev)
+    ws_b = cb.workspace(desc, cb.CBW_OP_BWD_BOTH, dev)
+    b_off = cb.both_weight_offset(desc)
+    masked_dx = spec.need_dx and spec.masked
 
+    # The step of the main line: one conv_bwd_sparse call (dX masked where
+    # the layer's data gradient is, dense where it is not, none for a first
+    # layer); the dense step is the same call without footprints and NO_SKIP.
     def sparse():
+        cb.conv_bwd_sparse(desc, x, dy, w, xm if masked_dx else None, dym, dx if spec.need_dx else None, dw,
+                           ws_b, 0)
+
+    def dense():
+        cb.conv_bwd_sparse(desc, x, dy, w, None, None, dx if spec.need_dx else None, dw, ws_b,
+                           cb.CBW_FLAG_NO_SKIP)
+
+    # the same step through the separate entry points
+    def separate():
         if spec.need_dx:
             if spec.masked:
                 cb.conv_bwd_data_masked(desc, dy, w, xm, dx, ws_m, 0)
@@ -681,11 +696,6 @@ def layer_timing(cb, torch, spec, steps, warmup):
             else:
                 cb.conv_bwd_data(desc, dy, w, dx, ws_d)
         cb.conv_bwd_weight_sparse_x(desc, x, dy, xm, dym, dw, ws_w, 0)
-
-    def dense():
-        if spec.need_dx:
-            cb.conv_bwd_data(desc, dy, w, dx, ws_d)
-        cb.conv_bwd_weight_sparse(desc, x, dy, None, dw, ws_w, cb.CBW_FLAG_NO_SKIP)
 
     def tm(fn):
         torch.cuda.synchronize()
@@ -703,20 +713,23 @@ def layer_timing(cb, torch, spec, steps, warmup):
         sparse()
         sparse_x()
         dense()
+        separate()
     import numpy as np
-    rr = alternate({"s": sparse, "x": sparse_x, "d": dense}, tm, 3)
-    ms_s, ms_x, ms_d = (float(np.median(rr[k])) for k in ("s", "x", "d"))
+    rr = alternate({"s": sparse, "x": sparse_x, "d": dense, "p": separate}, tm, 3)
+    ms_s, ms_x, ms_d, ms_p = (float(np.median(rr[k])) for k in ("s", "x", "d", "p"))
     sparse_x()
     st_x = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws_w)
     work_x = cb.cbw_read_weight_work(desc, ws_w)
+    separate()
     sparse()
     torch.cuda.synchronize()
-    work = cb.cbw_read_weight_work(desc, ws_w)
+    work = cb.cbw_read_weight_work(desc, ws_b[b_off:])
     rec = {"layer": spec.name, "N": spec.N, "C": spec.C, "K": spec.K, "H": spec.H, "W": spec.W, "R": spec.R,
            "masked_dx": bool(spec.need_dx and spec.masked), "need_dx": bool(spec.need_dx),
            "x_density": round(float((x > 0).float().mean().item()), 4),
            "dy_density": round(float((dy != 0).float().mean().item()), 4),
-           "sparse_ms": round(ms_s, 4), "dense_ms": round(ms_d, 4), "speedup_vs_dense": round(ms_d / ms_s, 4)}
+           "sparse_ms": round(ms_s, 4), "dense_ms": round(ms_d, 4), "speedup_vs_dense": round(ms_d / ms_s, 4),
+           "separate_calls_ms": round(ms_p, 4)}
     f = spec.dense_flops()
     nflops = f * (2 if spec.need_dx else 1)
     rec["dense_equiv_tflops"] = round(nflops / (ms_s * 1e-3) / 1e12, 2)
@@ -735,9 +748,9 @@ def layer_timing(cb, torch, spec, steps, warmup):
         useful += (2 * int(torch.count_nonzero(x > 0).item()) * spec.K * spec.R * spec.S if spec.masked else f)
     rec["useful_tflops"] = round(useful / (ms_s * 1e-3) / 1e12, 2)
     if spec.need_dx and spec.masked:
-        st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_DATA_MASKED, ws_m)
+        st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_DATA_MASKED, ws_b)
         rec["dx_rows_executed"] = round(st.rows_live / st.rows_total, 4)
-    st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws_w)
+    st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws_b[b_off:])
     rec["dw_blocks_executed"] = round(1.0 - st.blocks_skipped / max(st.blocks_total, 1), 4)
     rec["dw_split_balance"] = split_balance(work)
     # the variant whose weight gradient also skips all-zero X blocks
