@@ -61,6 +61,11 @@ def parse():
     ap.add_argument("--no-stack", action="store_true", help="skip the VGG-16 stack timing")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 256 MiB device copy three times (reference for HBM byte counters)")
+    ap.add_argument("--trace-layer", default=None, metavar="NAME",
+                    help="instead of the main line, run one named layer's combined sparse and dense steps in "
+                         "alternating rounds of --steps steps (after --warmup of each), a small fill kernel "
+                         "marking every round, for rocprofv3 kernel traces and counter passes; prints the "
+                         "round order and per-round times as JSON")
     return ap.parse_args()
 
 
@@ -76,6 +81,9 @@ def main():
         sys.exit(2)
     if args.sweep:
         run_sweep(args)
+        return
+    if args.trace_layer:
+        trace_layer(args)
         return
 
     import numpy as np
@@ -892,6 +900,66 @@ def useful_products(x, dy, spec):
             # output (h, w) reads source (h + pad - r, w + pad - s)
             tot += pad[:, 2 * spec.pad - r:2 * spec.pad - r + spec.H, 2 * spec.pad - s:2 * spec.pad - s + spec.W]
     return (tot * live_c).sum().item()
+
+
+def trace_layer(args):
+    """One layer's combined sparse step (footprints as the workload defines
+    them) and dense step, in alternating rounds: round r runs `--steps`
+    calls of one step after a one-element fill kernel (the marker a trace
+    parser splits phases at).  Layers: the configuration-2 layer, the three
+    bottleneck layers, the 13 VGG-16 layers."""
+    import numpy as np
+    import torch
+    import paper_2109_07710_amd as cb
+    import workloads as wl
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    specs = {s.name: s for s in wl.config2() + wl.config3() + wl.config5()}
+    if args.trace_layer not in specs:
+        print("unknown layer %r; one of: %s" % (args.trace_layer, ", ".join(sorted(specs))), file=sys.stderr)
+        sys.exit(2)
+    spec = specs[args.trace_layer]
+    t = wl.draw_on_device(spec, dev) if spec.config_id == 5 else {k: v.to(dev) for k, v in wl.draw(spec).items()}
+    x, w, dy = t["x"], t["w"], t["dy"]
+    desc = cb.ConvDesc.make(spec.N, spec.C, spec.H, spec.W, spec.K, spec.R, spec.S, spec.stride, spec.pad)
+    xm = torch.empty(max(cb.cbw_mask_words(desc), 1), dtype=torch.int32, device=dev)
+    dym = torch.empty(max(cb.cbw_dy_mask_words(desc), 1), dtype=torch.int32, device=dev)
+    cb.cbw_relu_mask_pack(desc, x, xm)
+    cb.cbw_nonzero_mask_pack(desc.dtype, dy.numel(), dy, dym)
+    dx = torch.empty_like(x) if spec.need_dx else None
+    dw = torch.empty((spec.K, spec.R, spec.S, spec.C), dtype=torch.float32, device=dev)
+    ws = cb.workspace(desc, cb.CBW_OP_BWD_BOTH, dev)
+    masked_dx = spec.need_dx and spec.masked
+    steps = {"sparse": lambda: cb.conv_bwd_sparse(desc, x, dy, w, xm if masked_dx else None, dym, dx, dw, ws, 0),
+             "dense": lambda: cb.conv_bwd_sparse(desc, x, dy, w, None, None, dx, dw, ws, cb.CBW_FLAG_NO_SKIP)}
+    marker = torch.empty(1, device=dev)
+    for _ in range(args.warmup):
+        steps["sparse"]()
+        steps["dense"]()
+    torch.cuda.synchronize()
+    order, times = [], {k: [] for k in steps}
+    for r in range(args.rounds):
+        for name in (("sparse", "dense") if r % 2 == 0 else ("dense", "sparse")):
+            marker.fill_(float(len(order)))
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(args.steps):
+                steps[name]()
+            b.record()
+            torch.cuda.synchronize()
+            order.append(name)
+            times[name].append(a.elapsed_time(b) / args.steps)
+    if args.copy_calibration:
+        # the byte counters' reference: a plain copy of 256 MiB, three times
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+    print(json.dumps({"trace_layer": spec.name, "steps_per_round": args.steps, "order": order,
+                      "ms_per_step_median": {k: round(float(np.median(v)), 4) for k, v in times.items()}}),
+          flush=True)
 
 
 def run_sweep(args):
