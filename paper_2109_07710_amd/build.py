@@ -20,7 +20,7 @@ PEAKS_LIB = os.path.join(HERE, "libcbwpeaks.so")
 PEAKS_SOURCES = ["peaks.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["api.cpp", "plan.cpp", "bwd_data.hip", "bwd_data_rows.hip", "bwd_weight.hip", "mask_kernels.hip", "elementwise.hip", "layout.hip"]
+SOURCES = ["api.cpp", "plan.cpp", "bwd_data.hip", "bwd_data_rows.hip", "bwd_data_pw.hip", "bwd_weight.hip", "mask_kernels.hip", "elementwise.hip", "layout.hip"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result"]
 DEVICE = ["-x", "hip", "--offload-arch=gfx950",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

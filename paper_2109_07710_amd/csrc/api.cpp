@@ -46,6 +46,7 @@ bool tiles_consistent()
     for (int t = 0; t < kDataTileCount; ++t)
         if (data_tile_channels(t) != kDataTiles[t].bm || data_tile_pixels(t) != kDataTiles[t].bn) return false;
     if (data_rows_segment() != kDataRowsSegment) return false;
+    if (data_pw_waves_per_group() != kDataPwWaves) return false;
     return weight_tile_channels() == kWeightTileC && weight_tile_k() == kWeightTileK &&
            compact_block_pixels() == kCompactBlock && weight_chunk(CBW_BF16) == weight_chunk_px(CBW_BF16) &&
            weight_chunk(CBW_F32) == weight_chunk_px(CBW_F32);
@@ -150,6 +151,29 @@ DataRowsParams data_rows_params(const cbw_conv_desc* d, const DataPlan& plan, co
     return p;
 }
 
+// Kernel parameters of the pointwise data gradient (NHWC tensors).
+DataPwParams data_pw_params(const cbw_conv_desc* d, const DataPlan& plan, const void* dY, const void* wt,
+                            const uint32_t* x_mask, void* dX, void* ws, bool skip)
+{
+    DataPwParams p{};
+    p.dy = dY;
+    p.wt = wt;
+    p.dx = dX;
+    p.mask = x_mask;
+    p.counts = at<int32_t>(ws, plan.row_counts);
+    p.npix = (int)plan.npix;
+    p.C = d->C;
+    p.K = d->K;
+    p.nblk = (int)((plan.npix + 15) / 16);
+    p.bpw = plan.pw_bpw;
+    p.skip = x_mask && skip ? 1 : 0;
+    const int64_t esz = elem_bytes(d->dtype);
+    p.dy_bytes = (uint32_t)(plan.npix * d->K * esz);
+    p.dx_bytes = (uint32_t)(plan.npix * d->C * esz);
+    p.mask_bytes = (uint32_t)((plan.npix * d->C + 31) / 32 * 4);
+    return p;
+}
+
 // compaction needs at most kGatherMaxGroups channel groups; wider layers
 // keep the footprint select without it
 bool data_gathers(const DataPlan& plan, bool masked, uint32_t flags)
@@ -233,6 +257,13 @@ int run_bwd_data(const cbw_conv_desc* desc, const void* dY, const void* W, const
                                                    !(flags & CBW_FLAG_NO_SKIP));
         if ((e = launch_bwd_data_rows(rp, plan.rows_grid, plan.rows_nbw, s, prof_events(0))) != hipSuccess)
             return hip_status(e);
+    } else if (plan.pw) {
+        e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, 1, desc->w_layout == CBW_KRSC, header, MODE_PW,
+                             nullptr, s);
+        if (e != hipSuccess) return hip_status(e);
+        const DataPwParams pp = data_pw_params(desc, plan, dY, wt, masked ? x_mask : nullptr, dX, ws,
+                                               !(flags & CBW_FLAG_NO_SKIP));
+        if ((e = launch_bwd_data_pw(pp, plan.pw_grid, s, prof_events(0))) != hipSuccess) return hip_status(e);
     } else {
         DataParams p;
         CompactParams cp;
@@ -642,13 +673,16 @@ static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY
                           flags & CBW_FLAG_NO_SKIP, stream);
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const bool gather = !dplan.rows && data_gathers(dplan, masked, flags);
-    const int mode = dplan.rows ? MODE_ROWS : !masked ? MODE_DENSE : (gather ? MODE_GATHER : MODE_SELECT);
+    const bool tiled = !dplan.rows && !dplan.pw;   // the tiled GEMM (else a dedicated kernel)
+    const bool gather = tiled && data_gathers(dplan, masked, flags);
+    const int mode = dplan.rows ? MODE_ROWS
+                     : dplan.pw ? MODE_PW
+                                : (!masked ? MODE_DENSE : (gather ? MODE_GATHER : MODE_SELECT));
     int* header = at<int>(ws, dplan.header);
     void* wt = at<void>(ws, dplan.wt);
     DataParams dp{};
     CompactParams cp;
-    if (!dplan.rows) data_gemm_params(desc, dplan, dY, wt, x_mask, dX, ws, gather, false, &dp, &cp);
+    if (tiled) data_gemm_params(desc, dplan, dY, wt, x_mask, dX, ws, gather, false, &dp, &cp);
     OccParams op{};
     if (skip) op = weight_occ_params(desc, wplan, dY, dy_mask, x_skip, x_mask, wws);
     hipError_t e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S,
@@ -658,6 +692,9 @@ static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY
     if (dplan.rows) {
         const DataRowsParams rp = data_rows_params(desc, dplan, dY, wt, x_mask, dX, ws, skip);
         e = launch_bwd_data_rows(rp, dplan.rows_grid, dplan.rows_nbw, s, prof_events(0));
+    } else if (dplan.pw) {
+        const DataPwParams pp = data_pw_params(desc, dplan, dY, wt, x_mask, dX, ws, skip);
+        e = launch_bwd_data_pw(pp, dplan.pw_grid, s, prof_events(0));
     } else {
         e = launch_bwd_data(desc->dtype, mode, dp, s, prof_events(0), false);
     }
@@ -678,7 +715,7 @@ static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY
         rp.G = splitk_reduce_group(wplan.nparts, n4);
         rp.blocks = (int)((n4 * rp.G + 255) / 256);
     }
-    const bool dx_reduce = !dplan.rows && (mode == MODE_GATHER || dplan.split > 1);
+    const bool dx_reduce = tiled && (mode == MODE_GATHER || dplan.split > 1);
     return hip_status(launch_bwd_reduce(desc->dtype, mode, dp, dx_reduce, rp, s));
 }
 
@@ -817,6 +854,19 @@ int cbw_read_stats(const cbw_conv_desc* desc, int op, const void* workspace, siz
                 for (int i = 0; i < n; ++i) live += buf[i];
             }
             r.rows_live = live / 2 * plan.groups;   // each pixel is counted by its two channel-half waves
+        } else if (plan.pw && header == MODE_PW) {
+            // pixels of the 16-pixel blocks each workgroup computed (dead blocks skipped)
+            int32_t buf[256];
+            int64_t live = 0;
+            const int32_t* slots = at<int32_t>(const_cast<void*>(workspace), plan.row_counts);
+            for (int i0 = 0; i0 < plan.pw_grid; i0 += 256) {
+                const int n = plan.pw_grid - i0 < 256 ? plan.pw_grid - i0 : 256;
+                e = hipMemcpyAsync(buf, slots + i0, n * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+                if (e == hipSuccess) e = hipStreamSynchronize(s);
+                if (e != hipSuccess) return hip_status(e);
+                for (int i = 0; i < n; ++i) live += buf[i];
+            }
+            r.rows_live = live * plan.groups;
         } else if (op == CBW_OP_BWD_DATA_MASKED && header == MODE_GATHER) {
             int32_t counts[64];
             int64_t live = 0;
@@ -875,7 +925,7 @@ int cbw_read_live_lists(const cbw_conv_desc* desc, const void* workspace, size_t
     if (workspace_bytes < plan.total) return CBW_ERR_WORKSPACE;
     hipStream_t s = static_cast<hipStream_t>(stream);
     void* ws = const_cast<void*>(workspace);
-    if (plan.rows) return CBW_ERR_UNSUPPORTED;   // the row-window kernel lists nothing
+    if (plan.rows || plan.pw) return CBW_ERR_UNSUPPORTED;   // the row-window and pointwise kernels list nothing
     int32_t n = 0;
     hipError_t e = hipMemcpyAsync(&n, at<int32_t>(ws, plan.counts) + group, sizeof(int32_t),
                                   hipMemcpyDeviceToHost, s);

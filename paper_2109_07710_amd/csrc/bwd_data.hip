@@ -240,7 +240,10 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     __shared__ uint4 Bs[2][BN * CH];
     __shared__ int pix_s[BN];
     constexpr bool SEL = MODE == MODE_SELECT || MODE == MODE_GATHER;   // footprint select in the epilogue
-    __shared__ uint32_t msk_s[SEL ? BN * (BM / 32) : 1];
+    // footprint words, one padded row of BM/32 + 1 words per pixel row: the
+    // epilogue's 16 lanes that read one word column hit 16 different banks
+    constexpr int MSTR = BM / 32 + 1;
+    __shared__ uint32_t msk_s[SEL ? BN * MSTR : 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -554,7 +557,10 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
 #pragma unroll
         for (int u = 0; u < MI; ++u) {
             const int i = tid + u * NT;
-            if (i < MW) msk_s[i] = mwords[u];
+            if (i < MW) {
+                const int pr = i / (BM / 32), wi = i - pr * (BM / 32);
+                msk_s[pr * MSTR + wi] = mwords[u];
+            }
         }
         __syncthreads();
     }
@@ -591,7 +597,7 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
             if (j >= fnw) break;   // uniform: the wave's column has fnw blocks
             const int pr = wrow0 + j * 16 + (lane & 15);
 #pragma unroll
-            for (int w = 0; w < MWJ; ++w) ew[j][w] = msk_s[pr * (BM / 32) + (wm * TM) / 32 + w];
+            for (int w = 0; w < MWJ; ++w) ew[j][w] = msk_s[pr * MSTR + (wm * TM) / 32 + w];
         }
     }
     // Forward: ReLU, rounding to the output type, and the footprint of the

@@ -12,9 +12,11 @@ namespace cbw {
 // convolution (flipped filters, padding R-1-pad, stride 1) with a ReLU
 // epilogue that also emits the output's footprint bits.
 enum { MODE_DENSE = 0, MODE_SELECT = 1, MODE_GATHER = 2, MODE_FWD = 3 };
-// Workspace header stamp of a data-gradient call served by the row-window
-// kernel (bwd_data_rows.hip) instead of the tiled GEMM.
+// Workspace header stamps of a data-gradient call served by the row-window
+// kernel (bwd_data_rows.hip) or the pointwise kernel (bwd_data_pw.hip)
+// instead of the tiled GEMM.
 constexpr int MODE_ROWS = 4;
+constexpr int MODE_PW = 5;
 
 // Optional timing events attached to the dispatch of a GEMM kernel (both
 // may be null): they record the kernel's own begin and end.
@@ -72,6 +74,22 @@ struct DataRowsParams {
 };
 int data_rows_segment();
 hipError_t launch_bwd_data_rows(const DataRowsParams& p, int grid, int nbw, hipStream_t stream, const ProfEvents& ev);
+
+// Pointwise data gradient (1 x 1, stride 1, no padding, bf16, NHWC, C and K
+// in {64, 128, 256}, C * K <= 16384): wave w of the grid owns the 16-pixel
+// blocks [w * bpw, (w + 1) * bpw).
+struct DataPwParams {
+    const void* dy;          // [npix][K]
+    const void* wt;          // [C][K]
+    void* dx;                // [npix][C]
+    const uint32_t* mask;    // packed footprint of X, or null (dense)
+    int32_t* counts;         // [grid] pixels of the blocks computed per workgroup
+    int npix, C, K, nblk, bpw;
+    int skip;                // masked: blocks whose footprint is empty skip the matrix work
+    uint32_t dy_bytes, dx_bytes, mask_bytes;
+};
+int data_pw_waves_per_group();
+hipError_t launch_bwd_data_pw(const DataPwParams& p, int grid, hipStream_t stream, const ProfEvents& ev);
 
 struct CompactParams {
     const uint32_t* mask;    // packed footprint, NHWC bit order

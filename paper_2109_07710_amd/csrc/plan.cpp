@@ -74,11 +74,44 @@ bool data_rows_eligible(const cbw_conv_desc* d)
            d->K == 64;
 }
 
+bool data_pw_eligible(const cbw_conv_desc* d)
+{
+    auto ok = [](int c) { return c == 64 || c == 128 || c == 256; };
+    return d->dtype == CBW_BF16 && d->R == 1 && d->S == 1 && d->stride_h == 1 && d->stride_w == 1 &&
+           d->pad_h == 0 && d->pad_w == 0 && ok(d->C) && ok(d->K) && d->C * d->K <= 16384;
+}
+
 int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out, bool no_split, bool allow_rows)
 {
     int st = validate_desc(d);
     if (st != CBW_OK) return st;
     DataPlan p;
+    if (allow_rows && data_pw_eligible(d)) {
+        // as many resident waves as give every wave the same whole number of
+        // 16-pixel blocks (the last wave takes the rest)
+        p.tile = data_tile_index(d->C);
+        p.bm = kDataTiles[p.tile].bm;
+        p.bn = kDataTiles[p.tile].bn;
+        p.npix = (int64_t)d->N * d->H * d->W;
+        p.groups = (d->C + p.bm - 1) / p.bm;
+        p.pw = true;
+        const int64_t nblk = (p.npix + 15) / 16;
+        p.pw_bpw = (int)((nblk + kDataPwMaxWaves - 1) / kDataPwMaxWaves);
+        const int64_t waves = (nblk + p.pw_bpw - 1) / p.pw_bpw;
+        p.pw_grid = (int)((waves + kDataPwWaves - 1) / kDataPwWaves);
+        size_t cur = 0;
+        p.header = take(&cur, 256);
+        p.wt = take(&cur, (size_t)d->K * d->C * elem_bytes(d->dtype));
+        p.row_counts = take(&cur, (size_t)p.pw_grid * 4);
+        if (d->act_layout == CBW_NCHW) {
+            p.t_dy = take(&cur, (size_t)d->N * d->P * d->Q * d->K * elem_bytes(d->dtype));
+            p.t_dx = take(&cur, (size_t)p.npix * d->C * elem_bytes(d->dtype));
+            if (masked) p.t_mask = take(&cur, ((size_t)p.npix * d->C + 31) / 32 * 4);
+        }
+        p.total = cur;
+        *out = p;
+        return CBW_OK;
+    }
     if (allow_rows && data_rows_eligible(d)) {
         // one workgroup per CU: strips of consecutive output rows, as many
         // as make the segments times the strips fill the CUs once

@@ -42,6 +42,11 @@ struct DataPlan {
     bool rows = false;
     int rows_grid = 0, rows_per_strip = 0, rows_nseg = 0, rows_nbw = 0;
     int rows_depth = 0, rows_slot = 0, rows_mslot = 0;   // prefetch depth, ring slot bytes
+    // Pointwise kernel (data_pw_eligible): pw_grid workgroups of
+    // kDataPwWaves waves, each wave pw_bpw 16-pixel blocks; it too replaces
+    // the tiled GEMM and its compaction (per-workgroup counts in row_counts).
+    bool pw = false;
+    int pw_grid = 0, pw_bpw = 0;
     Region header, wt, blk_counts, counts, dead_flags, lists, partial, row_counts;
     // NCHW callers: NHWC copies of dY and dX and the NHWC-order footprint,
     // after every other region (the other offsets do not depend on layout)
@@ -55,6 +60,9 @@ constexpr int kDataSlots = CBW_NUM_CUS * CBW_DX_OCC;  // resident data-gradient 
 // 1, 64 input and 64 output channels (any padding, any layout: NCHW calls
 // run it on their NHWC copies).
 bool data_rows_eligible(const cbw_conv_desc* d);
+// Layers the pointwise data gradient serves: bf16, 1 x 1 filters, stride 1,
+// no padding, C and K in {64, 128, 256} with C * K <= 16384.
+bool data_pw_eligible(const cbw_conv_desc* d);
 constexpr int kDataMaxSplit = 16;
 
 // Same rule as the kernels' data_split (see common.hpp).

@@ -41,6 +41,8 @@ constexpr DataTile kDataTiles[kDataTileCount] = {{256, 224, 8, 2}, {128, 448, 4,
 // Row-window data gradient (3 x 3, stride 1, 64 channels in and out): output
 // columns per segment at most, and the LDS its two rings share (dY rows of
 // 128 bytes per column plus halo, footprint rows of 8 bytes per pixel).
+constexpr int kDataPwWaves = 4;          // waves per pointwise workgroup
+constexpr int kDataPwMaxWaves = 2048;    // resident pointwise waves (two workgroups per CU)
 constexpr int kDataRowsSegment = 224;
 constexpr int kDataRowsLds = 159744;
 

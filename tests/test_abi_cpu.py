@@ -251,10 +251,10 @@ def test_data_tiling_rejects_bad_descriptors(L):
 def test_noalloc_rejects_descriptors_beyond_its_scratch(L):
     """The built-in-scratch data gradient refuses, before any device call, a
     layer whose workspace would exceed its 32 MiB: 64 channels at 224 x 224
-    with 200 images needs 4 bytes of live list per pixel (40 MB).  (A 1 x 1
-    layer: with a 3 x 3 filter the row-window kernel would serve it, with no
-    lists.)"""
-    d = _desc(N=200, C=64, K=64, H=224, W=224, R=1, S=1, pad=(0, 0))
+    with 200 images needs 4 bytes of live list per pixel (40 MB).  (A 5 x 5
+    layer: with a 3 x 3 or 1 x 1 filter the row-window or pointwise kernel
+    would serve it, with no lists.)"""
+    d = _desc(N=200, C=64, K=64, H=224, W=224, R=5, S=5, pad=(2, 2))
     assert cb.cbw_validate_desc(d) == cb.CBW_OK
     st = L.conv_bwd_data_masked_noalloc(ctypes.byref(d), None, None, None, None, 0, None)
     assert st == cb.CBW_ERR_WORKSPACE
