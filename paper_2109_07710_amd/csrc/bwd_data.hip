@@ -236,14 +236,25 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     constexpr int BK = CH * E;     // reduction elements per step
     constexpr uint32_t ESZ = sizeof(T);
 
-    __shared__ uint4 As[2][BM * CH];
-    __shared__ uint4 Bs[2][BN * CH];
+    // the operand buffers, one array: after the main loop the bf16
+    // epilogue stages the output tile in it
+    __shared__ uint4 AB[2 * BM * CH + 2 * BN * CH];
+    uint4 (*const As)[BM * CH] = reinterpret_cast<uint4 (*)[BM * CH]>(AB);
+    uint4 (*const Bs)[BN * CH] = reinterpret_cast<uint4 (*)[BN * CH]>(AB + 2 * BM * CH);
     __shared__ int pix_s[BN];
     constexpr bool SEL = MODE == MODE_SELECT || MODE == MODE_GATHER;   // footprint select in the epilogue
     // footprint words, one padded row of BM/32 + 1 words per pixel row: the
     // epilogue's 16 lanes that read one word column hit 16 different banks
     constexpr int MSTR = BM / 32 + 1;
     __shared__ uint32_t msk_s[SEL ? BN * MSTR : 1];
+    // footprint nibble (4 channels) -> masks of two bf16 pairs, for the
+    // staged epilogue
+    __shared__ uint2 mtab[16];
+    if (SEL && sizeof(T) == 2 && threadIdx.x < 16) {
+        const uint32_t t = threadIdx.x;
+        auto half = [](uint32_t b) { return b ? 0xffffu : 0u; };
+        mtab[t] = make_uint2(half(t & 1) | (half(t & 2) << 16), half(t & 4) | (half(t & 8) << 16));
+    }
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -590,7 +601,7 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     const __amdgpu_buffer_rsrc_t rs_dx = make_rsrc(p.dx, p.dx_bytes);
     constexpr int MWJ = TM / 32 > 0 ? TM / 32 : 1;
     uint32_t ew[FN][MWJ];
-    if (mask_lds) {
+    if (sizeof(T) == 4 && mask_lds) {   // the bf16 staged epilogue reads the words itself
         static_assert(TM % 32 == 0, "wave tile must cover whole footprint words");
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
@@ -705,12 +716,59 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
             }
         }
     };
+    // bf16 with the footprint words staged (or none needed): the tile's
+    // rounded outputs go into LDS by fragment (pixel row pr of SROW bytes,
+    // 8 bytes per lane and channel block), then out by whole 16-byte row
+    // pieces, 1 KB per store instruction, with the footprint applied to
+    // each piece (one byte of a staged word, widened through mtab): every
+    // tile row is BM consecutive channels of one pixel, so each
+    // instruction writes whole 128-byte lines (the fragments' own stores
+    // would write 32-byte pieces of 16 rows each).
+    auto staged_epilogue = [&]() {
+        constexpr int SROW = 2 * BM + 16;   // padded: the 16 rows of a fragment write spread over the banks
+        static_assert(BN * SROW <= (int)sizeof(AB), "the output tile fits the operand buffers");
+        char* const stage = reinterpret_cast<char*>(AB);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            if (j >= fnw) break;   // uniform: the wave's column has fnw blocks
+            const int pr = wrow0 + j * 16 + (lane & 15);
+            const int clane = wm * TM + 4 * (lane >> 4);
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int cl = clane + i * 16;
+                const floatx4 v = acc[i][j];
+                *reinterpret_cast<uint2*>(stage + pr * SROW + 2 * cl) =
+                    make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
+            }
+        }
+        __syncthreads();
+        // lane l of a store instruction: row l / (BM / 8), 16-byte piece l % (BM / 8)
+        constexpr int PPR = BM / 8, RPI = 64 / PPR;
+        const int prow = lane / PPR, piece = lane - prow * PPR;
+        const bool cin = c0 + 8 * piece < p.C;
+        for (int r0 = wave_u * RPI; r0 < BN; r0 += NW * RPI) {
+            const int row = r0 + prow;
+            const int pix = pix_s[row];
+            const uint32_t off = (pix >= 0 && cin) ? (uint32_t)(pix * p.C + c0 + 8 * piece) * ESZ : kOOB;
+            uint4 v = *reinterpret_cast<const uint4*>(stage + row * SROW + 16 * piece);
+            if (SEL) {
+                const uint32_t byte = (msk_s[row * MSTR + piece / 4] >> (8 * (piece & 3))) & 0xffu;
+                const uint2 k0 = mtab[byte & 15u], k1 = mtab[byte >> 4];
+                v.x &= k0.x; v.y &= k0.y; v.z &= k1.x; v.w &= k1.y;
+            }
+            __builtin_amdgcn_raw_buffer_store_b128(u32x4{v.x, v.y, v.z, v.w}, rs_dx, off, 0, 0);
+        }
+    };
     if constexpr (MODE == MODE_FWD) {
         fwd_epilogue();
         return;
+    } else if constexpr (sizeof(T) == 2) {
+        if (MODE == MODE_DENSE || mask_lds) staged_epilogue();
+        else epilogue(std::false_type{});
+    } else {
+        if (MODE == MODE_DENSE || mask_lds) epilogue(std::true_type{});
+        else epilogue(std::false_type{});
     }
-    if (MODE == MODE_DENSE || mask_lds) epilogue(std::true_type{});
-    else epilogue(std::false_type{});
 }
 
 // Wt[tap][c][k] = W[k][tap][c] (KRSC) or W[k][c][tap] (KCRS).  Threads run
