@@ -267,8 +267,15 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
         }
     };
     const __amdgpu_buffer_rsrc_t rs_dx = make_rsrc(p.dx, p.dx_bytes);
-    // outputs of `row` (footprint slot ms): 4 channels of one pixel per lane;
-    // a dead output is stored as +0.0 (the bit pattern 0)
+    // outputs of `row` (footprint slot ms): a lane holds 4 channels of one
+    // pixel in each of its two 16-channel blocks; a dead output is stored
+    // as +0.0 (the bit pattern 0).  Lanes l and l + 16 (k groups 0 and 1,
+    // and 2 and 3) then swap a block each, so that every lane holds 8
+    // consecutive channels (16 bytes) and a store instruction writes
+    // 64-byte pieces of 16 pixel rows rather than 32-byte ones (the
+    // memory's write granule is 64 bytes): group g gets channels
+    // 16 (g % 2) + 8 (g / 2) .. + 7 of the wave's half.
+    const int choff = 16 * (g & 1) + 8 * (g >> 1);
     auto store = [&](int row, int ms, auto nb_tag) {
         constexpr int NB = decltype(nb_tag)::value;
         uint32_t mw[NB > 0 ? NB : 1];
@@ -276,18 +283,22 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             const int w = 16 * (b0 + j) + col;
-            const uint32_t base = (uint32_t)(((row * p.W + w0 + w) * 64 + 32 * cw + 4 * g) * 2);
+            uint2 v[2];
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb) {
-                uint2 v = outv[cb][j];
+                v[cb] = outv[cb][j];
                 if (MASKED) {
                     const uint32_t keep = mw[j] >> (16 * cb + 4 * g);
-                    v.x &= ((0u - (keep & 1u)) & 0xffffu) | ((0u - ((keep >> 1) & 1u)) & 0xffff0000u);
-                    v.y &= ((0u - ((keep >> 2) & 1u)) & 0xffffu) | ((0u - ((keep >> 3) & 1u)) & 0xffff0000u);
+                    v[cb].x &= ((0u - (keep & 1u)) & 0xffffu) | ((0u - ((keep >> 1) & 1u)) & 0xffff0000u);
+                    v[cb].y &= ((0u - ((keep >> 2) & 1u)) & 0xffffu) | ((0u - ((keep >> 3) & 1u)) & 0xffff0000u);
                 }
-                const uint32_t off = w < wn ? base + 32u * cb : kOOB;
-                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), rs_dx, off, 0, 0);
             }
+            // odd lane rows of block 0 <-> even lane rows of block 1
+            const auto sx = __builtin_amdgcn_permlane16_swap(v[0].x, v[1].x, false, false);
+            const auto sy = __builtin_amdgcn_permlane16_swap(v[0].y, v[1].y, false, false);
+            const uint32_t base = (uint32_t)(((row * p.W + w0 + w) * 64 + 32 * cw + choff) * 2);
+            __builtin_amdgcn_raw_buffer_store_b128(u32x4{sx[0], sy[0], sx[1], sy[1]}, rs_dx, w < wn ? base : kOOB, 0,
+                                                   0);
         }
     };
 
