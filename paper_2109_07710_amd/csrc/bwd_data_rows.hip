@@ -37,8 +37,6 @@ namespace {
 
 constexpr int DR_NT = 512;                 // 8 waves: 2 channel halves x 4 column groups
 constexpr int DR_WT = kDataRowsSegment;    // output columns per segment (at most)
-constexpr int DR_NU_MAX = ((DR_WT + 15) / 16 * 16 + 2 + 7) / 8;   // copy instructions per dY row (8 rows each)
-constexpr int DR_UPW = (DR_NU_MAX + 7) / 8;      // per wave
 static_assert(DR_WT * 8 <= 256 * 8, "footprint copies: one per wave at most");
 
 // 128-byte rows (one dY column, all 64 k): the 16-byte chunk j of row i sits
@@ -139,52 +137,48 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
     auto mslot = [&](int row) { return (int)((uint32_t)row - fdiv((uint32_t)row, p.div_nmslot) * (p.depth + 2)); };
     auto wrap = [](int x, int n) { return x >= n ? x - n : (x < 0 ? x + n : x); };   // |x| < 2n
     const u32x4_t rs_dy = make_rsrc_words(p.dy, p.dy_bytes);
-    uint32_t ylane[DR_UPW];
-#pragma unroll
-    for (int m = 0; m < DR_UPW; ++m) {
-        const int u = wave + 8 * m;
-        const int i = 8 * u + (lane >> 3);
-        const int j = (lane & 7) ^ dr_swz(i);          // logical chunk stored at physical chunk lane % 8
-        const int q = w0 + p.pad_w - 2 + i;
-        ylane[m] = (u < nu && q >= 0 && q < p.Q) ? (uint32_t)((q * 64 + j * 8) * 2) : kOOB;
-    }
+    // Copy instruction m of this wave fills LDS rows 8 (wave + 8 m) + l / 8
+    // of a slot; the wave issues ny of them per dY row.  Loop-invariant
+    // per-instruction conditions are kept as counts and recomputed offsets,
+    // not as predicates: the compiler would hold each predicate as a
+    // 64-bit lane mask for the whole kernel and spill them.
+    const int ny = nu > wave ? (nu - wave + 7) / 8 : 0;
     // dY row (n, pp) into ring slot `slot`; a row outside the image (the
     // padding above and below) is written as zeros, so that the matrix loop
     // reads every tap's row without a branch
     auto copy_y = [&](int n, int pp, int slot) -> int {
         const bool in = pp >= 0 && pp < p.P;
-        const uint32_t base = in ? (uint32_t)(n * p.P + pp) * (uint32_t)(p.Q * 128) : 0u;
+        const uint32_t base = (uint32_t)(n * p.P + pp) * (uint32_t)(p.Q * 128);
         const uint32_t lds = lds_addr(Ys) + (uint32_t)(slot * p.slot_bytes);
-        int issued = 0;
-#pragma unroll
-        for (int m = 0; m < DR_UPW; ++m) {
+        for (int m = 0; m < ny; ++m) {
             const int u = wave + 8 * m;
-            if (u < nu) {
-                buf_load16_lds(rs_dy, (!in || ylane[m] == kOOB) ? kOOB : base + ylane[m], lds + 1024u * u);
-                ++issued;
-            }
+            const int i = 8 * u + (lane >> 3);
+            const int j = (lane & 7) ^ dr_swz(i);      // logical chunk stored at physical chunk lane % 8
+            const int q = w0 + p.pad_w - 2 + i;
+            const bool ok = in && q >= 0 && q < p.Q;
+            buf_load16_lds(rs_dy, ok ? base + (uint32_t)((q * 64 + j * 8) * 2) : kOOB, lds + 1024u * u);
         }
-        return issued;
+        return ny;
     };
     const u32x4_t rs_m = make_rsrc_words(p.mask, p.mask_bytes);
     // footprint of output row `row` (8 bytes per pixel, wn pixels): 16 bytes
     // per lane when the row is a whole number of 16-byte pieces (wn even),
-    // else 4 bytes per lane; one copy per wave of the first waves
+    // else 4 bytes per lane; one copy per wave of the first waves.  mlane
+    // is the lane's byte in the row, or kOOB past the row's end (src + kOOB
+    // stays past the buffer's end: src < 2^31).
+    const bool m16 = (wn & 1) == 0;
+    const int nm_copy = MASKED && wave * (m16 ? 1024 : 256) < wn * 8 ? 1 : 0;
+    const uint32_t mbyte = m16 ? 1024u * wave + 16u * lane : 256u * wave + 4u * lane;
+    const uint32_t mlane = mbyte < (uint32_t)(wn * 8) ? mbyte : kOOB;
     auto copy_m = [&](int row, int slot) -> int {
         if (!MASKED) return 0;
-        const uint32_t rowb = (uint32_t)(wn * 8);
         const uint32_t src = (uint32_t)(row * p.W + w0) * 8u;
         const uint32_t dst = lds_addr(Ms) + (uint32_t)(slot * p.mslot_bytes);
-        if ((wn & 1) == 0) {
-            if (wave * 1024 >= wn * 8) return 0;
-            const uint32_t byte = 1024u * wave + 16u * lane;
-            buf_load16_lds(rs_m, byte < rowb ? src + byte : kOOB, dst + 1024u * wave);
-        } else {
-            if (wave * 256 >= wn * 8) return 0;
-            const uint32_t byte = 256u * wave + 4u * lane;
-            buf_load4_lds(rs_m, byte < rowb ? src + byte : kOOB, dst + 256u * wave);
+        for (int k = 0; k < nm_copy; ++k) {
+            if (m16) buf_load16_lds(rs_m, src + mlane, dst + 1024u * wave);
+            else buf_load4_lds(rs_m, src + mlane, dst + 256u * wave);
         }
-        return 1;
+        return nm_copy;
     };
     auto image = [&](int row) { return (int)fdiv((uint32_t)row, p.div_h); };
 
