@@ -73,6 +73,40 @@ def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
+_HIP = None
+
+
+def _hip():
+    global _HIP
+    if _HIP is None:
+        import ctypes
+        _HIP = ctypes.CDLL("libamdhip64.so")
+    return _HIP
+
+
+def _fence_free_event():
+    """A raw timing hipEvent_t created with hipEventDisableSystemFence."""
+    import ctypes
+    ev = ctypes.c_void_p()
+    if _hip().hipEventCreateWithFlags(ctypes.byref(ev), 0x20000000) != 0:
+        raise RuntimeError("hipEventCreateWithFlags failed")
+    return ev.value
+
+
+def _event_ms(a, b):
+    import ctypes
+    ms = ctypes.c_float()
+    if _hip().hipEventSynchronize(ctypes.c_void_p(b)) != 0 or \
+            _hip().hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(a), ctypes.c_void_p(b)) != 0:
+        raise RuntimeError("hipEventElapsedTime failed")
+    return ms.value
+
+
+def _event_destroy(e):
+    import ctypes
+    _hip().hipEventDestroy(ctypes.c_void_p(e))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -152,14 +186,14 @@ def main():
         """Mean ms per call of fn over `steps` back-to-back calls, HIP events
         on the launch stream, synchronized on both sides; optionally the mean
         duration of the data- and weight-gradient GEMM kernels from events the
-        library records around their dispatch."""
+        library records around their dispatch.  Those per-kernel events are
+        created without the system-scope fence (hipEventDisableSystemFence):
+        default timing events write back and invalidate the caches when they
+        are recorded, which slows the kernel they bracket."""
         evs = []
         if per_kernel:
             for _ in range(steps):
-                pair = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-                for e in pair:
-                    e.record(stream)  # instantiate the events
-                evs.append(pair)
+                evs.append([_fence_free_event() for _ in range(4)])
         torch.cuda.synchronize()
         t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t0.record(stream)
@@ -176,8 +210,11 @@ def main():
         ms = t0.elapsed_time(t1) / steps
         kern = None
         if per_kernel:
-            kern = (float(np.mean([p[0].elapsed_time(p[1]) for p in evs])),
-                    float(np.mean([p[2].elapsed_time(p[3]) for p in evs])))
+            kern = (float(np.mean([_event_ms(p[0], p[1]) for p in evs])),
+                    float(np.mean([_event_ms(p[2], p[3]) for p in evs])))
+            for p in evs:
+                for e in p:
+                    _event_destroy(e)
         return ms, kern
 
     # footprints (forward-pass side, timed separately)

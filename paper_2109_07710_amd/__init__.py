@@ -301,9 +301,13 @@ def cbw_read_occupancy(desc, ws, stream=None):
 
 
 def cbw_set_profile_events(op, start=None, stop=None):
-    """Record torch.cuda.Event `start`/`stop` around the op's main GEMM kernel
-    on every following call of this thread (None, None switches it off).  The
-    events must have been recorded once so that they exist."""
-    sp = ctypes.c_void_p(start.cuda_event) if start is not None else None
-    tp = ctypes.c_void_p(stop.cuda_event) if stop is not None else None
+    """Record events `start`/`stop` around the op's main GEMM kernel on every
+    following call of this thread (None, None switches it off): torch.cuda.Event
+    objects (recorded once, so that they exist) or raw hipEvent_t handles
+    (int)."""
+    def handle(e):
+        if e is None:
+            return None
+        return ctypes.c_void_p(e if isinstance(e, int) else e.cuda_event)
+    sp, tp = handle(start), handle(stop)
     _check(lib().cbw_set_profile_events(op, sp, tp), "cbw_set_profile_events")

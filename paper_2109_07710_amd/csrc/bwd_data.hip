@@ -28,7 +28,6 @@
 // consecutive rows spread over all banks.
 #include <type_traits>
 
-#include <hip/hip_ext.h>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -1083,13 +1082,12 @@ namespace {
 template <typename T, int MODE, int TI>
 hipError_t launch_shape(const DataParams& p, int nb, hipStream_t stream, const ProfEvents& ev, bool with_reduce)
 {
+    hipError_t e_launch;
     if (p.stride_h == 1 && p.stride_w == 1)
-        hipExtLaunchKernelGGL(bwd_data_kernel<T, MODE, true, TI>, dim3(nb), dim3(Tile<TI>::NT), 0, stream, ev.start,
-                              ev.stop, 0, p);
+        e_launch = launch_timed(bwd_data_kernel<T, MODE, true, TI>, dim3(nb), dim3(Tile<TI>::NT), stream, ev, p);
     else
-        hipExtLaunchKernelGGL(bwd_data_kernel<T, MODE, false, TI>, dim3(nb), dim3(Tile<TI>::NT), 0, stream, ev.start,
-                              ev.stop, 0, p);
-    hipError_t e = hipGetLastError();
+        e_launch = launch_timed(bwd_data_kernel<T, MODE, false, TI>, dim3(nb), dim3(Tile<TI>::NT), stream, ev, p);
+    hipError_t e = e_launch;
     if (e != hipSuccess) return e;
     // in gather mode the split is only known on the device
     if (with_reduce && (MODE == MODE_GATHER || p.split > 1)) {

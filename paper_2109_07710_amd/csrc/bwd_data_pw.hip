@@ -21,7 +21,6 @@
 // dY rows, 8 consecutive k per lane), reduction = k.  Masked calls skip the
 // MFMAs of a block whose footprint is empty (every output +0.0) and count
 // the pixels of the blocks computed.
-#include <hip/hip_ext.h>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -202,13 +201,12 @@ __global__ __launch_bounds__(PW_NT, 2) void bwd_data_pw_kernel(DataPwParams p)
 template <int C, int K>
 hipError_t launch_ck(const DataPwParams& p, int grid, hipStream_t stream, const ProfEvents& ev)
 {
+    hipError_t e_launch;
     if (p.mask)
-        hipExtLaunchKernelGGL(bwd_data_pw_kernel<C, K, true>, dim3(grid), dim3(PW_NT), 0, stream, ev.start, ev.stop,
-                              0, p);
+        e_launch = launch_timed(bwd_data_pw_kernel<C, K, true>, dim3(grid), dim3(PW_NT), stream, ev, p);
     else
-        hipExtLaunchKernelGGL(bwd_data_pw_kernel<C, K, false>, dim3(grid), dim3(PW_NT), 0, stream, ev.start,
-                              ev.stop, 0, p);
-    return hipGetLastError();
+        e_launch = launch_timed(bwd_data_pw_kernel<C, K, false>, dim3(grid), dim3(PW_NT), stream, ev, p);
+    return e_launch;
 }
 
 }  // namespace

@@ -24,7 +24,6 @@
 // they are stored, and a wave skips the matrix work of a row when every one
 // of its outputs there (its channel half of its columns) is dead: those
 // outputs are +0.0 and are counted as not computed.
-#include <hip/hip_ext.h>
 
 #include <type_traits>
 
@@ -379,13 +378,12 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
 template <int NBW>
 hipError_t launch_nbw(const DataRowsParams& p, int grid, hipStream_t stream, const ProfEvents& ev)
 {
+    hipError_t e_launch;
     if (p.mask)
-        hipExtLaunchKernelGGL(bwd_data_rows_kernel<NBW, true>, dim3(grid), dim3(DR_NT), 0, stream, ev.start, ev.stop,
-                              0, p);
+        e_launch = launch_timed(bwd_data_rows_kernel<NBW, true>, dim3(grid), dim3(DR_NT), stream, ev, p);
     else
-        hipExtLaunchKernelGGL(bwd_data_rows_kernel<NBW, false>, dim3(grid), dim3(DR_NT), 0, stream, ev.start,
-                              ev.stop, 0, p);
-    return hipGetLastError();
+        e_launch = launch_timed(bwd_data_rows_kernel<NBW, false>, dim3(grid), dim3(DR_NT), stream, ev, p);
+    return e_launch;
 }
 
 }  // namespace

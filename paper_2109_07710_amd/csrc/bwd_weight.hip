@@ -18,7 +18,6 @@
 // Split-K: the pixel chunks are divided among nsplit workgroups per output
 // tile; each writes a float32 partial tile, reduced afterwards in a fixed
 // order (deterministic).
-#include <hip/hip_ext.h>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -1021,27 +1020,28 @@ int weight_chunk(int dtype) { return CH * (dtype == 1 ? 8 : 4); }
 hipError_t launch_bwd_weight(int dtype, const WeightParams& p, hipStream_t stream, const ProfEvents& ev)
 {
     const int nb = p.tgroups * p.ctiles * p.ktiles * p.nsplit;
+    hipError_t e_launch = hipSuccess;
     if (p.rows) {
         if (dtype != 1 || p.R > 3 || p.S > 3 || p.bk != 64 || p.cg != 64) return hipErrorInvalidValue;
         switch (p.R * p.S) {
-        case 1: hipExtLaunchKernelGGL(bwd_weight_rows_kernel<1>, dim3(nb), dim3(RW_NT), 0, stream, ev.start, ev.stop, 0, p); break;
-        case 2: hipExtLaunchKernelGGL(bwd_weight_rows_kernel<2>, dim3(nb), dim3(RW_NT), 0, stream, ev.start, ev.stop, 0, p); break;
-        case 3: hipExtLaunchKernelGGL(bwd_weight_rows_kernel<3>, dim3(nb), dim3(RW_NT), 0, stream, ev.start, ev.stop, 0, p); break;
-        case 4: hipExtLaunchKernelGGL(bwd_weight_rows_kernel<4>, dim3(nb), dim3(RW_NT), 0, stream, ev.start, ev.stop, 0, p); break;
-        case 6: hipExtLaunchKernelGGL(bwd_weight_rows_kernel<6>, dim3(nb), dim3(RW_NT), 0, stream, ev.start, ev.stop, 0, p); break;
-        case 9: hipExtLaunchKernelGGL(bwd_weight_rows_kernel<9>, dim3(nb), dim3(RW_NT), 0, stream, ev.start, ev.stop, 0, p); break;
+        case 1: e_launch = launch_timed(bwd_weight_rows_kernel<1>, dim3(nb), dim3(RW_NT), stream, ev, p); break;
+        case 2: e_launch = launch_timed(bwd_weight_rows_kernel<2>, dim3(nb), dim3(RW_NT), stream, ev, p); break;
+        case 3: e_launch = launch_timed(bwd_weight_rows_kernel<3>, dim3(nb), dim3(RW_NT), stream, ev, p); break;
+        case 4: e_launch = launch_timed(bwd_weight_rows_kernel<4>, dim3(nb), dim3(RW_NT), stream, ev, p); break;
+        case 6: e_launch = launch_timed(bwd_weight_rows_kernel<6>, dim3(nb), dim3(RW_NT), stream, ev, p); break;
+        case 9: e_launch = launch_timed(bwd_weight_rows_kernel<9>, dim3(nb), dim3(RW_NT), stream, ev, p); break;
         default: return hipErrorInvalidValue;
         }
-        return hipGetLastError();
+        return e_launch;
     }
     const dim3 grid(nb), block(dtype != 1 ? NT : p.bk == 64 ? WTile<64>::NT : WTile<256>::NT);
     if (dtype == 1) {
-        if (p.bk == 64) hipExtLaunchKernelGGL(bwd_weight_tr_kernel<64>, grid, block, 0, stream, ev.start, ev.stop, 0, p);
-        else if (p.bk == 128) hipExtLaunchKernelGGL(bwd_weight_tr_kernel<128>, grid, block, 0, stream, ev.start, ev.stop, 0, p);
-        else hipExtLaunchKernelGGL(bwd_weight_tr_kernel<256>, grid, block, 0, stream, ev.start, ev.stop, 0, p);
+        if (p.bk == 64) e_launch = launch_timed(bwd_weight_tr_kernel<64>, grid, block, stream, ev, p);
+        else if (p.bk == 128) e_launch = launch_timed(bwd_weight_tr_kernel<128>, grid, block, stream, ev, p);
+        else e_launch = launch_timed(bwd_weight_tr_kernel<256>, grid, block, stream, ev, p);
     }
-    else hipExtLaunchKernelGGL(bwd_weight_kernel<float>, grid, block, 0, stream, ev.start, ev.stop, 0, p);
-    return hipGetLastError();
+    else e_launch = launch_timed(bwd_weight_kernel<float>, grid, block, stream, ev, p);
+    return e_launch;
 }
 
 }  // namespace cbw
