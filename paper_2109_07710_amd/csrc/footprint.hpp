@@ -29,8 +29,8 @@ __device__ __forceinline__ bool any_bits(const uint32_t* __restrict__ bits, int6
 }
 
 // Liveness of (pixel px, channel group g of width G): any footprint bit set
-// among the group's channels.  With C a multiple of 256 and G = 256 the
-// group's 8 words are one 32-byte aligned run, read as two vectors.
+// among the group's channels.  With C a multiple of G and G = 256, 128 or 64
+// the group's 8, 4 or 2 words are one aligned run, read as vectors.
 __device__ __forceinline__ bool pixel_live_bits(const uint32_t* __restrict__ mask, int64_t npix, int C, int G, int px,
                                                 int g)
 {
@@ -41,6 +41,14 @@ __device__ __forceinline__ bool pixel_live_bits(const uint32_t* __restrict__ mas
         const uint4* w = reinterpret_cast<const uint4*>(mask + ((base + lo) >> 5));
         const uint4 a = w[0], b = w[1];
         return ((a.x | a.y | a.z | a.w) | (b.x | b.y | b.z | b.w)) != 0;
+    }
+    if (G == 128 && (C & 127) == 0) {
+        const uint4 a = *reinterpret_cast<const uint4*>(mask + ((base + lo) >> 5));
+        return (a.x | a.y | a.z | a.w) != 0;
+    }
+    if (G == 64 && (C & 63) == 0) {
+        const uint2 a = *reinterpret_cast<const uint2*>(mask + ((base + lo) >> 5));
+        return (a.x | a.y) != 0;
     }
     const int hi = min(C, lo + G);
     return any_bits(mask, base + lo, base + hi);
