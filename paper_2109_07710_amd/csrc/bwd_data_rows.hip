@@ -99,9 +99,19 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
     // Filters, per wave: channels 32 cw .. + 31 (two 16-channel blocks), all
     // nine taps and both 32-channel halves of k, as MFMA A fragments (lane:
     // channel col of the block, k = 32 kc + 8 g .. + 7).  wt is [tap][c][k].
+    // The 72 KB of filters go into LDS once per workgroup (the start of the
+    // dY ring, not yet in use; 1 KB copies spread over the waves), and each
+    // wave reads its fragments from there: the eight waves would otherwise
+    // read 36 KB each from L2, four times the same bytes per workgroup, and
+    // that burst at the start of every workgroup measured 6 to 10 us.
     uint4 afr[9][2][2];
     {
-        const __amdgpu_buffer_rsrc_t rw = make_rsrc(p.wt, p.wt_bytes);
+        static_assert(9 * 64 * 64 * 2 <= kDataRowsLds, "the filters fit the ring's LDS");
+        const u32x4_t rw = make_rsrc_words(p.wt, p.wt_bytes);
+        for (int u = wave; u < 9 * 64 * 64 * 2 / 1024; u += DR_NT / 64)
+            buf_load16_lds(rw, (uint32_t)(1024 * u + 16 * lane), lds_addr(Ys) + 1024u * u);
+        wait_vmem();
+        __syncthreads();
 #pragma unroll
         for (int tap = 0; tap < 9; ++tap)
 #pragma unroll
@@ -109,8 +119,9 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
 #pragma unroll
                 for (int kc = 0; kc < 2; ++kc) {
                     const int c = 32 * cw + 16 * cb + col;
-                    afr[tap][cb][kc] = buf_load16(rw, (uint32_t)(((tap * 64 + c) * 64 + kc * 32 + 8 * g) * 2));
+                    afr[tap][cb][kc] = *reinterpret_cast<const uint4*>(Ys + ((tap * 64 + c) * 64 + kc * 32 + 8 * g) * 2);
                 }
+        __syncthreads();   // every wave holds its fragments before the ring overwrites them
     }
 
     // B fragment offsets in a ring slot: output column block b0, tap column
