@@ -242,10 +242,15 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     uint4 (*const Bs)[BN * CH] = reinterpret_cast<uint4 (*)[BN * CH]>(AB + 2 * BM * CH);
     __shared__ int pix_s[BN];
     constexpr bool SEL = MODE == MODE_SELECT || MODE == MODE_GATHER;   // footprint select in the epilogue
-    // footprint words, one padded row of BM/32 + 1 words per pixel row: the
-    // epilogue's 16 lanes that read one word column hit 16 different banks
-    constexpr int MSTR = BM / 32 + 1;
-    __shared__ uint32_t msk_s[SEL ? BN * MSTR : 1];
+    // footprint words, BM/32 per pixel row.  bf16: copied straight into LDS
+    // with step 0's copies (rows unpadded: the staged epilogue reads 16
+    // consecutive words per store instruction; room for every copy lane, past
+    // the tile's words too).  fp32: fetched into registers and staged after
+    // the main loop, rows padded by a word so that the epilogue's 16 lanes
+    // reading one word column hit 16 different banks.
+    constexpr int MSTR = sizeof(T) == 2 ? BM / 32 : BM / 32 + 1;
+    constexpr int MSLOTS = SEL ? (sizeof(T) == 2 ? (BN * (BM / 32) + NT - 1) / NT * NT : BN * MSTR) : 1;
+    __shared__ uint32_t msk_s[MSLOTS];
     // footprint nibble (4 channels) -> masks of two bf16 pairs, for the
     // staged epilogue
     __shared__ uint2 mtab[16];
@@ -441,24 +446,42 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     // Footprint words of the tile (pixel row x 32-channel word, valid when
     // every pixel's group of BM channels starts on a word).  Only the
     // epilogue needs them: they are fetched together with step 0's copies
-    // (their latency hides under the copies'), held in registers through the
-    // main loop and staged in LDS after it.  (Fetching them next to step 1's
-    // copies instead measured 1.5 us slower per launch.)
+    // (their latency hides under the copies').  bf16: direct-to-LDS copies
+    // of one word per lane, complete once step 0's copies are (the waits
+    // count every copy); fp32: held in registers through the main loop and
+    // staged in LDS after it.  (Fetching them next to step 1's copies
+    // instead measured 1.5 us slower per launch.)
     bool mask_lds = false;
     constexpr int MW = SEL ? BN * (BM / 32) : 0;                  // footprint words per tile
     constexpr int MI = MW > 0 ? (MW + NT - 1) / NT : 1;          // per thread
-    uint32_t mwords[MI];
+    constexpr bool MDMA = sizeof(T) == 2;
+    uint32_t mwords[MDMA ? 1 : MI];
     auto fetch_mask = [&]() {
+        if constexpr (MDMA) {
+            const u32x4_t rs_m = make_rsrc_words(p.mask, (uint32_t)(((int64_t)p.npix * p.C + 31) / 32 * 4));
 #pragma unroll
-        for (int u = 0; u < MI; ++u) {
-            const int i = tid + u * NT;
-            uint32_t word = 0;
-            if (i < MW) {
-                const int pr = i / (BM / 32), wi = i - pr * (BM / 32);
-                const int pix = pix_s[pr];
-                if (pix >= 0 && c0 + 32 * wi < p.C) word = p.mask[((int64_t)pix * p.C + c0) / 32 + wi];
+            for (int u = 0; u < MI; ++u) {
+                const int i = tid + u * NT;   // the copy lanes past the tile's words fill msk_s's slack
+                uint32_t off = kOOB;
+                if (i < MW) {
+                    const int pr = i / (BM / 32), wi = i - pr * (BM / 32);
+                    const int pix = pix_s[pr];
+                    if (pix >= 0 && c0 + 32 * wi < p.C) off = (uint32_t)(((int64_t)pix * p.C + c0) / 32 + wi) * 4u;
+                }
+                buf_load4_lds(rs_m, off, lds_addr(msk_s) + 4u * (uint32_t)(u * NT + wave_u * 64));
             }
-            mwords[u] = word;
+        } else {
+#pragma unroll
+            for (int u = 0; u < MI; ++u) {
+                const int i = tid + u * NT;
+                uint32_t word = 0;
+                if (i < MW) {
+                    const int pr = i / (BM / 32), wi = i - pr * (BM / 32);
+                    const int pix = pix_s[pr];
+                    if (pix >= 0 && c0 + 32 * wi < p.C) word = p.mask[((int64_t)pix * p.C + c0) / 32 + wi];
+                }
+                mwords[u] = word;
+            }
         }
     };
 
@@ -562,17 +585,19 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     if (fnw == FN) main_loop(std::integral_constant<int, FN>{});
     else main_loop(std::integral_constant<int, FN - 1>{});
 
-    if (mask_lds) {
-        // msk_s is not an operand buffer: no barrier is needed before writing it
+    if constexpr (!MDMA) {
+        if (mask_lds) {
+            // msk_s is not an operand buffer: no barrier is needed before writing it
 #pragma unroll
-        for (int u = 0; u < MI; ++u) {
-            const int i = tid + u * NT;
-            if (i < MW) {
-                const int pr = i / (BM / 32), wi = i - pr * (BM / 32);
-                msk_s[pr * MSTR + wi] = mwords[u];
+            for (int u = 0; u < MI; ++u) {
+                const int i = tid + u * NT;
+                if (i < MW) {
+                    const int pr = i / (BM / 32), wi = i - pr * (BM / 32);
+                    msk_s[pr * MSTR + wi] = mwords[u];
+                }
             }
+            __syncthreads();
         }
-        __syncthreads();
     }
 
     // Epilogue: lane holds channels c0 + wm*TM + i*16 + 4*(lane/16) + v of
