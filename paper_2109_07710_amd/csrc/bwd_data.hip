@@ -528,17 +528,23 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     };
 
     // Gather mode: whether some group has a dead pixel, a flag per group that
-    // the preparation launch raised (the reduction launch lowers it again):
-    // scalar loads issued before the first copies, complete by the time the
-    // copies have landed, so the usual case (every pixel live) pays nothing.
-    int anydead = 0;
-    if (MODE == MODE_GATHER)
-        for (int g = 0; g < p.ctiles; ++g) anydead |= p.dead_flags[g];
+    // the preparation launch raised (the reduction launch lowers it again).
+    // The flags are read by one vector load per lane (lane g: group g's
+    // flag), issued behind step 0's copies and complete with them, so the
+    // usual case (every pixel live) pays nothing: a scalar read loop ahead of
+    // the copies waited for each load before the first copy went out (1.8 us
+    // per launch).
     map_item(true);
     if (active) start_item();
+    uint32_t dflag = 0;
+    if (MODE == MODE_GATHER) {
+        const __amdgpu_buffer_rsrc_t rs_f = make_rsrc(p.dead_flags, (uint32_t)p.ctiles * 4u);
+        dflag = __builtin_amdgcn_raw_buffer_load_b32(rs_f, lane < p.ctiles ? 4u * lane : kOOB, 0, 0);
+    }
     wait_vmem();
     __syncthreads();
-    if (MODE == MODE_GATHER && anydead != 0) {
+    const bool anydead = MODE == MODE_GATHER && __ballot(dflag != 0u) != 0ull;
+    if (MODE == MODE_GATHER && anydead) {
         // speculation failed (the copies have landed): every group's live
         // total from the block counts (workgroup 0 also stores them for the
         // reduction kernel and the readers), then the tiles over the live lists
