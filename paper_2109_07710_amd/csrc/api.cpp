@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstring>
 #include <mutex>
 
@@ -491,13 +492,28 @@ int conv_fwd_relu_mask(const cbw_conv_desc* desc, const void* X, const void* W, 
     return run_fwd(desc, X, W, Y, y_mask, workspace, workspace_bytes, stream);
 }
 
+// A number per weight-gradient call that skips: the occupancy pass stores it
+// as the call's dead-block flag, the GEMM compares it (a flag left by an
+// earlier call, or uninitialised memory, can only send a call down the
+// ranking path, which is always correct).
+static uint32_t next_call_number()
+{
+    static std::atomic<uint32_t> counter{0};
+    uint32_t g;
+    do g = counter.fetch_add(1, std::memory_order_relaxed) + 1; while (g == 0);
+    return g;
+}
+
 // Occupancy pass of the weight gradient on NHWC tensors (dY, and the
 // footprints, in NHWC order): dY block occupancy from dy_mask or dY, and
 // with x_skip the X-window liveness from the packed X footprint xbits.
 static OccParams weight_occ_params(const cbw_conv_desc* desc, const WeightPlan& plan, const void* dY,
-                                   const uint32_t* dy_mask, bool x_skip, const uint32_t* xbits, void* workspace)
+                                   const uint32_t* dy_mask, bool x_skip, const uint32_t* xbits, void* workspace,
+                                   uint32_t gen)
 {
     OccParams op{};
+    op.any_dead = at<int>(workspace, plan.header) + kDeadWord;
+    op.gen = gen;
     op.dy = dY;
     op.bits = dy_mask;
     op.occ = at<uint8_t>(workspace, plan.occ);
@@ -586,6 +602,7 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
     if ((st = check_ws(workspace, workspace_bytes, plan.total)) != CBW_OK) return st;
     if (!tiles_consistent()) return CBW_ERR_UNSUPPORTED;
     if (x_skip && plan.tgroups * plan.ctiles > 1024) return CBW_ERR_UNSUPPORTED;   // liveness flags per chunk
+    const uint32_t gen = next_call_number();
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool skip = !(flags & CBW_FLAG_NO_SKIP);
     hipError_t e;
@@ -622,10 +639,11 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
                 return hip_status(e);
             xbits = packed;
         }
-        const OccParams op = weight_occ_params(desc, plan, dY, dy_mask, x_skip, xbits, workspace);
+        const OccParams op = weight_occ_params(desc, plan, dY, dy_mask, x_skip, xbits, workspace, gen);
         if ((e = launch_occupancy(op, s)) != hipSuccess) return hip_status(e);
     }
-    const WeightParams p = weight_gemm_params(desc, plan, X, dY, dW, workspace, skip, x_skip, flags);
+    WeightParams p = weight_gemm_params(desc, plan, X, dY, dW, workspace, skip, x_skip, flags);
+    p.gen = gen;
     if ((e = launch_bwd_weight(desc->dtype, p, s, prof_events(1))) != hipSuccess) return hip_status(e);
     if (!plan.direct) {
         e = launch_splitk_reduce(p.out, dW, plan.nparts, desc->K, desc->R * desc->S, desc->C,
@@ -684,7 +702,8 @@ static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY
     CompactParams cp;
     if (tiled) data_gemm_params(desc, dplan, dY, wt, x_mask, dX, ws, gather, false, &dp, &cp);
     OccParams op{};
-    if (skip) op = weight_occ_params(desc, wplan, dY, dy_mask, x_skip, x_mask, wws);
+    const uint32_t gen = next_call_number();
+    if (skip) op = weight_occ_params(desc, wplan, dY, dy_mask, x_skip, x_mask, wws, gen);
     hipError_t e = launch_data_prep(desc->dtype, W, wt, desc->K, desc->C, desc->R * desc->S,
                                     desc->w_layout == CBW_KRSC, header, mode, gather ? &cp : nullptr, s,
                                     skip ? &op : nullptr);
@@ -699,8 +718,8 @@ static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY
         e = launch_bwd_data(desc->dtype, mode, dp, s, prof_events(0), false);
     }
     if (e != hipSuccess) return hip_status(e);
-    const WeightParams wp = weight_gemm_params(desc, wplan, X, dY, dW, wws, skip, x_skip,
-                                               flags & CBW_FLAG_NO_SKIP);
+    WeightParams wp = weight_gemm_params(desc, wplan, X, dY, dW, wws, skip, x_skip, flags & CBW_FLAG_NO_SKIP);
+    wp.gen = gen;
     if ((e = launch_bwd_weight(desc->dtype, wp, s, prof_events(1))) != hipSuccess) return hip_status(e);
     ReduceParams rp{};
     if (!wplan.direct) {

@@ -638,24 +638,43 @@ __global__ __launch_bounds__(WTile<BKT>::NT) void bwd_weight_tr_kernel(WeightPar
     // skipping), with the liveness of its first OCC_WIN chunks read once into
     // LDS so the loop tests them without a global read on its critical path.
     // The ranking scratch borrows the second operand buffer, not yet in use.
+    //
+    // The unskipped range's step-0 copies go out first and the call's
+    // dead-block flag is read behind them: when the occupancy pass found no
+    // dead block (the usual case for element-wise footprints) that range is
+    // this split's range and the copies stand; otherwise the range is ranked
+    // over the live chunks once the copies have landed, and step 0 copied
+    // again.
     __shared__ uint8_t live_s[OCC_WIN];
     const int combo = tg * p.ctiles + ct;
-    int ch_begin, ch_end;
+    int ch_begin = min(p.nchunks, z * p.chunks_per_split);
+    int ch_end = min(p.nchunks, ch_begin + p.chunks_per_split);
     static_assert(sizeof(As[1]) >= SPLIT_SCRATCH_BYTES, "ranking scratch fits the second operand buffer");
-    const bool all_live = split_range(p, kt, combo, z, ch_begin, ch_end, live_s, reinterpret_cast<uint8_t*>(As[1]));
-    int skipped = 0;
-    auto next_live = [&](int chunk) {
-        return all_live ? chunk : next_live_chunk(p, live_s, ch_begin, ch_end, kt, combo, chunk, skipped);
-    };
-
-    int chunk = next_live(ch_begin);
-    int buf = 0;
+    int chunk = ch_begin;
     if (chunk < ch_end) {
         set_chunk(chunk);
         load(0);
     }
+    uint32_t dflag = 0;
+    if (p.occ) dflag = __builtin_amdgcn_raw_buffer_load_b32(make_rsrc(p.header, 64), 4 * kDeadWord, 0, 0);
     wait_vmem();
     __syncthreads();
+    bool all_live = true;
+    int skipped = 0;
+    if (p.occ && __builtin_amdgcn_readfirstlane(dflag) == p.gen) {
+        all_live = split_range(p, kt, combo, z, ch_begin, ch_end, live_s, reinterpret_cast<uint8_t*>(As[1]));
+        chunk = all_live ? ch_begin : next_live_chunk(p, live_s, ch_begin, ch_end, kt, combo, ch_begin, skipped);
+        if (chunk < ch_end) {
+            set_chunk(chunk);
+            load(0);
+        }
+        wait_vmem();
+        __syncthreads();
+    }
+    auto next_live = [&](int c) {
+        return all_live ? c : next_live_chunk(p, live_s, ch_begin, ch_end, kt, combo, c, skipped);
+    };
+    int buf = 0;
     while (chunk < ch_end) {
         const int next = next_live(chunk + 1);
         if (next < ch_end) {
@@ -920,11 +939,16 @@ __global__ __launch_bounds__(RW_NT) void bwd_weight_rows_kernel(WeightParams p)
         }
     };
 
-    // this split's row range, balanced over the live rows when skipping
+    // this split's row range, balanced over the live rows when skipping:
+    // the unskipped range first, its step-0 copies issued at once with the
+    // call's dead-block flag read behind them; only when the occupancy pass
+    // found a dead row is the range ranked (in the X ring, once the copies
+    // have landed) and step 0 copied again
     const int combo = qt * p.ctiles + ct;
-    int ch_begin, ch_end;
+    int ch_begin = min(p.nchunks, z * p.chunks_per_split);
+    int ch_end = min(p.nchunks, ch_begin + p.chunks_per_split);
     static_assert(sizeof(Xs) >= SPLIT_SCRATCH_BYTES, "ranking scratch fits the X ring");
-    const bool all_live = split_range(p, kt, combo, z, ch_begin, ch_end, live_s, reinterpret_cast<uint8_t*>(Xs));
+    bool all_live = true;
     int skipped = 0;
     auto next_live = [&](int row) {
         return all_live ? row : next_live_chunk(p, live_s, ch_begin, ch_end, kt, combo, row, skipped);
@@ -941,9 +965,6 @@ __global__ __launch_bounds__(RW_NT) void bwd_weight_rows_kernel(WeightParams p)
     auto follows = [&](int a, int b) {   // output row b comes right after a in the same image
         return b == a + 1 && fdiv((uint32_t)b, p.div_p) == fdiv((uint32_t)a, p.div_p);
     };
-    int ra = next_live(ch_begin);
-    int rb = ra < ch_end ? next_live(ra + 1) : ch_end;
-    int rc = rb < ch_end ? next_live(rb + 1) : ch_end;
     auto new_row = [&](int c) {          // the input row a following output row adds to the window
         const int n = (int)fdiv((uint32_t)c, p.div_p), pp = c - n * p.P;
         return copy_x(n, pp - p.pad_h + p.R - 1);
@@ -952,16 +973,32 @@ __global__ __launch_bounds__(RW_NT) void bwd_weight_rows_kernel(WeightParams p)
         const int n = (int)fdiv((uint32_t)c, p.div_p), pp = c - n * p.P;
         for (int r = 0; r < p.R; ++r) copy_x(n, pp - p.pad_h + r);
     };
-    if (ra < ch_end) {
-        copy_y(0, ra);
-        all_rows(ra);
-        if (rb < ch_end) {
-            copy_y(1, rb);
-            if (follows(ra, rb)) new_row(rb);
+    int ra, rb, rc;
+    auto first_steps = [&]() {           // rows of steps 0 .. 2 and the copies of steps 0 and 1
+        ra = next_live(ch_begin);
+        rb = ra < ch_end ? next_live(ra + 1) : ch_end;
+        rc = rb < ch_end ? next_live(rb + 1) : ch_end;
+        if (ra < ch_end) {
+            copy_y(0, ra);
+            all_rows(ra);
+            if (rb < ch_end) {
+                copy_y(1, rb);
+                if (follows(ra, rb)) new_row(rb);
+            }
         }
-    }
+    };
+    first_steps();
+    uint32_t dflag = 0;
+    if (p.occ) dflag = __builtin_amdgcn_raw_buffer_load_b32(make_rsrc(p.header, 64), 4 * kDeadWord, 0, 0);
     wait_vmem();
     __syncthreads();
+    if (p.occ && __builtin_amdgcn_readfirstlane(dflag) == p.gen) {
+        all_live = split_range(p, kt, combo, z, ch_begin, ch_end, live_s, reinterpret_cast<uint8_t*>(Xs));
+        __syncthreads();   // the ranking scratch is free before the ring is copied again
+        first_steps();
+        wait_vmem();
+        __syncthreads();
+    }
     int ybuf = 0;
     while (ra < ch_end) {
         int issued = 0;   // this wave's copies for step i + 2

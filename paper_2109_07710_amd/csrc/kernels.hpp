@@ -137,7 +137,11 @@ struct WeightParams {
     int mode_flags;
     uint32_t x_bytes, dy_bytes;
     FastDiv div_q, div_p;    // pixel -> (n, p, q)
+    // this call's number: header[kDeadWord] == gen when the occupancy pass
+    // found a dead block (bf16 kernels; see OccParams)
+    uint32_t gen;
 };
+constexpr int kDeadWord = 4;   // weight workspace header word of the dead-block flag
 
 struct OccParams {
     const void* dy;          // values [npq][K] (used when bits == null)
@@ -154,6 +158,11 @@ struct OccParams {
     int tpg, tgroups, ctiles, ctw;   // taps per group, groups, channel tiles, channels per tile
     FastDiv div_q, div_p;
     FastDiv div_chunk, div_ktiles;   // pixel -> chunk, pair -> pixel
+    // The call's dead-block flag: a workgroup that finds a dead block (or a
+    // dead X window) stores gen, this call's number, into *any_dead, which
+    // the GEMM compares with the same number (nullable).
+    int* any_dead;
+    uint32_t gen;
 };
 
 // Per-element data gradient on the vector ALUs (bf16, NHWC, KRSC filters).

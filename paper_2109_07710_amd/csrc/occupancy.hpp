@@ -108,8 +108,13 @@ __device__ __forceinline__ void occupancy_block(const OccParams& p, int block)
         }
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < nloc * p.ktiles; i += blockDim.x)
+    bool dead = false;
+    for (int i = threadIdx.x; i < nloc * p.ktiles; i += blockDim.x) {
         p.occ[(int64_t)chunk0 * p.ktiles + i] = (uint8_t)(flags[i] != 0);
+        dead |= flags[i] == 0;
+    }
+    // the call's dead-block flag (every writer stores the same number)
+    if (__syncthreads_or(dead) && p.any_dead && threadIdx.x == 0) *p.any_dead = (int)p.gen;
 
     // X-window liveness for every (tap group, channel tile) of the weight
     // gradient's tiling: 1 iff some pixel of the chunk has, at one of the
@@ -151,8 +156,12 @@ __device__ __forceinline__ void occupancy_block(const OccParams& p, int block)
             if (any) xflags[(int)fdiv((uint32_t)j, p.div_chunk) * ncombo + combo] = 1;   // every writer stores 1
         }
         __syncthreads();
-        for (int i = threadIdx.x; i < nloc * ncombo; i += blockDim.x)
+        bool xdead = false;
+        for (int i = threadIdx.x; i < nloc * ncombo; i += blockDim.x) {
             p.xlive[(int64_t)chunk0 * ncombo + i] = (uint8_t)(xflags[i] != 0);
+            xdead |= xflags[i] == 0;
+        }
+        if (__syncthreads_or(xdead) && p.any_dead && threadIdx.x == 0) *p.any_dead = (int)p.gen;
     }
 }
 
