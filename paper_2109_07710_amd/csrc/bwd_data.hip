@@ -304,9 +304,13 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
             ntiles = p.ptiles * p.ctiles;
             nsplit = p.split;
         } else {
-            brows = gather_rows<BN>(gtot_s, p.ctiles, p.nslots);
+            // values read from LDS are per-lane to the compiler: made scalar
+            // here, or everything derived from them (the step range, the tap
+            // walk of the main loop) would be carried in vector registers
+            brows = __builtin_amdgcn_readfirstlane(gather_rows<BN>(gtot_s, p.ctiles, p.nslots));
             ntiles = 0;
             for (int g = 0; g < p.ctiles; ++g) ntiles += (gtot_s[g] + brows - 1) / brows;
+            ntiles = __builtin_amdgcn_readfirstlane(ntiles);
             nsplit = data_split(ntiles, nsteps, p.nslots, p.smax);
         }
         // The grid may hold more workgroups than items (gather mode sizes it
@@ -324,6 +328,8 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
             ctile = tile - ptile * p.ctiles;
         } else {
             gather_tile(gtot_s, p.ctiles, brows, tile, ctile, ptile);
+            ctile = __builtin_amdgcn_readfirstlane(ctile);
+            ptile = __builtin_amdgcn_readfirstlane(ptile);
         }
         c0 = ctile * BM;
         row0 = ptile * brows;
@@ -334,7 +340,7 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
         const int fn_base = nblk16 / WN, fn_rem = nblk16 - fn_base * WN;
         fnw = __builtin_amdgcn_readfirstlane(fn_base + (wn < fn_rem ? 1 : 0));
         wrow0 = 16 * (wn * fn_base + (wn < fn_rem ? wn : fn_rem));
-        nrows = dense_rule ? p.npix : gtot_s[ctile];
+        nrows = dense_rule ? p.npix : __builtin_amdgcn_readfirstlane(gtot_s[ctile]);
         listed = !dense_rule && nrows < p.npix;
         st_begin = (int)((int64_t)z * nsteps / nsplit);
         nloc = (int)((int64_t)(z + 1) * nsteps / nsplit) - st_begin;
