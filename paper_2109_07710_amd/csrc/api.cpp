@@ -93,7 +93,6 @@ void data_gemm_params(const cbw_conv_desc* desc, const DataPlan& plan, const voi
     p.mask = x_mask;
     p.ptiles = plan.ptiles;
     p.brows = plan.brows;
-    p.maxtiles = plan.maxtiles;
     p.nslots = kDataSlots;
     p.smax = no_split ? 1 : kDataMaxSplit;
     p.split = plan.split;   // gather mode: the split of its dense tiles, which it checks on the device
@@ -300,7 +299,6 @@ int run_fwd(const cbw_conv_desc* desc, const void* X, const void* W, void* Y, ui
     p.tile = plan.tile;
     p.ptiles = plan.ptiles;
     p.brows = plan.brows;
-    p.maxtiles = plan.maxtiles;
     p.nslots = kDataSlots;
     p.smax = kDataMaxSplit;
     p.split = plan.split;

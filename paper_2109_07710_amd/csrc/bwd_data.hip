@@ -88,9 +88,10 @@ __device__ __forceinline__ void wave_coords(int w, int& wm, int& wn)
 }
 
 // Rows per tile in gather mode, from the live counts of every channel group
-// (the host makes the same choice for the other modes from the pixel count).
+// (the host makes the same choice for the other modes from the pixel count),
+// among the choices that give at most `cap` tiles.
 template <int BN>
-__device__ __forceinline__ int gather_rows(const int32_t* counts, int groups, int slots)
+__device__ __forceinline__ int gather_rows(const int32_t* counts, int groups, int slots, int cap)
 {
     int tiles[kDataRowChoices];
 #pragma unroll
@@ -100,7 +101,7 @@ __device__ __forceinline__ int gather_rows(const int32_t* counts, int groups, in
         for (int g = 0; g < groups; ++g) t += (counts[g] + rows - 1) / rows;
         tiles[c] = t;
     }
-    return data_rows_pick(tiles, BN, slots);
+    return data_rows_pick(tiles, BN, slots, cap);
 }
 
 // Channel group and pixel tile of gather-mode tile `tile`.  Tiles are taken
@@ -307,7 +308,7 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
             // values read from LDS are per-lane to the compiler: made scalar
             // here, or everything derived from them (the step range, the tap
             // walk of the main loop) would be carried in vector registers
-            brows = __builtin_amdgcn_readfirstlane(gather_rows<BN>(gtot_s, p.ctiles, p.nslots));
+            brows = __builtin_amdgcn_readfirstlane(gather_rows<BN>(gtot_s, p.ctiles, p.nslots, p.ptiles * p.ctiles));
             ntiles = 0;
             for (int g = 0; g < p.ctiles; ++g) ntiles += (gtot_s[g] + brows - 1) / brows;
             ntiles = __builtin_amdgcn_readfirstlane(ntiles);
@@ -1156,9 +1157,12 @@ hipError_t launch_type(int mode, const DataParams& p, int nb, hipStream_t stream
 hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t stream, const ProfEvents& ev,
                            bool with_reduce)
 {
-    // enough workgroups for every tile unsplit (gather mode: at the smallest
-    // row choice), or for nslots split items
-    const int nb = max(mode == MODE_GATHER ? p.maxtiles : p.ptiles * p.ctiles, p.nslots);
+    // enough workgroups for every tile of the dense tiling unsplit, or for
+    // nslots split items.  Gather mode fits too: with at most as many live
+    // pixels per group its tiles at the dense row count are no more, its row
+    // choice is capped at the dense tile count, and a split tiling has at
+    // most nslots items.
+    const int nb = max(p.ptiles * p.ctiles, p.nslots);
     if (nb <= 0) return hipSuccess;
     if (p.tile < 0 || p.tile >= kDataTileCount || p.smax > kMaxDataSplit) return hipErrorInvalidValue;
     return dtype == 1 ? launch_type<uint16_t>(mode, p, nb, stream, ev, with_reduce)

@@ -60,7 +60,6 @@ struct DataParams {
     int ctiles;              // channel tiles = compaction groups
     int ptiles;              // pixel tiles (dense / select modes)
     int brows;               // pixel rows per tile (dense / select modes; gather derives its own)
-    int maxtiles;            // upper bound of the tile count any mode can derive (grid size)
     int split;               // reduction split (dense / select modes; gather derives its own)
     int nslots, smax;        // resident workgroups; largest split
     float* partial;          // [item][BN][BM] fp32 partial tiles when split

@@ -165,7 +165,6 @@ int plan_data(const cbw_conv_desc* d, bool masked, DataPlan* out, bool no_split,
     }
     p.brows = data_rows_pick(cand, p.bn, kDataSlots);
     p.ptiles = (int)((p.npix + p.brows - 1) / p.brows);
-    p.maxtiles = cand[kDataRowChoices - 1];
     const int bk = 8 * (d->dtype == CBW_BF16 ? 8 : 4);
     p.nsteps = d->R * d->S * ((d->K + bk - 1) / bk);
     p.split = no_split ? 1 : host_data_split(p.ptiles * p.groups, p.nsteps);

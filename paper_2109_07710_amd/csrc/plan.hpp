@@ -34,7 +34,6 @@ struct DataPlan {
     int groups = 0, nblk = 0;
     int ptiles = 0, nsteps = 0;
     int brows = 0;          // dense / select: pixel rows per tile (data_rows_pick)
-    int maxtiles = 0;       // most tiles any row choice can give (the gather mode's grid)
     int split = 1;          // dense / select: host-chosen reduction split
     // Row-window kernel (data_rows_eligible): a workgroup per (column
     // segment, strip of rows_per_strip output rows), nbw 16-column blocks

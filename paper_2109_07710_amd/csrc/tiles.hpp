@@ -54,17 +54,21 @@ constexpr int kDataRowsLds = 159744;
 // tiles of 224 rows (two rounds of 14 pixel blocks) or 483 tiles of 208 rows (two
 // rounds of 13).  When so few tiles exist that the reduction is split
 // (2 * tiles <= slots) the full tile is kept.  tiles[d] is the tile count at
-// BN - 16 d rows.  constexpr, so host planner and kernels share this one rule.
+// BN - 16 d rows; a choice with more than `cap` tiles is not taken (the
+// gather mode's grid holds the dense tiling's tile count, and the full tile
+// never exceeds it).  constexpr, so host planner and kernels share this one
+// rule.
 #ifndef CBW_DX_ROW_CHOICES
 #define CBW_DX_ROW_CHOICES 3
 #endif
 constexpr int kDataRowChoices = CBW_DX_ROW_CHOICES;
-constexpr int data_rows_pick(const int* tiles, int bn, int slots)
+constexpr int data_rows_pick(const int* tiles, int bn, int slots, int cap = 0x7fffffff)
 {
     if (2 * tiles[0] <= slots) return bn;
     int best = bn;
     long long best_cost = (long long)((tiles[0] + slots - 1) / slots) * bn;
     for (int d = 1; d < kDataRowChoices; ++d) {
+        if (tiles[d] > cap) continue;
         const int rows = bn - 16 * d;
         const long long cost = (long long)((tiles[d] + slots - 1) / slots) * rows;
         if (cost < best_cost) {
