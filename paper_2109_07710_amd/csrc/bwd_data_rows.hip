@@ -76,6 +76,9 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
     // this step's, the previous one's (stored now) and the next depth.
     __shared__ __attribute__((aligned(1024))) char Ys[kDataRowsLds];
     char* const Ms = Ys + p.mask_off;
+    // footprint nibble (4 channels) -> the masks of the lane's two output
+    // words, 16 bits per channel
+    __shared__ uint2 mtab[16];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -105,6 +108,10 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
     // read 36 KB each from L2, four times the same bytes per workgroup, and
     // that burst at the start of every workgroup measured 6 to 10 us.
     uint4 afr[9][2][2];
+    if (MASKED && tid < 16) {
+        auto half = [](int b) { return b ? 0xffffu : 0u; };
+        mtab[tid] = make_uint2(half(tid & 1) | (half(tid & 2) << 16), half(tid & 4) | (half(tid & 8) << 16));
+    }
     {
         static_assert(9 * 64 * 64 * 2 <= kDataRowsLds, "the filters fit the ring's LDS");
         const u32x4_t rw = make_rsrc_words(p.wt, p.wt_bytes);
@@ -173,11 +180,13 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
     const u32x4_t rs_m = make_rsrc_words(p.mask, p.mask_bytes);
     // footprint of output row `row` (8 bytes per pixel, wn pixels): 16 bytes
     // per lane when the row is a whole number of 16-byte pieces (wn even),
-    // else 4 bytes per lane; one copy per wave of the first waves.  mlane
+    // else 4 bytes per lane; one copy per wave of the first waves, over the
+    // row's 16-pixel blocks (128 nwb bytes, what the readers reach).  mlane
     // is the lane's byte in the row, or kOOB past the row's end (src + kOOB
-    // stays past the buffer's end: src < 2^31).
+    // stays past the buffer's end: src < 2^31), which writes zeros, so the
+    // pixels of the last block past the segment read as dead.
     const bool m16 = (wn & 1) == 0;
-    const int nm_copy = MASKED && wave * (m16 ? 1024 : 256) < wn * 8 ? 1 : 0;
+    const int nm_copy = MASKED && wave * (m16 ? 1024 : 256) < 128 * nwb ? 1 : 0;
     const uint32_t mbyte = m16 ? 1024u * wave + 16u * lane : 256u * wave + 4u * lane;
     const uint32_t mlane = mbyte < (uint32_t)(wn * 8) ? mbyte : kOOB;
     auto copy_m = [&](int row, int slot) -> int {
@@ -229,28 +238,25 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
 
     // The wave's footprint words of row slot `ms`: channels 32 cw .. + 31 of
     // pixel 16 (b0 + j) + col (0 past the segment).
+    const int mw_off = (16 * b0 + col) * 8 + cw * 4;   // the lane's word of block b0; block b0 + j: + 128 j
     auto mask_words = [&](int ms, uint32_t* mw, auto nb_tag) {
         constexpr int NB = decltype(nb_tag)::value;
-        const char* mrow = Ms + ms * p.mslot_bytes;
+        const char* mrow = Ms + ms * p.mslot_bytes + mw_off;
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-            const int px = 16 * (b0 + j) + col;
-            mw[j] = px < wn ? *reinterpret_cast<const uint32_t*>(mrow + px * 8 + cw * 4) : 0u;
-        }
+        for (int j = 0; j < NB; ++j) mw[j] = *reinterpret_cast<const uint32_t*>(mrow + 128 * j);
     };
     // pixels of this wave's columns (each pixel belongs to two waves, one
     // per channel half)
     const int wave_px = max(0, min(16 * (b0 + cnt), wn) - 16 * b0);
 
     // One output row: the matrix work unless every output of this wave is
-    // dead (its channel half of its columns), then the sums rounded and held
-    // for the next step, which applies the footprint and stores them.
-    auto step = [&](int h, int sl0, int ms, auto nb_tag) {
+    // dead (its channel half of its columns; mw: the row's footprint words),
+    // then the sums rounded and held for the next step, which applies the
+    // footprint and stores them.
+    auto step = [&](int h, int sl0, const uint32_t* mw, auto nb_tag) {
         constexpr int NB = decltype(nb_tag)::value;
         bool live = true;
         if (MASKED && p.skip) {
-            uint32_t mw[NB > 0 ? NB : 1];
-            mask_words(ms, mw, nb_tag);
             uint32_t any = 0;
 #pragma unroll
             for (int j = 0; j < NB; ++j) any |= mw[j];
@@ -280,10 +286,8 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
     // memory's write granule is 64 bytes): group g gets channels
     // 16 (g % 2) + 8 (g / 2) .. + 7 of the wave's half.
     const int choff = 16 * (g & 1) + 8 * (g >> 1);
-    auto store = [&](int row, int ms, auto nb_tag) {
+    auto store = [&](int row, const uint32_t* mw, auto nb_tag) {
         constexpr int NB = decltype(nb_tag)::value;
-        uint32_t mw[NB > 0 ? NB : 1];
-        if (MASKED) mask_words(ms, mw, nb_tag);
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             const int w = 16 * (b0 + j) + col;
@@ -292,9 +296,9 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
             for (int cb = 0; cb < 2; ++cb) {
                 v[cb] = outv[cb][j];
                 if (MASKED) {
-                    const uint32_t keep = mw[j] >> (16 * cb + 4 * g);
-                    v[cb].x &= ((0u - (keep & 1u)) & 0xffffu) | ((0u - ((keep >> 1) & 1u)) & 0xffff0000u);
-                    v[cb].y &= ((0u - ((keep >> 2) & 1u)) & 0xffffu) | ((0u - ((keep >> 3) & 1u)) & 0xffff0000u);
+                    const uint2 km = mtab[(mw[j] >> (16 * cb + 4 * g)) & 15u];
+                    v[cb].x &= km.x;
+                    v[cb].y &= km.y;
                 }
             }
             // odd lane rows of block 0 <-> even lane rows of block 1
@@ -343,8 +347,16 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
         }
         wait_vmem();
         __syncthreads();
+        // footprint words of the row stored at this step (read at the step
+        // before, for its skip test) and of the row computed now: each row's
+        // words are read from LDS once, first thing in its step, so their
+        // latency passes under the stores and copies issued behind them
+        constexpr int NB = decltype(nb_tag)::value;
+        uint32_t mwp[NB > 0 ? NB : 1] = {};
         for (; ra < row_end; ++ra) {
-            if (ra > row_begin) store(ra - 1, wrap(ms - 1, nm), nb_tag);
+            uint32_t mwc[NB > 0 ? NB : 1] = {};
+            if (MASKED) mask_words(ms, mwc, nb_tag);
+            if (ra > row_begin) store(ra - 1, mwp, nb_tag);
             int issued = 0;
             if (ra + D < row_end) {
                 if (h + D < p.H) issued += copy_y(n, h + p.pad_h + D, wrap(sl0 + D, p.nslot));
@@ -352,7 +364,9 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
             }
             hist = (hist << 8) | (uint64_t)issued;
             allowed += issued - (int)((hist >> (8 * (D - 1))) & 0xffu);
-            step(h, sl0, ms, nb_tag);
+            step(h, sl0, mwc, nb_tag);
+#pragma unroll
+            for (int j = 0; j < (NB > 0 ? NB : 1); ++j) mwp[j] = mwc[j];
             wait_vmem_le(allowed);
             __syncthreads();
             // advance to row ra + 1
@@ -366,7 +380,7 @@ __global__ __launch_bounds__(DR_NT) void bwd_data_rows_kernel(DataRowsParams p)
                 __syncthreads();
             }
         }
-        if (row_end > row_begin) store(row_end - 1, wrap(ms - 1, nm), nb_tag);
+        if (row_end > row_begin) store(row_end - 1, mwp, nb_tag);
     };
     // cnt <= NBW (checked by the host for the first segment, which is the widest)
     if (cnt >= NBW) pipeline(std::integral_constant<int, NBW>{});
