@@ -26,6 +26,7 @@
 // barrier per reduction step).  LDS rows are 128 bytes (8 chunks of 16
 // bytes) with an XOR chunk swizzle so that the MFMA fragment reads of 16
 // consecutive rows spread over all banks.
+#include <algorithm>
 #include <type_traits>
 
 
@@ -1009,6 +1010,23 @@ __global__ __launch_bounds__(256) void splitk_data_reduce_kernel(DataParams p)
     data_reduce_block<T, MODE, TI>(p, blockIdx.x, gridDim.x);
 }
 
+// Workgroups of the data gradient's split reduction: one output vector per
+// thread when the dense tiling is split (the host knows that split), and at
+// least one per resident GEMM workgroup, which covers gather mode's split
+// (decided on the device, over at most half that many tiles) with a few
+// vectors per thread.  Each vector's loads are one chain of latency, so the
+// grid follows the work rather than a fixed size.
+int data_reduce_blocks(const DataParams& p)
+{
+    int64_t nvec = 0;
+    if (p.split > 1) {
+        const int bm = p.tile == 0 ? Tile<0>::BM : p.tile == 1 ? Tile<1>::BM : Tile<2>::BM;
+        const int bn = p.tile == 0 ? Tile<0>::BN : p.tile == 1 ? Tile<1>::BN : Tile<2>::BN;
+        nvec = (int64_t)p.ptiles * p.ctiles * bn * (bm / 4);
+    }
+    return (int)std::max<int64_t>(p.nslots, (nvec + 255) / 256);
+}
+
 // The split reductions of both gradients in one launch (the call that
 // computes both): blocks [0, dw_blocks) sum the weight gradient's split-K
 // partials (G threads per output), the next dx_blocks blocks the data
@@ -1087,7 +1105,7 @@ hipError_t launch_data_prep(int dtype, const void* w, void* wt, int K, int C, in
 hipError_t launch_bwd_reduce(int dtype, int dx_mode, const DataParams& dp, bool dx_reduce, const ReduceParams& rp,
                              hipStream_t stream)
 {
-    const int dx_blocks = dx_reduce ? dp.nslots : 0;
+    const int dx_blocks = dx_reduce ? data_reduce_blocks(dp) : 0;
     const int nb = rp.blocks + dx_blocks;
     if (nb == 0) return hipSuccess;
     if (dx_reduce && (dp.tile < 0 || dp.tile >= kDataTileCount || dp.smax > kMaxDataSplit)) return hipErrorInvalidValue;
@@ -1129,7 +1147,7 @@ hipError_t launch_shape(const DataParams& p, int nb, hipStream_t stream, const P
     if (e != hipSuccess) return e;
     // in gather mode the split is only known on the device
     if (with_reduce && (MODE == MODE_GATHER || p.split > 1)) {
-        splitk_data_reduce_kernel<T, MODE, TI><<<p.nslots, 256, 0, stream>>>(p);
+        splitk_data_reduce_kernel<T, MODE, TI><<<data_reduce_blocks(p), 256, 0, stream>>>(p);
         e = hipGetLastError();
     }
     return e;
