@@ -3,6 +3,8 @@
 // vectors, and the dY block occupancy (with the X-window liveness).
 #pragma once
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "footprint.hpp"
@@ -52,46 +54,65 @@ __device__ __forceinline__ void occupancy_block(const OccParams& p, int block)
     for (int i = threadIdx.x; i < nloc * p.ktiles; i += blockDim.x) flags[i] = 0;
     __syncthreads();
     if (p.bits) {
-        // whole 16-, 8- or 32-byte aligned word runs per (pixel, k tile) when
-        // K is a multiple of the tile width (256, 128 or 64 channels)
+        // whole 8-, 16- or 32-byte aligned word runs per (pixel, k tile) when
+        // K is a multiple of the tile width (64, 128 or 256 channels)
         const int vw = (p.K % p.BNk) == 0 ? (p.BNk == 256 ? 8 : p.BNk == 128 ? 4 : p.BNk == 64 ? 2 : 0) : 0;
         const int pairs = npx * p.ktiles;
-        auto pair_any = [&](int i) -> bool {
-            const int j = (int)fdiv((uint32_t)i, p.div_ktiles), kt = i - j * p.ktiles;   // pixel of the group, k tile
-            const int64_t base = (int64_t)(px0 + j) * p.K;
-            const int lo = kt * p.BNk, hi = min(p.K, lo + p.BNk);
-            const uint32_t* wp = p.bits + ((base + lo) >> 5);
-            if (vw == 8) {
-                const uint4* w = reinterpret_cast<const uint4*>(wp);
-                const uint4 a = w[0], b = w[1];
-                return ((a.x | a.y | a.z | a.w) | (b.x | b.y | b.z | b.w)) != 0;
-            }
-            if (vw == 4) {
-                const uint4 a = *reinterpret_cast<const uint4*>(wp);
-                return (a.x | a.y | a.z | a.w) != 0;
-            }
-            if (vw == 2) {
-                const uint2 a = *reinterpret_cast<const uint2*>(wp);
-                return (a.x | a.y) != 0;
-            }
-            return any_bits(p.bits, base + lo, base + hi);
-        };
-        // eight (pixel, k tile) pairs per thread and round, their loads
-        // issued together; consecutive threads read consecutive runs
-        for (int i0 = threadIdx.x; i0 < pairs; i0 += 8 * blockDim.x) {
-            bool any[8];
+        const int64_t bits_bytes = ((int64_t)p.npq * p.K + 31) / 32 * 4;
+        const int lane = threadIdx.x & 63;
+        // eight (pixel, k tile) pairs per thread and round; consecutive
+        // threads read consecutive runs.  The runs go through a buffer
+        // descriptor, so every load is issued unconditionally (a pair past
+        // the group gets offset kOOB and reads zeros) and the eight of a
+        // round are in flight together.  A lane marks its pair's flag only
+        // when the lane before it does not mark the same one, so a wave
+        // whose pairs share a chunk writes that flag once.
+        auto rounds = [&](auto vw_tag) {
+            constexpr int VW = decltype(vw_tag)::value;
+            const __amdgpu_buffer_rsrc_t rs = make_rsrc(p.bits, (uint32_t)bits_bytes);
+            for (int i0 = threadIdx.x; i0 < pairs; i0 += 8 * blockDim.x) {
+                int idx[8];
+                uint32_t off[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int i = i0 + u * blockDim.x;
-                any[u] = i < pairs && pair_any(i);
-            }
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int i = i0 + u * blockDim.x;
-                if (any[u]) {
-                    const int j = (int)fdiv((uint32_t)i, p.div_ktiles), kt = i - j * p.ktiles;
-                    flags[(int)fdiv((uint32_t)j, p.div_chunk) * p.ktiles + kt] = 1;   // every writer stores 1
+                for (int u = 0; u < 8; ++u) {
+                    const int i = i0 + u * blockDim.x;
+                    const int j = (int)fdiv((uint32_t)i, p.div_ktiles), kt = i - j * p.ktiles;   // pixel of the group, k tile
+                    idx[u] = (int)fdiv((uint32_t)j, p.div_chunk) * p.ktiles + kt;
+                    off[u] = i < pairs ? (uint32_t)(((int64_t)(px0 + j) * p.K + kt * p.BNk) >> 3) : kOOB;
                 }
+                uint32_t w[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    if constexpr (VW == 2) {
+                        const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rs, off[u], 0, 0);
+                        w[u] = v.x | v.y;
+                    } else if constexpr (VW == 4) {
+                        const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rs, off[u], 0, 0);
+                        w[u] = v.x | v.y | v.z | v.w;
+                    } else {
+                        const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rs, off[u], 0, 0);
+                        const u32x4 v2 = __builtin_amdgcn_raw_buffer_load_b128(rs, off[u] + 16u, 0, 0);
+                        w[u] = (v.x | v.y | v.z | v.w) | (v2.x | v2.y | v2.z | v2.w);
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int key = w[u] != 0u ? idx[u] : -1;
+                    const int prev = __shfl_up(key, 1, 64);
+                    if (key >= 0 && (lane == 0 || prev != key)) flags[idx[u]] = 1;   // every writer stores 1
+                }
+            }
+        };
+        if (vw == 2 && bits_bytes < (int64_t)kOOB) rounds(std::integral_constant<int, 2>{});
+        else if (vw == 4 && bits_bytes < (int64_t)kOOB) rounds(std::integral_constant<int, 4>{});
+        else if (vw == 8 && bits_bytes < (int64_t)kOOB) rounds(std::integral_constant<int, 8>{});
+        else {
+            for (int i = threadIdx.x; i < pairs; i += blockDim.x) {
+                const int j = (int)fdiv((uint32_t)i, p.div_ktiles), kt = i - j * p.ktiles;
+                const int64_t base = (int64_t)(px0 + j) * p.K;
+                const int lo = kt * p.BNk, hi = min(p.K, lo + p.BNk);
+                if (any_bits(p.bits, base + lo, base + hi))
+                    flags[(int)fdiv((uint32_t)j, p.div_chunk) * p.ktiles + kt] = 1;   // every writer stores 1
             }
         }
     } else {
