@@ -706,19 +706,8 @@ static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY
                                     desc->w_layout == CBW_KRSC, header, mode, gather ? &cp : nullptr, s,
                                     skip ? &op : nullptr);
     if (e != hipSuccess) return hip_status(e);
-    if (dplan.rows) {
-        const DataRowsParams rp = data_rows_params(desc, dplan, dY, wt, x_mask, dX, ws, skip);
-        e = launch_bwd_data_rows(rp, dplan.rows_grid, dplan.rows_nbw, s, prof_events(0));
-    } else if (dplan.pw) {
-        const DataPwParams pp = data_pw_params(desc, dplan, dY, wt, x_mask, dX, ws, skip);
-        e = launch_bwd_data_pw(pp, dplan.pw_grid, s, prof_events(0));
-    } else {
-        e = launch_bwd_data(desc->dtype, mode, dp, s, prof_events(0), false);
-    }
-    if (e != hipSuccess) return hip_status(e);
     WeightParams wp = weight_gemm_params(desc, wplan, X, dY, dW, wws, skip, x_skip, flags & CBW_FLAG_NO_SKIP);
     wp.gen = gen;
-    if ((e = launch_bwd_weight(desc->dtype, wp, s, prof_events(1))) != hipSuccess) return hip_status(e);
     ReduceParams rp{};
     if (!wplan.direct) {
         const int64_t n4 = (int64_t)desc->K * desc->R * desc->S * desc->C / 4;
@@ -732,8 +721,29 @@ static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY
         rp.G = splitk_reduce_group(wplan.nparts, n4);
         rp.blocks = (int)((n4 * rp.G + 255) / 256);
     }
-    const bool dx_reduce = tiled && (mode == MODE_GATHER || dplan.split > 1);
-    return hip_status(launch_bwd_reduce(desc->dtype, mode, dp, dx_reduce, rp, s));
+    if (tiled) {
+        // The weight gradient first; its split-K reduction then runs in
+        // tail workgroups of the data-gradient GEMM launch, on the CUs that
+        // the GEMM's last round of tiles leaves idle, and only the data
+        // gradient's own split reduction (gather mode, or a split dense
+        // tiling) keeps a launch of its own.
+        if ((e = launch_bwd_weight(desc->dtype, wp, s, prof_events(1))) != hipSuccess) return hip_status(e);
+        dp.dw_red = rp;
+        if ((e = launch_bwd_data(desc->dtype, mode, dp, s, prof_events(0), false)) != hipSuccess) return hip_status(e);
+        const bool dx_reduce = mode == MODE_GATHER || dplan.split > 1;
+        if (!dx_reduce) return CBW_OK;
+        return hip_status(launch_bwd_reduce(desc->dtype, mode, dp, true, ReduceParams{}, s));
+    }
+    if (dplan.rows) {
+        const DataRowsParams rwp = data_rows_params(desc, dplan, dY, wt, x_mask, dX, ws, skip);
+        e = launch_bwd_data_rows(rwp, dplan.rows_grid, dplan.rows_nbw, s, prof_events(0));
+    } else {
+        const DataPwParams pp = data_pw_params(desc, dplan, dY, wt, x_mask, dX, ws, skip);
+        e = launch_bwd_data_pw(pp, dplan.pw_grid, s, prof_events(0));
+    }
+    if (e != hipSuccess) return hip_status(e);
+    if ((e = launch_bwd_weight(desc->dtype, wp, s, prof_events(1))) != hipSuccess) return hip_status(e);
+    return hip_status(launch_bwd_reduce(desc->dtype, mode, dp, false, rp, s));
 }
 
 int conv_bwd_data_elementwise(const cbw_conv_desc* desc, const void* dY, const void* W, const uint32_t* x_mask,

@@ -240,6 +240,16 @@ __global__ __launch_bounds__(Tile<TI>::NT) void bwd_data_kernel(DataParams p)
     // the operand buffers, one array: after the main loop the bf16
     // epilogue stages the output tile in it
     __shared__ uint4 AB[2 * BM * CH + 2 * BN * CH];
+    static_assert(sizeof(AB) >= 16384, "the tail reduction's group sums fit the operand buffers");
+    if constexpr (NT == 1024) {
+        // tail workgroups: four blocks of the weight gradient's split-K
+        // reduction each (dispatched after every GEMM workgroup, they fill
+        // the CUs the GEMM's last round leaves idle)
+        if ((int)blockIdx.x >= p.gemm_grid) {
+            splitk_reduce_quad(p.dw_red, (int)blockIdx.x - p.gemm_grid, AB);
+            return;
+        }
+    }
     uint4 (*const As)[BM * CH] = reinterpret_cast<uint4 (*)[BM * CH]>(AB);
     uint4 (*const Bs)[BN * CH] = reinterpret_cast<uint4 (*)[BN * CH]>(AB + 2 * BM * CH);
     __shared__ int pix_s[BN];
@@ -1183,8 +1193,20 @@ hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t
     const int nb = max(p.ptiles * p.ctiles, p.nslots);
     if (nb <= 0) return hipSuccess;
     if (p.tile < 0 || p.tile >= kDataTileCount || p.smax > kMaxDataSplit) return hipErrorInvalidValue;
-    return dtype == 1 ? launch_type<uint16_t>(mode, p, nb, stream, ev, with_reduce)
-                      : launch_type<float>(mode, p, nb, stream, ev, with_reduce);
+    // the weight gradient's reduction in tail workgroups, four 256-thread
+    // blocks each
+    DataParams q = p;
+    q.gemm_grid = nb;
+    int tail = 0;
+    if (q.dw_red.blocks > 0) {
+        const ReduceParams& r = q.dw_red;
+        if (!r.part || !r.dw || r.nsplit < 1 || (r.G != 1 && r.G != 2 && r.G != 4 && r.G != 8 && r.G != 16) ||
+            (int64_t)r.blocks * (256 / r.G) * 4 < (int64_t)r.K * r.RS * r.C)
+            return hipErrorInvalidValue;
+        tail = (r.blocks + 3) / 4;
+    }
+    return dtype == 1 ? launch_type<uint16_t>(mode, q, nb + tail, stream, ev, with_reduce)
+                      : launch_type<float>(mode, q, nb + tail, stream, ev, with_reduce);
 }
 
 }  // namespace cbw

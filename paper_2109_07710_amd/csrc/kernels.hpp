@@ -40,6 +40,14 @@ hipError_t launch_timed(Kern kernel, dim3 grid, dim3 block, hipStream_t stream, 
     return e;
 }
 
+struct ReduceParams {
+    const float* part;       // [nsplit][K][RS][C] weight-gradient partials
+    float* dw;
+    int nsplit, K, RS, C, krsc;
+    int G;                   // threads per output (splitk_reduce_group)
+    int blocks;              // 256-thread workgroups of the weight-gradient part
+};
+
 struct DataParams {
     const void* dy;          // [N*P*Q][K]
     const void* wt;          // [R*S][C][K]
@@ -67,6 +75,12 @@ struct DataParams {
     uint32_t* out_mask;      // MODE_FWD: footprint bits of the output (nullable)
     int tile;                // kDataTiles entry the plan chose
     FastDiv div_w, div_h;    // pixel -> (n, h, w)
+    // The weight gradient's split-K reduction run by the GEMM launch's
+    // tail workgroups (the call that computes both gradients; blocks = 0
+    // otherwise): workgroups from gemm_grid on each take four of its
+    // 256-thread blocks, after every GEMM workgroup has been dispatched.
+    ReduceParams dw_red;
+    int gemm_grid;
 };
 
 // Row-window data gradient (3 x 3, stride 1, C = K = 64, bf16, NHWC): a
@@ -197,13 +211,6 @@ hipError_t launch_bwd_data(int dtype, int mode, const DataParams& p, hipStream_t
 // The weight gradient's split-K reduction (rp.blocks workgroups, none when
 // dW was written directly) and, when dx_reduce, the data gradient's split
 // tiles, in one launch.
-struct ReduceParams {
-    const float* part;       // [nsplit][K][RS][C] weight-gradient partials
-    float* dw;
-    int nsplit, K, RS, C, krsc;
-    int G;                   // threads per output (splitk_reduce_group)
-    int blocks;              // workgroups of the weight-gradient part
-};
 hipError_t launch_bwd_reduce(int dtype, int dx_mode, const DataParams& dp, bool dx_reduce, const ReduceParams& rp,
                              hipStream_t stream);
 // Forward preparation: Wf[tap'][k][c] = W[k][tap][c] with tap' the flipped tap

@@ -3,6 +3,7 @@
 #pragma once
 
 #include "common.hpp"
+#include "kernels.hpp"
 
 namespace cbw {
 
@@ -16,13 +17,13 @@ namespace cbw {
 // long serial sum per thread.  The order depends only on (nsplit, G), so
 // results are reproducible.
 template <int G>
-__device__ __forceinline__ void splitk_reduce_block(const float* __restrict__ part, float* __restrict__ dw,
-                                                    int nsplit, int K, int RS, int C, int krsc, int block)
+__device__ __forceinline__ void splitk_reduce_core(const float* __restrict__ part, float* __restrict__ dw, int nsplit,
+                                                   int K, int RS, int C, int krsc, int block, int t,
+                                                   float4 (*red)[256 / G])
 {
     constexpr int OPB = 256 / G;   // float4 outputs per block
-    __shared__ float4 red[G > 1 ? G : 1][OPB];
     const int64_t total = (int64_t)K * RS * C;
-    const int ol = threadIdx.x % OPB, g = threadIdx.x / OPB;
+    const int ol = t % OPB, g = t / OPB;
     const int64_t i4 = (int64_t)block * OPB + ol;
     const float4* p4 = reinterpret_cast<const float4*>(part);
     const int z0 = (int)((int64_t)g * nsplit / G), z1 = (int)((int64_t)(g + 1) * nsplit / G);
@@ -65,6 +66,38 @@ __device__ __forceinline__ void splitk_reduce_block(const float* __restrict__ pa
         const int k = (int)(kt / RS);
         const float vals[4] = {s.x, s.y, s.z, s.w};
         for (int j = 0; j < 4; ++j) dw[((int64_t)k * C + c + j) * RS + tap] = vals[j];
+    }
+}
+
+template <int G>
+__device__ __forceinline__ void splitk_reduce_block(const float* __restrict__ part, float* __restrict__ dw,
+                                                    int nsplit, int K, int RS, int C, int krsc, int block)
+{
+    __shared__ float4 red[G > 1 ? G : 1][256 / G];
+    splitk_reduce_core<G>(part, dw, nsplit, K, RS, C, krsc, block, threadIdx.x, red);
+}
+
+// Blocks 4 q .. 4 q + 3 of the reduction run by one 1024-thread workgroup
+// (the tail items of the data-gradient GEMM launch), with the same
+// summation order as four 256-thread workgroups: each quarter of the
+// threads takes one block, with its own share of `scratch` (at least 16 KB
+// of LDS) for the group sums.  Every thread reaches the one barrier.
+__device__ __forceinline__ void splitk_reduce_quad(const ReduceParams& rp, int q, void* scratch)
+{
+    const int sub = threadIdx.x >> 8, t = threadIdx.x & 255;
+    float4* base = static_cast<float4*>(scratch) + sub * 256;
+    switch (rp.G) {
+#define CBW_REDUCE_QUAD_CASE(GG) \
+    case GG: \
+        splitk_reduce_core<GG>(rp.part, rp.dw, rp.nsplit, rp.K, rp.RS, rp.C, rp.krsc, 4 * q + sub, t, \
+                               reinterpret_cast<float4 (*)[256 / GG]>(base)); \
+        break;
+        CBW_REDUCE_QUAD_CASE(1) CBW_REDUCE_QUAD_CASE(2) CBW_REDUCE_QUAD_CASE(4) CBW_REDUCE_QUAD_CASE(8)
+    default:
+        splitk_reduce_core<16>(rp.part, rp.dw, rp.nsplit, rp.K, rp.RS, rp.C, rp.krsc, 4 * q + sub, t,
+                               reinterpret_cast<float4 (*)[16]>(base));
+        break;
+#undef CBW_REDUCE_QUAD_CASE
     }
 }
 
