@@ -236,10 +236,13 @@ int conv_bwd_weight_sparse_x(const cbw_conv_desc* desc, const void* X, const voi
  *     set conv_bwd_weight_sparse_x(desc, X, dY, x_mask, dy_mask, ...).
  * Values are those of the separate calls (bitwise, unless a reduction is
  * split differently).  The integer work of both gradients (filter
- * transform, compaction counts, dY block occupancy) shares one launch and
- * their split reductions share one, so with NHWC tensors the call always
- * takes four launches, skipping or not; the skipping and the
- * CBW_FLAG_NO_SKIP calls therefore differ only in the kernels' own work.
+ * transform, compaction counts, dY block occupancy) shares one launch.
+ * With the tiled data gradient the weight GEMM runs next and the data GEMM
+ * after it, its tail workgroups summing the weight gradient's split-K
+ * partials; a data gradient that may split (the skipping call decides on
+ * the device; a dense tiling split by the planner) adds its split
+ * reduction: three or four launches.  With the row-window or pointwise data
+ * gradient: the data GEMM, the weight GEMM and one reduction launch.
  * NCHW tensors are served by the two separate calls.  Arguments as in the
  * separate calls (X, dY, W, dX, dW and the footprints 16-byte aligned);
  * dX = NULL computes the weight gradient alone (a first layer, whose input

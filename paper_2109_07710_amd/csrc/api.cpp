@@ -651,9 +651,12 @@ static int run_weight(const cbw_conv_desc* desc, const void* X, const void* dY, 
     return CBW_OK;
 }
 
-// Both gradients of one layer.  NHWC: four launches whatever is skipped --
-// one preparation (filter transform, compaction counts, dY occupancy), the
-// two GEMMs, one reduction (both split reductions).  NCHW: the two
+// Both gradients of one layer.  NHWC: one preparation launch (filter
+// transform, compaction counts, dY occupancy), then with the tiled data
+// gradient the weight GEMM, the data GEMM (the weight gradient's split-K
+// reduction in its tail workgroups) and, when the data gradient may split,
+// its split reduction; with the row-window or pointwise data gradient the
+// data GEMM, the weight GEMM and one reduction launch.  NCHW: the two
 // separate calls on the two parts of the workspace.
 static int run_bwd_both(const cbw_conv_desc* desc, const void* X, const void* dY, const void* W,
                         const uint32_t* x_mask, const uint32_t* dy_mask, void* dX, float* dW, void* ws,

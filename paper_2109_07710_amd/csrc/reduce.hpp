@@ -1,5 +1,6 @@
 // Split-K reduction of the weight gradient (device body, shared by its own
-// launch and the combined reduction launch of both gradients).
+// launch, the combined reduction launch and the tail workgroups of the
+// data-gradient GEMM launch).
 #pragma once
 
 #include "common.hpp"
