@@ -30,14 +30,17 @@ __device__ __forceinline__ void splitk_reduce_core(const float* __restrict__ par
     const int z0 = (int)((int64_t)g * nsplit / G), z1 = (int)((int64_t)(g + 1) * nsplit / G);
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
     if (i4 * 4 < total) {
-        // the loads of four splits are issued before they are added, in order
-        for (int zb = z0; zb < z1; zb += 4) {
-            float4 v[4];
+        // the loads of up to sixteen splits are issued before any is added
+        // (one round trip for the usual 4 to 16 splits per thread: the sum
+        // is a chain of load latencies otherwise), then added in order
+        constexpr int NL = 16;
+        for (int zb = z0; zb < z1; zb += NL) {
+            float4 v[NL];
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < NL; ++u)
                 v[u] = zb + u < z1 ? p4[(int64_t)(zb + u) * (total / 4) + i4] : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < NL; ++u) {
                 if (zb + u >= z1) break;
                 if (zb + u == z0) s = v[u];
                 else { s.x += v[u].x; s.y += v[u].y; s.z += v[u].z; s.w += v[u].w; }
