@@ -2,7 +2,8 @@
 layer: against the separate calls it stands for (bitwise where their
 reductions are grouped alike) and against the fp64 oracle, for skipping,
 non-skipping and dense data gradients, layers whose data-gradient reduction
-is split, X-block skipping, fp32, KCRS filters and NCHW tensors.  Every test
+is split, X-block skipping, fp32, KCRS filters and NCHW tensors, and the
+weight gradient's dead-block flag over a workspace shared by calls.  Every test
 prints its case before the first GPU call."""
 import numpy as np
 import pytest
@@ -164,3 +165,59 @@ def test_weight_gradient_alone():
     cb.conv_bwd_weight_sparse(desc, d["x"], d["dy"], dym, dw2, cb.workspace(desc, cb.CBW_OP_BWD_WEIGHT), 0)
     torch.cuda.synchronize()
     assert torch.equal(dw, dw2)
+
+
+@pytest.mark.parametrize("layer", ["tiled", "rows"])
+def test_weight_dead_block_flag_sequence_shared_workspace(layer):
+    """One workspace over weight-gradient calls whose dY alternates between
+    every block live and whole images of zeros, starting from a zeroed and
+    from a 0xff-filled workspace, through conv_bwd_weight_sparse and
+    conv_bwd_sparse: each call's dW and skip counts equal those of the same
+    call on a fresh workspace, whatever dead-block flag the previous call
+    (or the fill) left in the header.  The skipping GEMM takes the unskipped
+    ranges unless the occupancy pass of the same call stored its number."""
+    spec = wl.config2(N=3, H=14)[0] if layer == "tiled" else wl.config3(N=3, H=14)[1]
+    _case("dW dead-block flag sequence %s %s N=%d C=%d K=%d %dx%d" % (layer, spec.name, spec.N, spec.C, spec.K,
+                                                                   spec.H, spec.W))
+    t = wl.draw(spec)
+    d = to_dev(t)
+    desc = desc_of(spec)
+    dy_live = d["dy"].clone()
+    dy_live[dy_live == 0] = 0.5          # every dY entry non-zero: no dead block
+    dy_dead = d["dy"].clone()
+    dy_dead[1] = 0                       # image 1 entirely zero: its blocks are dead
+    xm = torch.zeros(max(cb.cbw_mask_words(desc), 1), dtype=torch.int32, device="cuda")
+    cb.cbw_relu_mask_pack(desc, d["x"], xm)
+
+    def dym_of(dy):
+        m = torch.zeros(max(cb.cbw_dy_mask_words(desc), 1), dtype=torch.int32, device="cuda")
+        cb.cbw_nonzero_mask_pack(desc.dtype, dy.numel(), dy, m)
+        return m
+
+    def run(dy, ws, both):
+        dw = torch.full((spec.K, spec.R, spec.S, spec.C), 7.0, dtype=torch.float32, device="cuda")
+        if both:
+            dx = torch.empty_like(d["x"])
+            cb.conv_bwd_sparse(desc, d["x"], dy, d["w"], xm, dym_of(dy), dx, dw, ws, 0)
+            st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_BOTH, ws)
+        else:
+            cb.conv_bwd_weight_sparse(desc, d["x"], dy, dym_of(dy), dw, ws, 0)
+            st = cb.cbw_read_stats(desc, cb.CBW_OP_BWD_WEIGHT, ws)
+        torch.cuda.synchronize()
+        return dw, st.blocks_skipped, st.blocks_total
+
+    for both in (False, True):
+        op = cb.CBW_OP_BWD_BOTH if both else cb.CBW_OP_BWD_WEIGHT
+        fresh = {}
+        for name, dy in (("live", dy_live), ("dead", dy_dead)):
+            fresh[name] = run(dy, cb.workspace(desc, op, "cuda").zero_(), both)
+        assert fresh["live"][1] == 0
+        assert fresh["dead"][1] > 0
+        for fill in (0, 255):
+            ws = cb.workspace(desc, op, "cuda")
+            ws.fill_(fill)
+            for i, name in enumerate(("live", "dead", "live", "dead", "dead", "live")):
+                dw, skipped, total = run(dy_live if name == "live" else dy_dead, ws, both)
+                ref, ref_skipped, ref_total = fresh[name]
+                assert torch.equal(dw, ref), (both, fill, i, name)
+                assert (skipped, total) == (ref_skipped, ref_total), (both, fill, i, name)
