@@ -76,6 +76,13 @@ CASES = [
     ("config4 channel-shared d=0.2, X blocks skipped",
      lambda: wl.config4(0.2, "channel_shared", N=8)[0], cb.CBW_FLAG_SKIP_X_BLOCKS, True, True, "krsc", "nhwc"),
     ("config2 reduced, KCRS filters", lambda: wl.config2(N=1, H=20)[0], 0, True, True, "kcrs", "nhwc"),
+    # the weight gradient's reduction in the data GEMM's tail workgroups with
+    # 16 threads per output (row-window dW, 224 splits), and with a data
+    # gradient whose dense tiling is split (its own reduction launch)
+    ("VGG conv2_2 at 28x28, tail reduction", lambda: wl.config5(N=32, scale=4)[3], 0, True, True, "krsc", "nhwc"),
+    ("VGG conv5_2, split data gradient", lambda: wl.config5(N=8)[11], 0, True, True, "krsc", "nhwc"),
+    ("VGG conv5_2, split data gradient, no skip", lambda: wl.config5(N=8)[11], cb.CBW_FLAG_NO_SKIP, True, False,
+     "kcrs", "nhwc"),
     ("config2 reduced, NCHW", lambda: wl.config2(N=1, H=20)[0], 0, True, True, "krsc", "nchw"),
 ]
 
