@@ -963,6 +963,11 @@ __device__ __forceinline__ void data_reduce_block(const DataParams& p, int block
         if (r >= nrows || c >= p.C) continue;
         // (a fully live group's list is 0, 1, 2, ... and is not stored)
         const int pix = nrows < p.npix ? p.lists[(int64_t)ctile * p.npix + r] : r;
+        const int64_t o = (int64_t)pix * p.C + c;
+        // the footprint word goes out with the partials, not after their sum
+        // (a second round trip per vector otherwise)
+        uint32_t mword = 0u;
+        if constexpr (MODE == MODE_SELECT || MODE == MODE_GATHER) mword = p.mask[o >> 5];
         // every split's partial is loaded before any is added (latency, not
         // bandwidth, bounds a serial chain of loads); the sum runs in split order
         const float* __restrict__ base = p.partial + ((int64_t)tile * nsplit * BN + pr) * BM + cl;
@@ -974,7 +979,6 @@ __device__ __forceinline__ void data_reduce_block(const DataParams& p, int block
 #pragma unroll
         for (int zz = 1; zz < kMaxDataSplit; ++zz)
             if (zz < nsplit) s += pv[zz];
-        const int64_t o = (int64_t)pix * p.C + c;
         if constexpr (MODE == MODE_FWD) {
             // ReLU, rounding and footprint bits as in the GEMM's forward epilogue
             // (the footprint words were cleared by the preparation kernel)
@@ -996,7 +1000,7 @@ __device__ __forceinline__ void data_reduce_block(const DataParams& p, int block
             continue;
         }
         uint32_t keep = 0xfu;
-        if (MODE != MODE_DENSE) keep = (p.mask[o >> 5] >> (o & 31)) & 0xfu;
+        if (MODE != MODE_DENSE) keep = (mword >> (o & 31)) & 0xfu;
         if constexpr (sizeof(T) == 2) {
             uint32_t h0 = (keep & 1u) ? f32_to_bf16_rne(s.x) : 0u;
             uint32_t h1 = (keep & 2u) ? f32_to_bf16_rne(s.y) : 0u;
